@@ -1,0 +1,229 @@
+"""Python bindings of the CPU oracle (``rcref.c``) for RcLLM's selective prefill.
+
+TEST INFRASTRUCTURE ONLY: the test suite, the smoke check and the benchmark's
+CPU-baseline leg are its only users. The GPU path never imports it.
+
+Every function takes and returns host numpy arrays. Storage dtypes: ``float32``
+arrays are fp32 tensors; ``uint16`` arrays hold bf16 bit patterns. Layouts are
+the token-major layouts documented in ``rcref.c``.
+
+Paper passages followed (arXiv 2605.07443):
+  * Sec. III-C.3, end-to-end prefill pipeline: (i) assembly, (ii) alignment by
+    RoPE rotation, (iii) heavy-hitter update;
+  * Sec. III-C.2b and Eq. (3): importance score (deviation term, K only,
+    lambda = 1) and the heavy-hitter top-k;
+  * Eq. (1): scaled dot-product attention, causal, grouped-query;
+  * Sec. IV-A: Full-Recompute baseline (every row recomputed).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+SRC_PATH = os.path.join(_HERE, "rcref.c")
+LIB_PATH = os.path.join(_HERE, "librcref.so")
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile ``rcref.c`` with gcc: no FMA contraction, no fast-math, OpenMP."""
+    if not force and os.path.exists(LIB_PATH):
+        return LIB_PATH
+    tmp = LIB_PATH + ".tmp"
+    cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off",
+           "-fno-fast-math", "-Wall", "-Wextra", "-o", tmp, SRC_PATH, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, LIB_PATH)
+    return LIB_PATH
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            build()
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, f64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_double
+        L.rcref_rope_table.argtypes = [i32, i32, f64, vp, vp]
+        L.rcref_assemble.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, vp, i32, vp, i32,
+                                     vp, vp, vp, vp, vp, vp]
+        L.rcref_rerope.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, vp]
+        L.rcref_deviation.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp]
+        L.rcref_topk.argtypes = [i32, i32, vp, i32, i32, vp, vp]
+        L.rcref_topk.restype = i32
+        L.rcref_patch.argtypes = [i32, i32, i32, i32, i32, vp, i32, vp, i32, vp, vp, vp, vp]
+        L.rcref_attention.argtypes = [i32, i32, i32, i32, i32, i32, vp, vp, i32, vp, vp, f64, vp]
+        L.rcref_selective_prefill.argtypes = [i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, i32,
+                                              vp, i32, i32, vp, vp, vp, vp, vp, f64,
+                                              vp, vp, vp, vp, vp]
+        L.rcref_selective_prefill.restype = i32
+        _lib = L
+    return _lib
+
+
+def _dt(a: np.ndarray) -> int:
+    if a.dtype == np.float32:
+        return 0
+    if a.dtype == np.uint16:
+        return 1
+    raise TypeError(f"storage dtype must be float32 or uint16 (bf16 bits), got {a.dtype}")
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dtype=None):
+    return np.ascontiguousarray(a if dtype is None else a.astype(dtype, copy=False))
+
+
+def fresh_count(segs: np.ndarray) -> np.ndarray:
+    """Per-request number of fresh positions (segments with pool < 0)."""
+    segs = np.asarray(segs)
+    return np.where(segs[..., 2] < 0, segs[..., 1], 0).sum(axis=1)
+
+
+def rope_table(max_pos: int, D: int, base: float):
+    cos = np.empty((max_pos, D // 2), np.float32)
+    sin = np.empty((max_pos, D // 2), np.float32)
+    lib().rcref_rope_table(max_pos, D, float(base), _p(cos), _p(sin))
+    return cos, sin
+
+
+def assemble(k_fresh, v_fresh, pools, segs, cos=None, sin=None):
+    """Gather (and, given tables, re-align) K/V rows. ``pools`` is a list of
+    (pool_k, pool_v) arrays of shape [num_blocks, block_len, Hkv, D]."""
+    k_fresh, v_fresh = _c(k_fresh), _c(v_fresh)
+    B, N, Hkv, D = k_fresh.shape
+    dt = _dt(k_fresh)
+    segs = _c(segs, np.int32)
+    S = segs.shape[1]
+    pools = [(_c(pk), _c(pv)) for pk, pv in pools]
+    n = len(pools)
+    pk_arr = (ctypes.c_void_p * max(n, 1))(*[pk.ctypes.data for pk, _ in pools])
+    pv_arr = (ctypes.c_void_p * max(n, 1))(*[pv.ctypes.data for _, pv in pools])
+    nb = np.array([pk.shape[0] for pk, _ in pools] or [0], np.int32)
+    bl = np.array([pk.shape[1] for pk, _ in pools] or [0], np.int32)
+    k_asm = np.empty_like(k_fresh)
+    v_asm = np.empty_like(v_fresh)
+    cos = None if cos is None else _c(cos, np.float32)
+    sin = None if sin is None else _c(sin, np.float32)
+    lib().rcref_assemble(B, N, Hkv, D, dt, pk_arr, pv_arr, _p(nb), _p(bl), n, _p(segs), S,
+                         _p(k_fresh), _p(v_fresh), _p(cos), _p(sin), _p(k_asm), _p(v_asm))
+    return k_asm, v_asm
+
+
+def rerope(k, delta, cos, sin):
+    """Return a copy of K [B,N,Hkv,D] with row (b,i) rotated by delta[b,i]."""
+    out = np.array(k, copy=True)
+    B, N, Hkv, D = out.shape
+    delta = _c(delta, np.int32)
+    lib().rcref_rerope(B, N, Hkv, D, _dt(out), _p(out), _p(delta), _p(_c(cos, np.float32)),
+                       _p(_c(sin, np.float32)))
+    return out
+
+
+def deviation(k_fresh, k_asm):
+    k_fresh, k_asm = _c(k_fresh), _c(k_asm)
+    B, N, Hkv, D = k_fresh.shape
+    scores = np.empty((B, N), np.float32)
+    lib().rcref_deviation(B, N, Hkv, D, _dt(k_fresh), _p(k_fresh), _p(k_asm), _p(scores))
+    return scores
+
+
+def topk(segs, N: int, k: int, scores):
+    segs = _c(segs, np.int32)
+    B, S = segs.shape[:2]
+    F = int(fresh_count(segs)[0])
+    scores = _c(scores, np.float32)
+    rows = np.empty((B, F + k), np.int32)
+    st = lib().rcref_topk(B, N, _p(segs), S, int(k), _p(scores), _p(rows))
+    if st != 0:
+        raise ValueError("k exceeds the cached positions of a request, or fresh counts differ")
+    return rows
+
+
+def patch(segs, rows, k_fresh, v_fresh, k_asm, v_asm):
+    segs = _c(segs, np.int32)
+    rows = _c(rows, np.int32)
+    k_fresh, v_fresh = _c(k_fresh), _c(v_fresh)
+    k_out = np.array(k_asm, copy=True)
+    v_out = np.array(v_asm, copy=True)
+    B, N, Hkv, D = k_fresh.shape
+    lib().rcref_patch(B, N, Hkv, D, _dt(k_fresh), _p(segs), segs.shape[1], _p(rows),
+                      rows.shape[1], _p(k_fresh), _p(v_fresh), _p(k_out), _p(v_out))
+    return k_out, v_out
+
+
+def attention(q, k, v, rows=None, scale=None):
+    """Causal GQA attention of the listed rows (all rows if ``rows`` is None)."""
+    q, k, v = _c(q), _c(k), _c(v)
+    B, N, Hq, D = q.shape
+    Hkv = k.shape[2]
+    if scale is None:
+        scale = 1.0 / np.sqrt(D)
+    if rows is not None:
+        rows = _c(rows, np.int32)
+        R = rows.shape[1]
+    else:
+        R = N
+    out = np.empty((B, R, Hq, D), q.dtype)
+    lib().rcref_attention(B, N, Hq, Hkv, D, _dt(q), _p(q), _p(rows), R, _p(k), _p(v),
+                          float(scale), _p(out))
+    return out
+
+
+def selective_prefill(q, k_fresh, v_fresh, pools, segs, k: int, cos, sin, scale=None):
+    """The whole pipeline; returns a dict with every intermediate."""
+    q, k_fresh, v_fresh = _c(q), _c(k_fresh), _c(v_fresh)
+    B, N, Hq, D = q.shape
+    Hkv = k_fresh.shape[2]
+    dt = _dt(q)
+    segs = _c(segs, np.int32)
+    S = segs.shape[1]
+    F = int(fresh_count(segs)[0])
+    R = F + int(k)
+    pools = [(_c(pk), _c(pv)) for pk, pv in pools]
+    n = len(pools)
+    pk_arr = (ctypes.c_void_p * max(n, 1))(*[pk.ctypes.data for pk, _ in pools])
+    pv_arr = (ctypes.c_void_p * max(n, 1))(*[pv.ctypes.data for _, pv in pools])
+    nb = np.array([pk.shape[0] for pk, _ in pools] or [0], np.int32)
+    bl = np.array([pk.shape[1] for pk, _ in pools] or [0], np.int32)
+    if scale is None:
+        scale = 1.0 / np.sqrt(D)
+    k_asm = np.empty_like(k_fresh)
+    v_asm = np.empty_like(v_fresh)
+    scores = np.empty((B, N), np.float32)
+    rows = np.empty((B, R), np.int32)
+    out = np.empty((B, R, Hq, D), q.dtype)
+    st = lib().rcref_selective_prefill(
+        B, N, Hq, Hkv, D, dt, pk_arr, pv_arr, _p(nb), _p(bl), n, _p(segs), S, int(k), _p(q),
+        _p(k_fresh), _p(v_fresh), _p(_c(cos, np.float32)), _p(_c(sin, np.float32)),
+        float(scale), _p(k_asm), _p(v_asm), _p(scores), _p(rows), _p(out))
+    if st != 0:
+        raise ValueError("k exceeds the cached positions of a request, or fresh counts differ")
+    return dict(k_asm=k_asm, v_asm=v_asm, scores=scores, rows=rows, out=out)
+
+
+# ---------------------------------------------------------------------------
+# bf16 conversions for host-side comparisons (exact widening; RNE narrowing)
+# ---------------------------------------------------------------------------
+
+def bf16_to_f32(a: np.ndarray) -> np.ndarray:
+    return (np.asarray(a, np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def f32_to_bf16(a: np.ndarray) -> np.ndarray:
+    u = np.ascontiguousarray(a, np.float32).view(np.uint32).astype(np.uint64)
+    nan = (u & 0x7FFFFFFF) > 0x7F800000
+    r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+    return np.where(nan, ((u >> 16) | 0x40).astype(np.uint16), r)
+
+
+def as_f32(a: np.ndarray) -> np.ndarray:
+    return bf16_to_f32(a) if a.dtype == np.uint16 else np.asarray(a, np.float32)

@@ -1,0 +1,456 @@
+"""Pins for the CPU oracle: each test checks the oracle against something other
+than itself -- a hand-derived worked example, a closed form, a library routine,
+an invariant the paper's method must satisfy, or a brute force on tiny inputs.
+
+Paper: arXiv 2605.07443 (RcLLM). Steps: Sec. III-C.3 (assembly, alignment,
+correction), Sec. III-C.2b / Eq. (3) (selection), Eq. (1) (attention).
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2605_07443_amd import inputs
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "worked_examples.json")
+H = inputs.to_host_bits
+
+
+@pytest.fixture(scope="module")
+def golden():
+    with open(GOLDEN) as f:
+        return json.load(f)
+
+
+def _segs(B, spans):
+    """spans: list of (dst, len, pool, block) shared by all requests."""
+    s = np.array(spans, np.int32)[None].repeat(B, axis=0)
+    return np.ascontiguousarray(s)
+
+
+# ---------------------------------------------------------------------------
+# worked examples (tests/golden/worked_examples.json)
+# ---------------------------------------------------------------------------
+
+def test_worked_rerope(golden):
+    for case in golden["rerope"]:
+        D, d = case["D"], case["delta"]
+        cos, sin = O.rope_table(abs(d) + 1, D, case["base"])
+        k = np.array(case["k_in"], np.float32).reshape(1, 1, 1, D)
+        out = O.rerope(k, np.array([[d]], np.int32), cos, sin).reshape(-1)
+        np.testing.assert_allclose(out, case["k_out"], rtol=0, atol=3e-7, err_msg=case["derivation"])
+
+
+def test_worked_deviation(golden):
+    c = golden["deviation"]
+    kf = np.array(c["k_fresh"], np.float32)[None]
+    kc = np.array(c["k_cached"], np.float32)[None]
+    np.testing.assert_array_equal(O.deviation(kf, kc)[0], np.array(c["d"], np.float32))
+
+
+def test_worked_topk(golden):
+    c = golden["topk"]
+    f0, f1 = c["fresh"]
+    segs = _segs(1, [(f0, f1 - f0, -1, 0), (f1, c["N"] - f1, 0, 0)])
+    scores = np.array([c["scores"]], np.float32)
+    for case in c["cases"]:
+        rows = O.topk(segs, c["N"], case["k"], scores)
+        assert rows[0].tolist() == case["rows"], c["derivation"]
+
+
+def test_worked_attention(golden):
+    c = golden["attention"]
+    N, D = c["N"], c["D"]
+    q = np.array(c["q"], np.float32).reshape(1, N, 1, D)
+    k = np.array(c["k"], np.float32).reshape(1, N, 1, D)
+    v = np.array(c["v"], np.float32).reshape(1, N, 1, D)
+    out = O.attention(q, k, v, scale=1.0 / math.sqrt(D)).reshape(N, D)
+    np.testing.assert_allclose(out, np.array(c["out"]), rtol=0, atol=2e-6, err_msg=c["derivation"])
+
+
+# ---------------------------------------------------------------------------
+# RoPE table and re-alignment (Sec. III-C.3 step ii)
+# ---------------------------------------------------------------------------
+
+def test_rope_table_closed_forms():
+    D, P = 64, 300
+    cos, sin = O.rope_table(P, D, 10000.0)
+    assert np.all(cos[0] == 1.0) and np.all(sin[0] == 0.0)
+    # j = 0 has frequency 1: the angle is the position itself
+    p = np.arange(P)
+    np.testing.assert_array_equal(cos[:, 0], np.cos(p.astype(np.float64)).astype(np.float32))
+    # every entry is the unit phasor exp(i * p * base^(-2j/D)) rounded once to fp32
+    z = np.power(np.exp(1j * np.power(10000.0, -2.0 * np.arange(D // 2) / D)), p[:, None])
+    np.testing.assert_allclose(cos, z.real, rtol=0, atol=1e-7)
+    np.testing.assert_allclose(sin, z.imag, rtol=0, atol=1e-7)
+
+
+def _rand_k(shape, seed, dtype):
+    x = np.random.default_rng(seed).standard_normal(shape).astype(np.float32)
+    return O.f32_to_bf16(x) if dtype == "bf16" else x
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_rerope_matches_complex_rotation(dtype):
+    """Rotate-half RoPE is multiplication of (x_j + i y_j) by exp(i delta theta_j)."""
+    B, N, Hkv, D, base = 2, 17, 3, 64, 10000.0
+    k = _rand_k((B, N, Hkv, D), 1, dtype)
+    delta = np.random.default_rng(2).integers(-400, 400, (B, N)).astype(np.int32)
+    cos, sin = O.rope_table(401, D, base)
+    out = O.as_f32(O.rerope(k, delta, cos, sin)).astype(np.float64)
+    kin = O.as_f32(k).astype(np.float64)
+    theta = np.power(base, -2.0 * np.arange(D // 2) / D)
+    z = (kin[..., :D // 2] + 1j * kin[..., D // 2:]) * np.exp(1j * delta[..., None, None] * theta)
+    want = np.concatenate([z.real, z.imag], axis=-1)
+    tol = 3e-6 if dtype == "f32" else 4e-2
+    np.testing.assert_allclose(out, want, rtol=0, atol=tol)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_rerope_composition_inverse_norm(dtype):
+    """R(b) R(a) = R(a+b); R(-a) R(a) = I; each rotated pair keeps its norm."""
+    B, N, Hkv, D = 1, 64, 2, 128
+    k = _rand_k((B, N, Hkv, D), 3, dtype)
+    rng = np.random.default_rng(4)
+    a = rng.integers(0, 3000, (B, N)).astype(np.int32)
+    b = rng.integers(0, 3000, (B, N)).astype(np.int32)
+    cos, sin = O.rope_table(6001, D, 500000.0)
+    two = O.as_f32(O.rerope(O.rerope(k, a, cos, sin), b, cos, sin))
+    one = O.as_f32(O.rerope(k, a + b, cos, sin))
+    back = O.as_f32(O.rerope(O.rerope(k, a, cos, sin), -a, cos, sin))
+    kin = O.as_f32(k)
+    tol = 2e-6 if dtype == "f32" else 5e-2
+    np.testing.assert_allclose(two, one, rtol=0, atol=tol)
+    np.testing.assert_allclose(back, kin, rtol=0, atol=tol)
+    rot = O.as_f32(O.rerope(k, a, cos, sin))
+    n0 = kin[..., :D // 2] ** 2 + kin[..., D // 2:] ** 2
+    n1 = rot[..., :D // 2] ** 2 + rot[..., D // 2:] ** 2
+    np.testing.assert_allclose(n1, n0, rtol=1e-5 if dtype == "f32" else 2e-2, atol=1e-6)
+
+
+def test_rerope_delta_zero_is_bit_identity():
+    k = _rand_k((2, 9, 2, 64), 5, "bf16")
+    cos, sin = O.rope_table(10, 64, 10000.0)
+    out = O.rerope(k, np.zeros((2, 9), np.int32), cos, sin)
+    np.testing.assert_array_equal(out, k)
+
+
+# ---------------------------------------------------------------------------
+# Assembly (Sec. III-C.3 step i)
+# ---------------------------------------------------------------------------
+
+def test_gather_rows_are_the_named_pool_rows():
+    """Every assembled row equals the pool row its segment names, at block offset
+    i - dst_start (or the fresh row), exactly; the table is unused without RoPE."""
+    B, Hkv, D = 2, 2, 8
+    pools = []
+    off = 0.0
+    for (P, L) in [(3, 5), (4, 3)]:
+        n = P * L * Hkv * D
+        pk = (off + np.arange(n, dtype=np.float32)).reshape(P, L, Hkv, D)
+        pv = -pk
+        off += n
+        pools.append((pk, pv))
+    spans = [[(0, 2, -1, 0), (2, 5, 0, 2), (7, 3, 1, 1), (10, 3, -1, 0), (13, 3, 1, 3)],
+             [(0, 2, -1, 0), (2, 5, 0, 0), (7, 3, 1, 3), (10, 3, -1, 0), (13, 3, 1, 3)]]
+    segs = np.array(spans, np.int32)
+    N = 16
+    kf = np.random.default_rng(0).standard_normal((B, N, Hkv, D)).astype(np.float32) + 1e6
+    vf = kf + 1.0
+    ka, va = O.assemble(kf, vf, pools, segs)
+    for b in range(B):
+        for (dst, ln, p, blk) in spans[b]:
+            for t in range(ln):
+                if p < 0:
+                    assert np.array_equal(ka[b, dst + t], kf[b, dst + t])
+                    assert np.array_equal(va[b, dst + t], vf[b, dst + t])
+                else:
+                    assert np.array_equal(ka[b, dst + t], pools[p][0][blk, t])
+                    assert np.array_equal(va[b, dst + t], pools[p][1][blk, t])
+
+
+@pytest.mark.parametrize("name", ["tiny-f32-gqa", "tiny-bf16"])
+def test_zero_noise_realigned_keys_equal_fresh_keys(name):
+    """With no cache noise, re-aligning a block stored at local positions to its
+    absolute position reproduces the freshly computed key (up to rounding): this
+    ties delta = dst_start and the rotation direction to the model's own RoPE."""
+    cfg = inputs.TEST_CONFIGS[name]
+    w = inputs.make(cfg, 11, sigma=0.0)
+    cos, sin = O.rope_table(cfg.N, cfg.D, cfg.rope_base)
+    pools = [(H(a), H(b)) for a, b in w.pools]
+    ka, va = O.assemble(H(w.k_fresh), H(w.v_fresh), pools, w.segs.numpy(), cos, sin)
+    tol = 2e-6 if cfg.dtype == "f32" else 3e-2
+    np.testing.assert_allclose(O.as_f32(ka), O.as_f32(H(w.k_fresh)), rtol=0, atol=tol)
+    np.testing.assert_array_equal(va, H(w.v_fresh))
+    # without re-alignment the cached keys are far off
+    ka0, _ = O.assemble(H(w.k_fresh), H(w.v_fresh), pools, w.segs.numpy())
+    assert np.abs(O.as_f32(ka0) - O.as_f32(H(w.k_fresh))).max() > 0.5
+
+
+# ---------------------------------------------------------------------------
+# Deviation score (Eq. (3), K term)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("sigma", [0.05, 0.1])
+def test_deviation_matches_half_normal_closed_form(sigma):
+    """Cache noise eps ~ N(0, sigma^2) on every key entry (rotation keeps it iid),
+    so d = sum of Hkv*D half-normals: E[d] = Hkv*D*sigma*sqrt(2/pi),
+    sd(d) = sigma*sqrt(Hkv*D*(1 - 2/pi)). A dropped head, an L2 norm or an added
+    V term moves the mean by many standard errors."""
+    cfg = inputs.CONFIGS[1]
+    w = inputs.make(cfg, 1000, sigma=sigma)
+    cos, sin = O.rope_table(cfg.N, cfg.D, cfg.rope_base)
+    pools = [(H(a), H(b)) for a, b in w.pools]
+    ka, _ = O.assemble(H(w.k_fresh), H(w.v_fresh), pools, w.segs.numpy(), cos, sin)
+    d = O.deviation(H(w.k_fresh), ka)[0]
+    reused = d[cfg.F:]
+    n = cfg.Hkv * cfg.D
+    mean = n * sigma * math.sqrt(2 / math.pi)
+    sd = sigma * math.sqrt(n * (1 - 2 / math.pi))
+    assert abs(reused.mean() - mean) < 5 * sd / math.sqrt(reused.size)
+    assert 0.7 * sd < reused.std() < 1.3 * sd
+    assert np.all(d[:cfg.F] == 0.0)
+
+
+# ---------------------------------------------------------------------------
+# Heavy-hitter top-k (Sec. III-C.2b)
+# ---------------------------------------------------------------------------
+
+def _brute_rows(segs_b, N, k, scores_b):
+    fresh = set()
+    for dst, ln, p, _ in segs_b:
+        if p < 0:
+            fresh.update(range(dst, dst + ln))
+    cand = sorted((i for i in range(N) if i not in fresh), key=lambda i: (-scores_b[i], i))
+    return sorted(fresh | set(cand[:k]))
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_topk_matches_full_sort_with_ties(seed):
+    rng = np.random.default_rng(seed)
+    B, N = 3, int(rng.integers(20, 90))
+    cut = sorted(rng.choice(np.arange(1, N), 4, replace=False).tolist())
+    bounds = [0] + cut + [N]
+    spans = []
+    for s in range(len(bounds) - 1):
+        p = -1 if s in (0, 2) else 0
+        spans.append((bounds[s], bounds[s + 1] - bounds[s], p, 0))
+    segs = _segs(B, spans)
+    scores = rng.integers(0, 6, (B, N)).astype(np.float32)
+    n_r = sum(ln for _, ln, p, _ in spans if p >= 0)
+    for k in sorted({0, 1, n_r // 3, n_r // 2, n_r}):
+        rows = O.topk(segs, N, k, scores)
+        for b in range(B):
+            assert rows[b].tolist() == _brute_rows(spans, N, k, scores[b])
+
+
+def test_topk_special_values_and_errors():
+    N = 8
+    segs = _segs(1, [(0, 1, -1, 0), (1, 7, 0, 0)])
+    s = np.array([[0.0, 1.0, np.nan, 3.0, np.inf, 3.0, -2.0, 0.5]], np.float32)
+    assert O.topk(segs, N, 1, s)[0].tolist() == [0, 2]          # NaN ranks first
+    assert O.topk(segs, N, 2, s)[0].tolist() == [0, 2, 4]       # then +inf
+    assert O.topk(segs, N, 4, s)[0].tolist() == [0, 2, 3, 4, 5]  # tie 3.0: both
+    assert O.topk(segs, N, 3, s)[0].tolist() == [0, 2, 3, 4]    # tie: lower index
+    eq = np.full((1, N), 7.0, np.float32)
+    assert O.topk(segs, N, 3, eq)[0].tolist() == [0, 1, 2, 3]   # all equal: lowest
+    with pytest.raises(ValueError):
+        O.topk(segs, N, 8, s)
+
+
+def test_planted_heavy_hitters_are_selected():
+    cfg = inputs.CONFIGS[1]
+    w = inputs.make(cfg, 7, planted=10)
+    cos, sin = O.rope_table(cfg.N, cfg.D, cfg.rope_base)
+    pools = [(H(a), H(b)) for a, b in w.pools]
+    r = O.selective_prefill(H(w.q), H(w.k_fresh), H(w.v_fresh), pools, w.segs.numpy(), cfg.k,
+                            cos, sin)
+    assert set(w.planted[0].tolist()) <= set(r["rows"][0].tolist())
+
+
+# ---------------------------------------------------------------------------
+# Attention (Eq. (1)), causal GQA
+# ---------------------------------------------------------------------------
+
+def _sdpa64(q, k, v):
+    """torch CPU scaled_dot_product_attention in fp64 (a library routine)."""
+    qt = torch.from_numpy(O.as_f32(q).astype(np.float64)).permute(0, 2, 1, 3)
+    kt = torch.from_numpy(O.as_f32(k).astype(np.float64)).permute(0, 2, 1, 3)
+    vt = torch.from_numpy(O.as_f32(v).astype(np.float64)).permute(0, 2, 1, 3)
+    g = qt.shape[1] // kt.shape[1]
+    kt = kt.repeat_interleave(g, dim=1)
+    vt = vt.repeat_interleave(g, dim=1)
+    o = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, is_causal=True)
+    return o.permute(0, 2, 1, 3).numpy()
+
+
+@pytest.mark.parametrize("dtype,Hq,Hkv,D", [("f32", 8, 2, 64), ("bf16", 4, 4, 128),
+                                            ("bf16", 8, 1, 64)])
+def test_full_prefill_matches_torch_sdpa(dtype, Hq, Hkv, D):
+    B, N = 2, 37
+    q = _rand_k((B, N, Hq, D), 1, dtype)
+    k = _rand_k((B, N, Hkv, D), 2, dtype)
+    v = _rand_k((B, N, Hkv, D), 3, dtype)
+    out = O.as_f32(O.attention(q, k, v))
+    want = _sdpa64(q, k, v)
+    tol = 1e-6 if dtype == "f32" else 8e-3
+    np.testing.assert_allclose(out, want, rtol=0, atol=tol)
+
+
+def test_attention_closed_forms():
+    B, N, Hq, Hkv, D = 1, 12, 2, 1, 64
+    rng = np.random.default_rng(9)
+    q = rng.standard_normal((B, N, Hq, D)).astype(np.float32)
+    k = rng.standard_normal((B, N, Hkv, D)).astype(np.float32)
+    v = rng.standard_normal((B, N, Hkv, D)).astype(np.float32)
+    out = O.attention(q, k, v)
+    for h in range(Hq):
+        np.testing.assert_array_equal(out[0, 0, h], v[0, 0, 0])   # row 0 sees only key 0
+    out0 = O.attention(np.zeros_like(q), k, v)                      # Q = 0: uniform weights
+    prefix_mean = np.cumsum(v[0, :, 0].astype(np.float64), 0) / np.arange(1, N + 1)[:, None]
+    np.testing.assert_allclose(out0[0, :, 0], prefix_mean, rtol=0, atol=1e-6)
+
+
+def test_attention_matrix_bruteforce_and_row_subset():
+    """Materialised-mask matrix form on a tiny shape; listed rows equal the same
+    rows of the all-rows call."""
+    B, N, Hq, Hkv, D = 2, 23, 6, 3, 64
+    rng = np.random.default_rng(10)
+    q = rng.standard_normal((B, N, Hq, D)).astype(np.float32)
+    k = rng.standard_normal((B, N, Hkv, D)).astype(np.float32)
+    v = rng.standard_normal((B, N, Hkv, D)).astype(np.float32)
+    full = O.attention(q, k, v)
+    g = Hq // Hkv
+    mask = np.tril(np.ones((N, N), bool))
+    for b in range(B):
+        for h in range(Hq):
+            s = (q[b, :, h].astype(np.float64) @ k[b, :, h // g].astype(np.float64).T) / math.sqrt(D)
+            s = np.where(mask, s, -np.inf)
+            p = np.exp(s - s.max(1, keepdims=True))
+            p /= p.sum(1, keepdims=True)
+            np.testing.assert_allclose(full[b, :, h], p @ v[b, :, h // g], rtol=0, atol=1e-6)
+    rows = np.array([[0, 3, 4, 22], [1, 2, 10, 21]], np.int32)
+    sub = O.attention(q, k, v, rows=rows)
+    for b in range(B):
+        np.testing.assert_array_equal(sub[b], full[b, rows[b]])
+
+
+# ---------------------------------------------------------------------------
+# Whole-pipeline invariants
+# ---------------------------------------------------------------------------
+
+def _run(cfg, w, k):
+    cos, sin = O.rope_table(cfg.N, cfg.D, cfg.rope_base)
+    pools = [(H(a), H(b)) for a, b in w.pools]
+    return O.selective_prefill(H(w.q), H(w.k_fresh), H(w.v_fresh), pools, w.segs.numpy(), k,
+                               cos, sin)
+
+
+@pytest.mark.parametrize("name", ["tiny-f32-gqa", "tiny-bf16", "miss-bf16"])
+def test_full_ratio_equals_full_prefill(name):
+    """Selecting every cached token patches every row with fresh KV and
+    recomputes every row: the output is the full prefill, bit for bit."""
+    cfg = inputs.TEST_CONFIGS[name]
+    w = inputs.make(cfg, 21)
+    r = _run(cfg, w, cfg.n_reused)
+    full = O.attention(H(w.q), H(w.k_fresh), H(w.v_fresh))
+    assert r["rows"].shape[1] == cfg.N
+    np.testing.assert_array_equal(r["out"], full)
+    np.testing.assert_array_equal(r["k_asm"], H(w.k_fresh))
+
+
+@pytest.mark.parametrize("name", ["tiny-f32-gqa", "tiny-bf16"])
+@pytest.mark.parametrize("pct", [0, 15, 50])
+def test_zero_perturbation_equals_full_prefill(name, pct):
+    cfg = inputs.TEST_CONFIGS[name]
+    w = inputs.make(cfg, 22, sigma=0.0)
+    r = _run(cfg, w, cfg.k_for(pct))
+    full = O.attention(H(w.q), H(w.k_fresh), H(w.v_fresh))
+    tol = 1e-5 if cfg.dtype == "f32" else 2e-2
+    for b in range(cfg.B):
+        np.testing.assert_allclose(O.as_f32(r["out"][b]), O.as_f32(full[b, r["rows"][b]]),
+                                   rtol=0, atol=tol)
+
+
+@pytest.mark.parametrize("name", ["tiny-bf16", "miss-bf16"])
+def test_noise_changes_output_but_not_instruction_rows(name):
+    """Instruction rows attend only fresh keys, so they equal the full prefill at
+    any noise level; cached rows that were not recomputed do see the noise."""
+    cfg = inputs.TEST_CONFIGS[name]
+    w = inputs.make(cfg, 23, sigma=0.2)
+    r = _run(cfg, w, cfg.k)
+    full = O.attention(H(w.q), H(w.k_fresh), H(w.v_fresh))
+    for b in range(cfg.B):
+        rows = r["rows"][b]
+        first = rows < cfg.F
+        np.testing.assert_array_equal(r["out"][b][first], full[b, rows[first]])
+        later = O.as_f32(r["out"][b][~first]) - O.as_f32(full[b, rows[~first]])
+        assert np.abs(later).max() > 1e-2
+
+
+def test_cache_miss_segments_are_always_recomputed():
+    cfg = inputs.TEST_CONFIGS["miss-bf16"]
+    w = inputs.make(cfg, 24)
+    r = _run(cfg, w, 0)
+    fresh = [i for dst, ln, p, _ in w.segs[0].tolist() if p < 0 for i in range(dst, dst + ln)]
+    assert r["rows"][0].tolist() == fresh
+    assert len(fresh) == cfg.n_fresh
+
+
+# ---------------------------------------------------------------------------
+# Input generator
+# ---------------------------------------------------------------------------
+
+def test_generator_is_deterministic_and_tiles_the_prompt():
+    cfg = inputs.TEST_CONFIGS["ragged-bf16"]
+    a = inputs.make(cfg, 5)
+    b = inputs.make(cfg, 5)
+    c = inputs.make(cfg, 6)
+    assert torch.equal(a.q, b.q) and torch.equal(a.k_fresh, b.k_fresh)
+    assert torch.equal(a.pools[1][0], b.pools[1][0]) and torch.equal(a.segs, b.segs)
+    assert not torch.equal(a.q, c.q)
+    for req in a.segs.tolist():
+        pos = 0
+        for dst, ln, p, blk in req:
+            assert dst == pos and ln > 0
+            pos += ln
+        assert pos == cfg.N
+
+
+@pytest.mark.parametrize("cid", [2, 3, 4, 5])
+def test_item_ids_follow_the_config(cid):
+    cfg = inputs.CONFIGS[cid]
+    hist, items = inputs.sample_ids(cfg, 1000 * cid)
+    assert items.shape == (cfg.B, cfg.n_items)
+    assert int(items.min()) >= 0 and int(items.max()) < cfg.item_pool
+    assert int(hist.max()) < cfg.hist_pool
+    for row in items:
+        assert row.unique().numel() == cfg.n_items        # no repeats within a request
+
+
+def test_zipf_ids_are_heavy_tailed():
+    cfg = inputs.CONFIGS[2].with_(B=400)
+    _, items = inputs.sample_ids(cfg, 3)
+    counts = torch.bincount(items.reshape(-1), minlength=cfg.item_pool).sort(descending=True).values
+    c = counts.numpy().astype(np.float64)
+    # Zipf(1.1) over 10,000 ids, 20 draws per request: the hottest id is in
+    # nearly every request, most ids never appear, and the rank-frequency curve
+    # falls with a log-log slope near -1.1 (flattened a little by drawing
+    # without replacement)
+    assert c[0] > 0.9 * cfg.B
+    assert (c == 0).mean() > 0.5
+    r = np.arange(20, 300)
+    slope = np.polyfit(np.log(r + 1.0), np.log(c[r] + 0.5), 1)[0]
+    assert -1.4 < slope < -0.7
+
+
+def test_config_sizes():
+    c = inputs.CONFIGS
+    assert [c[i].N for i in range(1, 6)] == [416, 3008, 8160, 4096, 2080]
+    assert [c[i].k for i in range(1, 6)] == [58, 442, 810, 600, 308]
+    assert [c[i].R for i in range(1, 6)] == [90, 506, 874, 696, 340]
+    assert [c[4].k_for(p) for p in inputs.SWEEP_PCTS] == [0, 200, 400, 600, 1000, 2000, 4000]

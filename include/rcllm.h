@@ -1,0 +1,195 @@
+/*
+ * rcllm.h -- C ABI of the MI355X (gfx950) selective-prefill library for one
+ * transformer attention layer, after RcLLM (arXiv 2605.07443).
+ *
+ * The paper reuses precomputed KV blocks of user histories and candidate
+ * items at arbitrary, non-prefix positions of a recommendation prompt and
+ * repairs the reuse by recomputing only a few "heavy hitter" tokens
+ * (Sec. III-C.2 and III-C.3). One layer of that prefill is four calls:
+ *
+ *   rc_kv_assemble          (i)  assembly: gather K/V rows of pool blocks
+ *                                through a segment table, with
+ *                           (ii) alignment: RoPE re-rotation of cached keys
+ *                                fused into the gather
+ *   rc_rerope               (ii) alignment as a standalone in-place pass
+ *   rc_select_tokens        Eq. (3) deviation score (K only, lambda = 1),
+ *                           deterministic top-k of cached tokens, and
+ *                           (iii) correction: heavy hitters get fresh K/V
+ *   rc_selective_attention  Eq. (1) causal GQA attention for the selected
+ *                           query rows over the whole assembled context,
+ *                           or for every row (Full-Recompute, Sec. IV-A)
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Pointers are DEVICE pointers unless marked (host). The caller owns every
+ *   buffer; the library never allocates, frees or keeps a pointer after the
+ *   call returns. Buffers must stay valid until `stream` has run the work.
+ * - Every compute call only enqueues kernels on `stream` (no host
+ *   synchronisation). A NULL stream is the default stream.
+ * - Layouts are row-major and token-major:
+ *     pool K/V        [num_blocks, block_len, Hkv, D]
+ *     fresh/assembled [B, N, Hkv, D]
+ *     Q               [B, N, Hq, D]
+ *     out             [B, R, Hq, D]
+ *     segments        [B, S] of rc_segment
+ *     RoPE tables     [max_pos, D/2] fp32 (cos and sin of pos * base^(-2j/D))
+ * - Storage dtype is fp32 or bf16 (rc_dtype) for every K/V/Q/out tensor of a
+ *   call; arithmetic is fp32 (attention accumulates in fp32; bf16 products on
+ *   the matrix cores).
+ * - Return value: RC_OK, or a negative rc_status. On failure nothing was
+ *   enqueued and rc_last_error() holds a description.
+ * - Supported: D in {64, 128}; Hq % Hkv == 0; for bf16 attention the group
+ *   size Hq/Hkv must divide 128; N <= 16384 for rc_select_tokens; S <= 1024
+ *   segments per request; at most 8 pools.
+ * - Device-side contents (segment tables, block ids, row lists, deltas) cannot
+ *   be checked without a synchronisation. Kernels bound-check them and skip
+ *   what is out of range (the affected outputs are then unspecified) instead
+ *   of reading or writing out of bounds.
+ */
+#ifndef RCLLM_H
+#define RCLLM_H
+
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  RC_OK = 0,
+  RC_ERR_INVALID_ARG = -1, /* NULL pointer, inconsistent sizes, bad value */
+  RC_ERR_UNSUPPORTED = -2, /* valid request outside the supported shapes */
+  RC_ERR_HIP = -3          /* a HIP launch failed; see rc_last_error() */
+} rc_status;
+
+typedef enum { RC_F32 = 0, RC_BF16 = 1 } rc_dtype;
+
+/* Problem shape of one call (host struct). */
+typedef struct {
+  int32_t B;     /* requests in the batch */
+  int32_t N;     /* prompt length (tokens) of every request */
+  int32_t Hq;    /* query heads */
+  int32_t Hkv;   /* KV heads; q-head h uses KV head h / (Hq / Hkv) */
+  int32_t D;     /* head dimension */
+  int32_t dtype; /* rc_dtype */
+} rc_shape;
+
+/* One precomputed KV pool (host struct, device pointers): the offline item or
+ * history KV store of Sec. III-B. Block b, token t, head h, dim d lives at
+ * ((b * block_len + t) * Hkv + h) * D + d. Keys are stored rotated to their
+ * block-local positions 0 .. block_len-1. */
+typedef struct {
+  const void* k;
+  const void* v;
+  int32_t num_blocks;
+  int32_t block_len;
+} rc_pool;
+
+/* One segment of a request's prompt (the logical-to-physical block mapping of
+ * Sec. III-A): positions [dst_start, dst_start + len) come from block `block`
+ * of pool `pool`, token offsets 0 .. len-1, or, when pool < 0, are fresh
+ * (instruction tokens and cache misses, always recomputed, Sec. III-C.2a).
+ * A request's segments must tile [0, N) in increasing dst_start order. */
+typedef struct {
+  int32_t dst_start;
+  int32_t len;
+  int32_t pool;
+  int32_t block;
+} rc_segment;
+
+/* RoPE tables (host). Writes cos/sin of pos * base^(-2j/D) for pos in
+ * [0, max_pos), j in [0, D/2), evaluated in fp64 and rounded once to fp32,
+ * into host arrays cos_out/sin_out of max_pos * D/2 floats each. The caller
+ * uploads them. Rotary encoding as cited for the alignment step
+ * (Sec. III-C.3 (ii)); the pair (j, j + D/2) of each head is rotated
+ * ("rotate-half" convention). Errors: INVALID_ARG for NULL outputs,
+ * max_pos < 1, odd or non-positive D, base <= 0. */
+int rc_rope_table(int32_t max_pos, int32_t D, double base, float* cos_out, float* sin_out);
+
+/* Assembly and fused alignment (Sec. III-C.3 (i) and (ii); zero-copy block
+ * retrieval of Sec. III-C.2a served from an HBM-resident pool).
+ * For request b and position i in segment s = segs[b*S + s]:
+ *   fresh segment: K_asm[b,i] = K_fresh[b,i], V_asm[b,i] = V_fresh[b,i]
+ *   pool segment:  K_asm[b,i] = R(dst_start) pool.k[block][i - dst_start]
+ *                  V_asm[b,i] = pool.v[block][i - dst_start]
+ * where R(delta) rotates every head's pairs (j, j+D/2) by delta * theta_j:
+ *   x' = x*c - y*s, y' = x*s + y*c in fp32 (no fused multiply-add), c and s
+ *   from row delta of the tables, then rounded to the storage dtype (RNE).
+ * Blocks are stored at block-local positions from 0, so the rotation that
+ * moves a cached row to its absolute position is delta = dst_start.
+ * rope_cos/rope_sin NULL: plain gather, no rotation (then max_pos is
+ * ignored); otherwise both must be given with max_pos >= N.
+ * pools: host array of n_pools rc_pool (1..8). segs: device [B, S].
+ * k_fresh/v_fresh: device [B, N, Hkv, D]; only rows of fresh segments are
+ * read. k_asm/v_asm: device [B, N, Hkv, D] outputs (must not alias inputs).
+ * Errors: INVALID_ARG for NULL pointers, bad shape, bad pool, S < 1 or
+ * max_pos < N with tables given; UNSUPPORTED for D, dtype, S > 1024. */
+int rc_kv_assemble(const rc_shape* shape, const rc_pool* pools, int32_t n_pools,
+                   const rc_segment* segs, int32_t S, const void* k_fresh, const void* v_fresh,
+                   const float* rope_cos, const float* rope_sin, int32_t max_pos, void* k_asm,
+                   void* v_asm, hipStream_t stream);
+
+/* Standalone alignment (Sec. III-C.3 (ii)), in place: K[b,i] <- R(delta[b,i])
+ * K[b,i] with the same fp32 operation order as rc_kv_assemble; a negative
+ * delta uses cos(|delta|) and -sin(|delta|); rows with delta == 0 are not
+ * touched. k: device [B, N, Hkv, D]; delta: device [B, N] int32 with
+ * |delta| < max_pos (rows outside are skipped); tables device
+ * [max_pos, D/2]. Hq in the shape is unused (may be any value >= 1).
+ * Errors: INVALID_ARG for NULL pointers, bad shape, max_pos < 1;
+ * UNSUPPORTED for D or dtype. */
+int rc_rerope(const rc_shape* shape, void* k, const int32_t* delta, const float* rope_cos,
+              const float* rope_sin, int32_t max_pos, hipStream_t stream);
+
+/* Heavy-hitter selection and correction (Sec. III-C.2b, Eq. (3) with M = K
+ * and lambda = 1; Sec. III-C.3 (iii)).
+ * 1. Score: unless scores_in is given, d[b,i] = sum over h < Hkv, j < D of
+ *    |K_fresh[b,i,h,j] - K_asm[b,i,h,j]|, accumulated in fp32, for every
+ *    position (0 at fresh positions, whose assembled rows are fresh), written
+ *    to scores_out [B, N] (required when scores_in is NULL; optional else).
+ * 2. Select: the k cached positions (not in a fresh segment) with the largest
+ *    score -- NaN above +inf above every finite value, ties to the lower
+ *    position -- together with the n_fresh fresh positions, in ascending
+ *    order: rows [B, n_fresh + k] int32. Bit-exact for given scores.
+ * 3. Patch (patch != 0): K_asm/V_asm rows of the k selected cached positions
+ *    are overwritten with K_fresh/V_fresh rows.
+ * n_fresh must equal the number of fresh positions of every request
+ * (requests whose table disagrees get a truncated or padded row list).
+ * Requires 0 <= k <= N - n_fresh; rows may be NULL when n_fresh + k == 0.
+ * Hq in the shape is unused.
+ * Errors: INVALID_ARG for NULL pointers, bad shape, k or n_fresh out of
+ * range; UNSUPPORTED for D, dtype, N > 16384, S > 1024. */
+int rc_select_tokens(const rc_shape* shape, const rc_segment* segs, int32_t S, int32_t n_fresh,
+                     int32_t k, const void* k_fresh, const void* v_fresh, void* k_asm,
+                     void* v_asm, const float* scores_in, float* scores_out, int32_t* rows,
+                     int32_t patch, hipStream_t stream);
+
+/* Selective attention (Eq. (1); Sec. III-C.2b: exact attention recomputed for
+ * the selected rows over the full assembled context).
+ * For r < R, p = rows[b*R + r] (or p = r when rows is NULL: Full-Recompute
+ * over all N rows, then R must equal N), q-head h, KV head g = h/(Hq/Hkv):
+ *   out[b,r,h] = sum_{j<=p} softmax_j(scale * Q[b,p,h] . K[b,j,g]) V[b,j,g]
+ * fp32 accumulation and online softmax; bf16 inputs use the matrix cores.
+ * q: [B, N, Hq, D]; rows: [B, R] int32, ascending within a request (any
+ * order is correct, ascending is fastest); k, v: [B, N, Hkv, D];
+ * out: [B, R, Hq, D]. Rows outside [0, N) are clamped into range.
+ * Errors: INVALID_ARG for NULL pointers, bad shape, R < 0, R != N without
+ * rows, non-finite or non-positive scale; UNSUPPORTED for D, dtype, or a
+ * bf16 group size that does not divide 128. R == 0 enqueues nothing (out may
+ * then be NULL). */
+int rc_selective_attention(const rc_shape* shape, const void* q, const int32_t* rows, int32_t R,
+                           const void* k, const void* v, float scale, void* out,
+                           hipStream_t stream);
+
+/* Static description of a status code. */
+const char* rc_status_string(int status);
+
+/* Description of the last failure on the calling thread ("" if none). */
+const char* rc_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RCLLM_H */

@@ -1,0 +1,270 @@
+// Assembly of cached KV blocks with fused RoPE re-alignment, and the
+// standalone re-alignment pass (RcLLM, arXiv 2605.07443, Sec. III-C.3 steps
+// (i) and (ii); logical-to-physical block mapping of Sec. III-A).
+//
+// Both are HBM-bound copies. A workgroup of 256 threads owns TOK consecutive
+// positions of one request (TOK * row = 32 KiB of K+V reads): it first
+// resolves each position to its source row (binary search of the request's
+// segment table staged in LDS), then streams 16-byte units. A key unit pairs
+// element block [j, j+E) of a head with [j+D/2, j+D/2+E) so the rotation of
+// the pairs (j, j+D/2) happens in registers between the load and the store.
+#include "rc_common.h"
+
+namespace rc {
+namespace {
+
+using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;
+constexpr int kMaxTok = 256;      // positions per workgroup (small rows)
+constexpr int kRowBytesPerWg = 32768;
+
+// Rotate E = 16/ES elements of the first half (a) and second half (b) of a
+// head by the angle whose cos/sin are c[0..E), s[0..E).
+//   a' = a*c - b*s,  b' = a*s + b*c   (fp32, no contraction), then RNE.
+template <int ES>
+__device__ __forceinline__ void rotate_unit(u32x4& a, u32x4& b, const float* c, const float* s) {
+#pragma clang fp contract(off)
+  if constexpr (ES == 4) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float x = __uint_as_float(a[e]);
+      const float y = __uint_as_float(b[e]);
+      const float xc = x * c[e], ys = y * s[e], xs = x * s[e], yc = y * c[e];
+      a[e] = __float_as_uint(xc - ys);
+      b[e] = __float_as_uint(xs + yc);
+    }
+  } else {
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      uint32_t na = 0, nb = 0;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int e = 2 * w + h;
+        const float x = bf16_to_f32(static_cast<uint16_t>(a[w] >> (16 * h)));
+        const float y = bf16_to_f32(static_cast<uint16_t>(b[w] >> (16 * h)));
+        const float xc = x * c[e], ys = y * s[e], xs = x * s[e], yc = y * c[e];
+        na |= static_cast<uint32_t>(f32_to_bf16(xc - ys)) << (16 * h);
+        nb |= static_cast<uint32_t>(f32_to_bf16(xs + yc)) << (16 * h);
+      }
+      a[w] = na;
+      b[w] = nb;
+    }
+  }
+}
+
+// ASSEMBLE: source rows come from the segment table (pool block or fresh
+// row), V is copied as well, delta = dst_start for pool rows when tables are
+// given. REROPE (in place): source = destination = k, delta from the array.
+template <int ES, bool ASSEMBLE>
+__global__ __launch_bounds__(kThreads) void kv_rows_kernel(
+    PoolArgs pools, const int4* __restrict__ segs, int S, int N, int tok_per_wg, int row_units,
+    int head_units, const char* __restrict__ k_fresh, const char* __restrict__ v_fresh,
+    const int32_t* __restrict__ delta_arr, const float* __restrict__ cos_t,
+    const float* __restrict__ sin_t, int max_pos, int half, char* __restrict__ k_out,
+    char* __restrict__ v_out) {
+  constexpr int E = 16 / ES;  // elements per 16-byte unit
+  __shared__ int4 s_segs[ASSEMBLE ? kMaxSegments : 1];
+  __shared__ const char* s_srck[kMaxTok];
+  __shared__ const char* s_srcv[kMaxTok];
+  __shared__ int s_delta[kMaxTok];
+
+  const int b = blockIdx.y;
+  const int i0 = blockIdx.x * tok_per_wg;
+  const int tok_cnt = min(tok_per_wg, N - i0);
+  const size_t row_bytes = static_cast<size_t>(row_units) * 16;
+
+  if constexpr (ASSEMBLE) {
+    for (int s = threadIdx.x; s < S; s += kThreads) s_segs[s] = segs[static_cast<size_t>(b) * S + s];
+    __syncthreads();
+  }
+  for (int t = threadIdx.x; t < tok_cnt; t += kThreads) {
+    const int i = i0 + t;
+    const size_t row_off = (static_cast<size_t>(b) * N + i) * row_bytes;
+    const char* sk = nullptr;
+    const char* sv = nullptr;
+    int d = 0;
+    if constexpr (ASSEMBLE) {
+      const int s = find_segment(s_segs, S, i);
+      if (s >= 0) {
+        const int4 g = s_segs[s];
+        if (g.z < 0) {
+          sk = k_fresh + row_off;
+          sv = v_fresh + row_off;
+        } else if (g.z < pools.n && g.w >= 0 && g.w < pools.num_blocks[g.z] && g.x >= 0 &&
+                   i - g.x < pools.block_len[g.z]) {
+          const size_t src = (static_cast<size_t>(g.w) * pools.block_len[g.z] + (i - g.x)) * row_bytes;
+          sk = pools.k[g.z] + src;
+          sv = pools.v[g.z] + src;
+          if (cos_t != nullptr && g.x < max_pos) d = g.x;
+        }
+      }
+    } else {
+      const int dd = delta_arr[static_cast<size_t>(b) * N + i];
+      if (dd != 0 && dd < max_pos && -dd < max_pos) {
+        sk = k_out + row_off;
+        d = dd;
+      }
+    }
+    s_srck[t] = sk;
+    s_srcv[t] = sv;
+    s_delta[t] = d;
+  }
+  __syncthreads();
+
+  // ---- keys: pairs of units (first half, second half of a head)
+  const int pairs_per_row = row_units / 2;
+  const int half_units = head_units / 2;
+  const int k_items = tok_cnt * pairs_per_row;
+  for (int base = threadIdx.x; base < k_items; base += kThreads * 4) {
+    u32x4 ua[4], ub[4];
+    int tok[4], unit[4];
+    bool ok[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int idx = base + u * kThreads;
+      ok[u] = idx < k_items;
+      tok[u] = ok[u] ? idx / pairs_per_row : 0;
+      const int pr = idx - tok[u] * pairs_per_row;
+      const int head = pr / half_units;
+      unit[u] = head * head_units + (pr - head * half_units);
+      ok[u] = ok[u] && s_srck[tok[u]] != nullptr;
+      if (ok[u]) {
+        const u32x4* src = reinterpret_cast<const u32x4*>(s_srck[tok[u]]);
+        if constexpr (ASSEMBLE) {
+          ua[u] = __builtin_nontemporal_load(src + unit[u]);
+          ub[u] = __builtin_nontemporal_load(src + unit[u] + half_units);
+        } else {
+          ua[u] = src[unit[u]];
+          ub[u] = src[unit[u] + half_units];
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (!ok[u]) continue;
+      const int d = s_delta[tok[u]];
+      if (d != 0) {
+        const int a = d < 0 ? -d : d;
+        const int j0 = (unit[u] % head_units) * E;  // element offset in the half
+        float c[E], s[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          c[e] = cos_t[static_cast<size_t>(a) * half + j0 + e];
+          const float sv = sin_t[static_cast<size_t>(a) * half + j0 + e];
+          s[e] = d < 0 ? -sv : sv;
+        }
+        rotate_unit<ES>(ua[u], ub[u], c, s);
+      }
+      u32x4* dst = reinterpret_cast<u32x4*>(k_out + (static_cast<size_t>(b) * N + i0 + tok[u]) * row_bytes);
+      dst[unit[u]] = ua[u];
+      dst[unit[u] + half_units] = ub[u];
+    }
+  }
+
+  if constexpr (ASSEMBLE) {
+    // ---- values: plain 16-byte copies
+    const int v_items = tok_cnt * row_units;
+    for (int base = threadIdx.x; base < v_items; base += kThreads * 8) {
+      u32x4 val[8];
+      int tok[8], unit[8];
+      bool ok[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int idx = base + u * kThreads;
+        ok[u] = idx < v_items;
+        tok[u] = ok[u] ? idx / row_units : 0;
+        unit[u] = idx - tok[u] * row_units;
+        ok[u] = ok[u] && s_srcv[tok[u]] != nullptr;
+        if (ok[u]) val[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(s_srcv[tok[u]]) + unit[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (!ok[u]) continue;
+        u32x4* dst = reinterpret_cast<u32x4*>(v_out + (static_cast<size_t>(b) * N + i0 + tok[u]) * row_bytes);
+        dst[unit[u]] = val[u];
+      }
+    }
+  }
+}
+
+int tokens_per_wg(int row_bytes) {
+  int t = kRowBytesPerWg / row_bytes;
+  return t < 1 ? 1 : (t > kMaxTok ? kMaxTok : t);
+}
+
+template <bool ASSEMBLE>
+int launch_rows(const rc_shape* s, const PoolArgs& pools, const int4* segs, int S,
+                const void* k_fresh, const void* v_fresh, const int32_t* delta, const float* cos_t,
+                const float* sin_t, int max_pos, void* k_out, void* v_out, hipStream_t stream) {
+  const int es = elem_size(s->dtype);
+  const int row_bytes = s->Hkv * s->D * es;
+  const int row_units = row_bytes / 16;
+  const int head_units = s->D * es / 16;
+  const int tok = tokens_per_wg(ASSEMBLE ? row_bytes : row_bytes / 2);
+  dim3 grid((s->N + tok - 1) / tok, s->B);
+  if (grid.y > 65535) return fail(RC_ERR_UNSUPPORTED, "B=%d exceeds 65535", s->B);
+  auto args = [&](auto kern) {
+    hipLaunchKernelGGL(kern, grid, dim3(kThreads), 0, stream, pools, segs, S, s->N, tok, row_units,
+                       head_units, static_cast<const char*>(k_fresh),
+                       static_cast<const char*>(v_fresh), delta, cos_t, sin_t, max_pos, s->D / 2,
+                       static_cast<char*>(k_out), static_cast<char*>(v_out));
+  };
+  if (s->dtype == RC_BF16)
+    args(kv_rows_kernel<2, ASSEMBLE>);
+  else
+    args(kv_rows_kernel<4, ASSEMBLE>);
+  return check_launch(ASSEMBLE ? "rc_kv_assemble" : "rc_rerope");
+}
+
+}  // namespace
+}  // namespace rc
+
+extern "C" int rc_kv_assemble(const rc_shape* shape, const rc_pool* pools, int32_t n_pools,
+                              const rc_segment* segs, int32_t S, const void* k_fresh,
+                              const void* v_fresh, const float* rope_cos, const float* rope_sin,
+                              int32_t max_pos, void* k_asm, void* v_asm, hipStream_t stream) {
+  using namespace rc;
+  clear_error();
+  if (int st = check_shape(shape, false)) return st;
+  if (n_pools < 1 || n_pools > kMaxPools)
+    return fail(n_pools > kMaxPools ? RC_ERR_UNSUPPORTED : RC_ERR_INVALID_ARG,
+                "n_pools=%d (1..%d)", n_pools, kMaxPools);
+  if (!pools) return fail(RC_ERR_INVALID_ARG, "pools is NULL");
+  if (!segs || !k_fresh || !v_fresh || !k_asm || !v_asm)
+    return fail(RC_ERR_INVALID_ARG, "segs, k_fresh, v_fresh, k_asm and v_asm must be non-NULL");
+  if (S < 1) return fail(RC_ERR_INVALID_ARG, "S=%d must be >= 1", S);
+  if (S > kMaxSegments) return fail(RC_ERR_UNSUPPORTED, "S=%d exceeds %d segments", S, kMaxSegments);
+  if ((rope_cos == nullptr) != (rope_sin == nullptr))
+    return fail(RC_ERR_INVALID_ARG, "rope_cos and rope_sin must both be given or both be NULL");
+  if (rope_cos && max_pos < shape->N)
+    return fail(RC_ERR_INVALID_ARG, "max_pos=%d < N=%d", max_pos, shape->N);
+  if (k_asm == k_fresh || v_asm == v_fresh || k_asm == v_asm)
+    return fail(RC_ERR_INVALID_ARG, "outputs alias inputs");
+  PoolArgs pa{};
+  pa.n = n_pools;
+  for (int p = 0; p < n_pools; ++p) {
+    if (!pools[p].k || !pools[p].v || pools[p].num_blocks < 1 || pools[p].block_len < 1)
+      return fail(RC_ERR_INVALID_ARG, "pool %d: NULL tensor or empty shape", p);
+    pa.k[p] = static_cast<const char*>(pools[p].k);
+    pa.v[p] = static_cast<const char*>(pools[p].v);
+    pa.num_blocks[p] = pools[p].num_blocks;
+    pa.block_len[p] = pools[p].block_len;
+  }
+  return launch_rows<true>(shape, pa, reinterpret_cast<const int4*>(segs), S, k_fresh, v_fresh,
+                           nullptr, rope_cos, rope_sin, rope_cos ? max_pos : 0, k_asm, v_asm, stream);
+}
+
+extern "C" int rc_rerope(const rc_shape* shape, void* k, const int32_t* delta,
+                         const float* rope_cos, const float* rope_sin, int32_t max_pos,
+                         hipStream_t stream) {
+  using namespace rc;
+  clear_error();
+  if (int st = check_shape(shape, false)) return st;
+  if (!k || !delta || !rope_cos || !rope_sin)
+    return fail(RC_ERR_INVALID_ARG, "k, delta, rope_cos and rope_sin must be non-NULL");
+  if (max_pos < 1) return fail(RC_ERR_INVALID_ARG, "max_pos=%d must be >= 1", max_pos);
+  PoolArgs pa{};
+  return launch_rows<false>(shape, pa, nullptr, 0, nullptr, nullptr, delta, rope_cos, rope_sin,
+                            max_pos, k, nullptr, stream);
+}

@@ -1,0 +1,384 @@
+// Selective causal attention (RcLLM, arXiv 2605.07443, Sec. III-C.2b: exact
+// attention recomputed for the selected rows over the full assembled context;
+// Eq. (1) with a causal mask and grouped-query heads) and the Full-Recompute
+// baseline (every row; Sec. IV-A).
+//
+// bf16 path (matrix cores, gfx950 v_mfma_f32_16x16x32_bf16):
+//   * A workgroup owns M = 128 query vectors of one (request, KV head): BR
+//     consecutive selected rows x the G = Hq/Hkv query heads that share the KV
+//     head, so one K/V stream feeds all of them.
+//   * Each of the 4 waves owns 32 query vectors and computes S^T = K Q^T for a
+//     64-key tile (keys on the MFMA rows, queries on its columns) with Q held
+//     in registers and K read from LDS. In the output layout a lane then holds
+//     4 consecutive keys of one query column, which is also the B-operand
+//     layout of the second product O^T = V^T P^T, so P never leaves registers;
+//     V is staged transposed in LDS to serve as the A operand.
+//   * Online softmax in the log2 domain with fp32 running max and sum.
+//   * Workgroup ids are remapped so that all row tiles of one (request, KV
+//     head) run on the same XCD (ids are dealt round-robin over the 8 XCDs),
+//     sharing its L2 for the K/V stream, with the longest (latest) tiles
+//     first.
+// fp32 path: one wave per (request, row, head), fp32 FMA on the vector ALUs.
+#include <cmath>
+
+#include "rc_common.h"
+
+namespace rc {
+namespace {
+
+constexpr int kAttnThreads = 256;
+constexpr int kM = 128;  // query vectors per workgroup
+constexpr int kKT = 64;  // keys per KV tile
+constexpr int kXcds = 8;
+
+using u32x2 = uint32_t __attribute__((ext_vector_type(2)));
+using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
+
+template <int D>
+struct AttnSmem {
+  uint16_t k[kKT][D + 8];   // K tile, key-major; +16 B per row against bank conflicts
+  uint16_t vt[D][kKT + 4];  // V tile transposed, dim-major; +8 B per row
+};
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const __bf16 a = static_cast<__bf16>(lo);
+  const __bf16 b = static_cast<__bf16>(hi);
+  return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, a)) |
+         (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, b)) << 16);
+}
+
+template <int D>
+__global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)))
+void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict__ rows, int R,
+                      int N, int Hq, int Hkv, int G, int BR, const uint16_t* __restrict__ k,
+                      const uint16_t* __restrict__ v, float scale_log2e,
+                      uint16_t* __restrict__ out, int n_tiles, int total_wg, int per_xcd) {
+  constexpr int DC = D / 32;          // 32-wide d chunks (S^T reduction)
+  constexpr int DB = D / 16;          // 16-wide d blocks (O^T rows)
+  constexpr int KU = kKT * D / 8 / kAttnThreads;   // K 16-byte units per thread
+  constexpr int KPG = D / 32;         // V keys per thread (transposed staging)
+  constexpr int UPR = D / 8;          // 16-byte units per K/V head row
+  __shared__ AttnSmem<D> sm;
+  __shared__ int s_ext[4];
+
+  const int hw = blockIdx.x;
+  const int logical = (hw % kXcds) * per_xcd + hw / kXcds;
+  if (logical >= total_wg) return;
+  const int grp = logical / n_tiles;
+  const int tile = n_tiles - 1 - (logical - grp * n_tiles);
+  const int b = grp / Hkv;
+  const int g = grp - b * Hkv;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int c16 = lane & 15;
+  const int q4 = lane >> 4;
+
+  // ---- the two query vectors (S^T columns) this lane serves
+  int pos[2], head[2], row[2];
+  bool valid[2];
+  int pmax = 0, pmin = 0x7fffffff;
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb) {
+    const int m = wave * 32 + nb * 16 + c16;
+    const int hh = m / BR;
+    const int rl = m - hh * BR;
+    const int r = tile * BR + rl;
+    valid[nb] = hh < G && r < R;
+    int p = 0;
+    if (valid[nb]) {
+      p = rows ? rows[static_cast<size_t>(b) * R + r] : r;
+      p = min(max(p, 0), N - 1);
+      pmax = max(pmax, p);
+      pmin = min(pmin, p);
+    }
+    pos[nb] = p;
+    head[nb] = g * G + (hh < G ? hh : 0);
+    row[nb] = r;
+  }
+  pmax = wave_max_i(pmax);
+  const int wave_pmin = wave_min_i(pmin);
+  if (lane == 0) s_ext[wave] = pmax;
+  __syncthreads();
+  const int wg_pmax = max(max(s_ext[0], s_ext[1]), max(s_ext[2], s_ext[3]));
+  const int n_kv = wg_pmax / kKT + 1;
+
+  // ---- Q fragments (B operand of S^T = K Q^T): 8 consecutive dims per lane
+  bf16x8 qf[2][DC];
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb) {
+    const uint16_t* qrow = q + ((static_cast<size_t>(b) * N + pos[nb]) * Hq + head[nb]) * D;
+#pragma unroll
+    for (int dc = 0; dc < DC; ++dc)
+      qf[nb][dc] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(qrow + dc * 32 + q4 * 8));
+  }
+
+  // ---- K/V tile prefetch registers
+  const size_t kv_row_stride = static_cast<size_t>(Hkv) * D;   // elements between keys
+  const uint16_t* kbase = k + static_cast<size_t>(b) * N * kv_row_stride + static_cast<size_t>(g) * D;
+  const uint16_t* vbase = v + static_cast<size_t>(b) * N * kv_row_stride + static_cast<size_t>(g) * D;
+  u32x4 kreg[KU], vreg[KPG];
+  const int v_d0 = (tid % UPR) * 8;
+  const int v_k0 = (tid / UPR) * KPG;
+  auto load_tile = [&](int t) {
+    const int j0 = t * kKT;
+#pragma unroll
+    for (int i = 0; i < KU; ++i) {
+      const int u = tid + i * kAttnThreads;
+      const int key = u / UPR;
+      const int col = (u % UPR) * 8;
+      const int j = j0 + key;
+      kreg[i] = j < N ? *reinterpret_cast<const u32x4*>(kbase + j * kv_row_stride + col) : u32x4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int i = 0; i < KPG; ++i) {
+      const int j = j0 + v_k0 + i;
+      vreg[i] = j < N ? *reinterpret_cast<const u32x4*>(vbase + j * kv_row_stride + v_d0) : u32x4{0, 0, 0, 0};
+    }
+  };
+  load_tile(0);
+
+  f32x4 o[DB][2];
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) o[db][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run[2] = {-INFINITY, -INFINITY};
+  float l_run[2] = {0.f, 0.f};
+
+  for (int t = 0; t < n_kv; ++t) {
+    __syncthreads();  // every wave is done reading the previous tile
+#pragma unroll
+    for (int i = 0; i < KU; ++i) {
+      const int u = tid + i * kAttnThreads;
+      *reinterpret_cast<u32x4*>(&sm.k[u / UPR][(u % UPR) * 8]) = kreg[i];
+    }
+    // transpose V: vreg[i] holds dims v_d0..v_d0+7 of key v_k0+i
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      uint16_t h[KPG];
+#pragma unroll
+      for (int i = 0; i < KPG; ++i) h[i] = static_cast<uint16_t>(vreg[i][e >> 1] >> (16 * (e & 1)));
+      if constexpr (KPG == 4) {
+        u32x2 w = {static_cast<uint32_t>(h[0]) | (static_cast<uint32_t>(h[1]) << 16),
+                   static_cast<uint32_t>(h[2]) | (static_cast<uint32_t>(h[3]) << 16)};
+        *reinterpret_cast<u32x2*>(&sm.vt[v_d0 + e][v_k0]) = w;
+      } else {
+        *reinterpret_cast<uint32_t*>(&sm.vt[v_d0 + e][v_k0]) =
+            static_cast<uint32_t>(h[0]) | (static_cast<uint32_t>(h[1]) << 16);
+      }
+    }
+    __syncthreads();
+    if (t + 1 < n_kv) load_tile(t + 1);
+
+    // ---- S^T = K Q^T for 64 keys x 32 queries
+    f32x4 s[4][2];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      s[kb][0] = f32x4{0.f, 0.f, 0.f, 0.f};
+      s[kb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int dc = 0; dc < DC; ++dc) {
+        const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(&sm.k[kb * 16 + c16][dc * 32 + q4 * 8]));
+        s[kb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[0][dc], s[kb][0], 0, 0, 0);
+        s[kb][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[1][dc], s[kb][1], 0, 0, 0);
+      }
+    }
+
+    // ---- causal mask + online softmax (per query column)
+    const int j0 = t * kKT;
+    const bool need_mask = j0 + kKT - 1 > wave_pmin;
+    bf16x8 pb[2][2];
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float x = s[kb][nb][i] * scale_log2e;
+          if (need_mask && j0 + kb * 16 + q4 * 4 + i > pos[nb]) x = -INFINITY;
+          s[kb][nb][i] = x;
+          mx = fmaxf(mx, x);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float m_new = fmaxf(m_run[nb], mx);
+      const float m_use = m_new == -INFINITY ? 0.f : m_new;
+      const float alpha = exp2f(m_run[nb] - m_use);
+      float ls = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float p = exp2f(s[kb][nb][i] - m_use);
+          s[kb][nb][i] = p;
+          ls += p;
+        }
+      l_run[nb] = l_run[nb] * alpha + ls;
+      m_run[nb] = m_new;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) o[db][nb] *= alpha;
+#pragma unroll
+      for (int kc = 0; kc < 2; ++kc) {
+        u32x4 w = {pack_bf16x2(s[2 * kc][nb][0], s[2 * kc][nb][1]),
+                   pack_bf16x2(s[2 * kc][nb][2], s[2 * kc][nb][3]),
+                   pack_bf16x2(s[2 * kc + 1][nb][0], s[2 * kc + 1][nb][1]),
+                   pack_bf16x2(s[2 * kc + 1][nb][2], s[2 * kc + 1][nb][3])};
+        pb[kc][nb] = __builtin_bit_cast(bf16x8, w);
+      }
+    }
+
+    // ---- O^T += V^T P^T
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int kc = 0; kc < 2; ++kc) {
+        const u32x2 lo = *reinterpret_cast<const u32x2*>(&sm.vt[db * 16 + c16][kc * 32 + q4 * 4]);
+        const u32x2 hi = *reinterpret_cast<const u32x2*>(&sm.vt[db * 16 + c16][kc * 32 + 16 + q4 * 4]);
+        const bf16x8 a = __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
+        o[db][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][0], o[db][0], 0, 0, 0);
+        o[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][1], o[db][1], 0, 0, 0);
+      }
+  }
+
+  // ---- normalise and store: lane holds dims db*16 + q4*4 .. +3 of its query
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb) {
+    float l = l_run[nb];
+    l += __shfl_xor(l, 16, 64);
+    l += __shfl_xor(l, 32, 64);
+    const float inv = 1.f / l;
+    if (!valid[nb]) continue;
+    uint16_t* orow = out + ((static_cast<size_t>(b) * R + row[nb]) * Hq + head[nb]) * D;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const u32x2 w = {pack_bf16x2(o[db][nb][0] * inv, o[db][nb][1] * inv),
+                       pack_bf16x2(o[db][nb][2] * inv, o[db][nb][3] * inv)};
+      *reinterpret_cast<u32x2*>(orow + db * 16 + q4 * 4) = w;
+    }
+  }
+}
+
+// fp32: one wave per (request, row, q-head). Lanes own keys while scoring
+// (64 keys per step) and dims while accumulating P V.
+template <int D>
+__global__ __launch_bounds__(256) void attn_f32_kernel(const float* __restrict__ q,
+                                                       const int32_t* __restrict__ rows, int R,
+                                                       int N, int Hq, int Hkv,
+                                                       const float* __restrict__ k,
+                                                       const float* __restrict__ v, float scale,
+                                                       float* __restrict__ out, int64_t total) {
+  constexpr int PER = D / 64;
+  __shared__ float s_q[4][D];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int64_t w = static_cast<int64_t>(blockIdx.x) * 4 + wave;
+  const bool active = w < total;
+  const int64_t wi = active ? w : 0;
+  const int h = static_cast<int>(wi % Hq);
+  const int64_t br = wi / Hq;
+  const int r = static_cast<int>(br % R);
+  const int b = static_cast<int>(br / R);
+  int p = rows ? rows[static_cast<size_t>(b) * R + r] : r;
+  p = min(max(p, 0), N - 1);
+  const int g = h / (Hq / Hkv);
+  const float* qrow = q + ((static_cast<size_t>(b) * N + p) * Hq + h) * D;
+  for (int d = lane; d < D; d += 64) s_q[wave][d] = qrow[d];
+  __syncthreads();
+  if (!active) return;
+  const size_t kv_stride = static_cast<size_t>(Hkv) * D;
+  const float* kb = k + static_cast<size_t>(b) * N * kv_stride + static_cast<size_t>(g) * D;
+  const float* vb = v + static_cast<size_t>(b) * N * kv_stride + static_cast<size_t>(g) * D;
+  float m = -INFINITY, l = 0.f, acc[PER];
+#pragma unroll
+  for (int e = 0; e < PER; ++e) acc[e] = 0.f;
+  for (int c = 0; c <= p; c += 64) {
+    const int j = c + lane;
+    float sc = -INFINITY;
+    if (j <= p) {
+      const float* kr = kb + j * kv_stride;
+      float dot = 0.f;
+#pragma unroll 8
+      for (int d = 0; d < D; ++d) dot = fmaf(s_q[wave][d], kr[d], dot);
+      sc = dot * scale;
+    }
+    const float cm = wave_max(sc);
+    const float m_new = fmaxf(m, cm);
+    const float alpha = expf(m - m_new);
+    const float pj = j <= p ? expf(sc - m_new) : 0.f;
+    l = l * alpha + wave_sum(pj);
+#pragma unroll
+    for (int e = 0; e < PER; ++e) acc[e] *= alpha;
+    const int cnt = min(64, p - c + 1);
+    for (int jj = 0; jj < cnt; ++jj) {
+      const float pw = __shfl(pj, jj, 64);
+      const float* vr = vb + (c + jj) * kv_stride;
+#pragma unroll
+      for (int e = 0; e < PER; ++e) acc[e] = fmaf(pw, vr[lane * PER + e], acc[e]);
+    }
+    m = m_new;
+  }
+  float* orow = out + ((static_cast<size_t>(b) * R + r) * Hq + h) * D;
+#pragma unroll
+  for (int e = 0; e < PER; ++e) orow[lane * PER + e] = acc[e] / l;
+}
+
+}  // namespace
+}  // namespace rc
+
+extern "C" int rc_selective_attention(const rc_shape* shape, const void* q, const int32_t* rows,
+                                      int32_t R, const void* k, const void* v, float scale,
+                                      void* out, hipStream_t stream) {
+  using namespace rc;
+  clear_error();
+  if (int st = check_shape(shape, true)) return st;
+  if (R < 0) return fail(RC_ERR_INVALID_ARG, "R=%d must be >= 0", R);
+  if (!q || !k || !v || (!out && R > 0))
+    return fail(RC_ERR_INVALID_ARG, "q, k, v and out must be non-NULL");
+  if (!rows && R != shape->N)
+    return fail(RC_ERR_INVALID_ARG, "full-prefill mode (rows NULL) needs R == N (R=%d, N=%d)", R, shape->N);
+  if (!(scale > 0.f) || !std::isfinite(scale))
+    return fail(RC_ERR_INVALID_ARG, "scale must be finite and > 0");
+  if (R == 0) return RC_OK;
+  const int B = shape->B, N = shape->N, Hq = shape->Hq, Hkv = shape->Hkv, D = shape->D;
+  const int G = Hq / Hkv;
+  if (shape->dtype == RC_BF16) {
+    if (kM % G != 0) return fail(RC_ERR_UNSUPPORTED, "group size Hq/Hkv=%d must divide %d", G, kM);
+    const int BR = kM / G;
+    const int n_tiles = (R + BR - 1) / BR;
+    const int64_t total = static_cast<int64_t>(n_tiles) * B * Hkv;
+    const int64_t per_xcd = (total + kXcds - 1) / kXcds;
+    if (per_xcd * kXcds > 0x7fffffff) return fail(RC_ERR_UNSUPPORTED, "grid too large");
+    const float scale_log2e = static_cast<float>(static_cast<double>(scale) * 1.4426950408889634);
+    dim3 grid(static_cast<unsigned>(per_xcd * kXcds));
+    if (D == 128)
+      hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, dim3(kAttnThreads), 0, stream,
+                         static_cast<const uint16_t*>(q), rows, R, N, Hq, Hkv, G, BR,
+                         static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
+                         scale_log2e, static_cast<uint16_t*>(out), n_tiles, static_cast<int>(total),
+                         static_cast<int>(per_xcd));
+    else
+      hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, dim3(kAttnThreads), 0, stream,
+                         static_cast<const uint16_t*>(q), rows, R, N, Hq, Hkv, G, BR,
+                         static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
+                         scale_log2e, static_cast<uint16_t*>(out), n_tiles, static_cast<int>(total),
+                         static_cast<int>(per_xcd));
+  } else {
+    const int64_t total = static_cast<int64_t>(B) * R * Hq;
+    const int64_t blocks = (total + 3) / 4;
+    if (blocks > 0x7fffffff) return fail(RC_ERR_UNSUPPORTED, "grid too large");
+    dim3 grid(static_cast<unsigned>(blocks));
+    if (D == 128)
+      hipLaunchKernelGGL(attn_f32_kernel<128>, grid, dim3(256), 0, stream,
+                         static_cast<const float*>(q), rows, R, N, Hq, Hkv,
+                         static_cast<const float*>(k), static_cast<const float*>(v), scale,
+                         static_cast<float*>(out), total);
+    else
+      hipLaunchKernelGGL(attn_f32_kernel<64>, grid, dim3(256), 0, stream,
+                         static_cast<const float*>(q), rows, R, N, Hq, Hkv,
+                         static_cast<const float*>(k), static_cast<const float*>(v), scale,
+                         static_cast<float*>(out), total);
+  }
+  return check_launch("rc_selective_attention");
+}

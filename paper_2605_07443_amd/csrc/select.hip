@@ -1,0 +1,376 @@
+// Heavy-hitter selection and correction (RcLLM, arXiv 2605.07443,
+// Sec. III-C.2b with the deviation term of Eq. (3) for M = K, lambda = 1, and
+// Sec. III-C.3 step (iii)).
+//
+//   deviation_kernel  one wave per position: L1 distance between the fresh
+//                     and the assembled key row (HBM-bound, 16-byte loads,
+//                     wave reduction)
+//   topk_kernel       one 1024-thread workgroup per request: range-adaptive
+//                     radix select of the k-th largest score key in LDS
+//                     (11-bit digits), then a block scan that emits the fresh
+//                     and selected positions in ascending order
+//   patch_kernel      copies the fresh K/V rows of the selected cached
+//                     positions over the assembled rows
+#include "rc_common.h"
+
+namespace rc {
+namespace {
+
+using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
+
+// ------------------------------------------------------------------ deviation
+
+constexpr int kDevWaves = 4;
+constexpr int kDevTokPerWave = 4;
+
+template <int ES>
+__device__ __forceinline__ float absdiff_unit(const u32x4& a, const u32x4& b) {
+  float acc = 0.f;
+  if constexpr (ES == 4) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc += fabsf(__uint_as_float(a[e]) - __uint_as_float(b[e]));
+  } else {
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      acc += fabsf(bf16_to_f32(static_cast<uint16_t>(a[w])) - bf16_to_f32(static_cast<uint16_t>(b[w])));
+      acc += fabsf(bf16_to_f32(static_cast<uint16_t>(a[w] >> 16)) -
+                   bf16_to_f32(static_cast<uint16_t>(b[w] >> 16)));
+    }
+  }
+  return acc;
+}
+
+// d[t] = sum |k_fresh[t] - k_asm[t]| over the row of t (t = b*N + i).
+template <int ES>
+__global__ __launch_bounds__(64 * kDevWaves) void deviation_kernel(
+    const char* __restrict__ k_fresh, const char* __restrict__ k_asm, int64_t rows, int row_units,
+    float* __restrict__ scores) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int64_t t0 = (static_cast<int64_t>(blockIdx.x) * kDevWaves + wave) * kDevTokPerWave;
+  float acc[kDevTokPerWave];
+#pragma unroll
+  for (int r = 0; r < kDevTokPerWave; ++r) acc[r] = 0.f;
+  for (int u0 = 0; u0 < row_units; u0 += 64) {
+    const int u = u0 + lane;
+    u32x4 a[kDevTokPerWave], c[kDevTokPerWave];
+#pragma unroll
+    for (int r = 0; r < kDevTokPerWave; ++r) {
+      const int64_t t = t0 + r;
+      if (t < rows && u < row_units) {
+        a[r] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(k_fresh + t * row_units * 16) + u);
+        c[r] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(k_asm + t * row_units * 16) + u);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < kDevTokPerWave; ++r)
+      if (t0 + r < rows && u < row_units) acc[r] += absdiff_unit<ES>(a[r], c[r]);
+  }
+#pragma unroll
+  for (int r = 0; r < kDevTokPerWave; ++r) {
+    const float s = wave_sum(acc[r]);
+    if (lane == 0 && t0 + r < rows) scores[t0 + r] = s;
+  }
+}
+
+// ---------------------------------------------------------------------- top-k
+
+constexpr int kTopkThreads = 1024;
+constexpr int kTopkWaves = kTopkThreads / 64;
+constexpr int kBins = 2048;  // 11-bit digits
+constexpr int kDigitBits = 11;
+
+// Total order on fp32: larger key = larger value; +NaN above +inf.
+__device__ __forceinline__ uint32_t score_key(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Inclusive block scan of one int per thread (1024 threads); also returns
+// the block total. `warp_tot` is LDS scratch of kTopkWaves ints.
+__device__ __forceinline__ int block_inclusive_scan(int x, int* warp_tot, int& total) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(x, off, 64);
+    if (lane >= off) x += y;
+  }
+  if (lane == 63) warp_tot[wave] = x;
+  __syncthreads();
+  int before = 0;
+  total = 0;
+#pragma unroll
+  for (int w = 0; w < kTopkWaves; ++w) {
+    const int v = warp_tot[w];
+    before += (w < wave) ? v : 0;
+    total += v;
+  }
+  __syncthreads();
+  return x + before;
+}
+
+__device__ __forceinline__ int block_sum(int x, int* warp_tot) {
+  int total;
+  block_inclusive_scan(x, warp_tot, total);
+  return total;
+}
+
+// One workgroup per request. Candidates are positions outside fresh
+// segments. Key of position i: score_key(score[i]); order (key desc, i asc).
+__global__ __launch_bounds__(kTopkThreads) void topk_kernel(
+    const float* __restrict__ scores, const int4* __restrict__ segs, int S, int N, int k, int R,
+    int32_t* __restrict__ rows) {
+  __shared__ uint32_t s_key[kMaxSelectN];
+  __shared__ uint8_t s_cand[kMaxSelectN];
+  __shared__ int4 s_segs[kMaxSegments];
+  __shared__ int s_hist[kBins];
+  __shared__ int s_wt[kTopkWaves];
+  __shared__ uint32_t s_bounds[4];
+
+  const int b = blockIdx.x;
+  const int tid = threadIdx.x;
+  for (int s = tid; s < S; s += kTopkThreads) s_segs[s] = segs[static_cast<size_t>(b) * S + s];
+  __syncthreads();
+
+  uint32_t kmin = 0xffffffffu, kmax = 0u;
+  int ncand = 0;
+  for (int i = tid; i < N; i += kTopkThreads) {
+    const int s = find_segment(s_segs, S, i);
+    const bool cand = s >= 0 && s_segs[s].z >= 0;
+    const uint32_t key = score_key(scores[static_cast<size_t>(b) * N + i]);
+    s_key[i] = key;
+    s_cand[i] = cand ? 1 : 0;
+    if (cand) {
+      kmin = min(kmin, key);
+      kmax = max(kmax, key);
+      ++ncand;
+    }
+  }
+  // block reductions of min/max/count
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    kmin = min(kmin, static_cast<uint32_t>(__shfl_xor(static_cast<int>(kmin), off, 64)));
+    kmax = max(kmax, static_cast<uint32_t>(__shfl_xor(static_cast<int>(kmax), off, 64)));
+  }
+  if (tid == 0) {
+    s_bounds[0] = 0xffffffffu;
+    s_bounds[1] = 0u;
+    s_bounds[2] = 0u;
+    s_bounds[3] = 0u;
+  }
+  __syncthreads();
+  if ((tid & 63) == 0) {
+    atomicMin(&s_bounds[0], kmin);
+    atomicMax(&s_bounds[1], kmax);
+  }
+  ncand = block_sum(ncand, s_wt);  // contains barriers
+  const int kk = min(k, ncand);
+
+  // ---- find the threshold key T: the kk-th largest candidate key
+  uint32_t lo = s_bounds[0], hi = s_bounds[1];
+  int need = kk;  // how many of the keys in [lo, hi] we still take
+  if (kk > 0) {
+    while (lo != hi) {
+      const uint32_t range = hi - lo;
+      const int bits = 32 - __clz(range);
+      const int shift = bits > kDigitBits ? bits - kDigitBits : 0;
+      for (int j = tid; j < kBins; j += kTopkThreads) s_hist[j] = 0;
+      __syncthreads();
+      for (int i = tid; i < N; i += kTopkThreads) {
+        const uint32_t key = s_key[i];
+        if (s_cand[i] && key >= lo && key <= hi) atomicAdd(&s_hist[(key - lo) >> shift], 1);
+      }
+      __syncthreads();
+      // suffix sums from the top bin: each thread owns two adjacent bins,
+      // counted from the highest bin down
+      const int b1 = kBins - 1 - 2 * tid, b0 = b1 - 1;
+      const int c1 = s_hist[b1], c0 = s_hist[b0];
+      int total;
+      const int incl = block_inclusive_scan(c1 + c0, s_wt, total);
+      const int excl = incl - c1 - c0;  // count in bins above b1
+      // the bin where the running count first reaches `need`
+      int sel = -1, above = 0;
+      if (excl < need && excl + c1 >= need) {
+        sel = b1;
+        above = excl;
+      } else if (excl + c1 < need && incl >= need) {
+        sel = b0;
+        above = excl + c1;
+      }
+      if (sel >= 0) {
+        s_bounds[2] = static_cast<uint32_t>(sel);
+        s_bounds[3] = static_cast<uint32_t>(above);
+      }
+      __syncthreads();
+      const uint32_t bin = s_bounds[2];
+      need -= static_cast<int>(s_bounds[3]);
+      const uint32_t nlo = lo + (bin << shift);
+      const uint32_t width_m1 = (shift >= 32) ? 0xffffffffu : ((1u << shift) - 1u);
+      const uint32_t nhi = (hi - nlo > width_m1) ? nlo + width_m1 : hi;
+      lo = nlo;
+      hi = nhi;
+      __syncthreads();
+    }
+  }
+  const uint32_t T = lo;  // threshold key (meaningful when kk > 0)
+  // `need` = number of candidates with key == T to take, lowest positions first
+
+  // ---- emit rows: fresh positions, keys > T, and the first `need` ties
+  const int per = (N + kTopkThreads - 1) / kTopkThreads;
+  const int beg = min(N, tid * per), end = min(N, beg + per);
+  int ties = 0;
+  if (kk > 0)
+    for (int i = beg; i < end; ++i) ties += (s_cand[i] && s_key[i] == T) ? 1 : 0;
+  int tot;
+  int tie_before = block_inclusive_scan(ties, s_wt, tot) - ties;
+  int take = 0;
+  for (int i = beg; i < end; ++i) {
+    bool t;
+    if (!s_cand[i]) {
+      t = true;
+    } else if (kk == 0) {
+      t = false;
+    } else if (s_key[i] > T) {
+      t = true;
+    } else if (s_key[i] == T) {
+      t = tie_before < need;
+      ++tie_before;
+    } else {
+      t = false;
+    }
+    take += t ? 1 : 0;
+    s_cand[i] = t ? 2 : s_cand[i];  // mark taken (2); candidates not taken keep 1
+  }
+  __syncthreads();
+  int out = block_inclusive_scan(take, s_wt, tot) - take;
+  for (int i = beg; i < end; ++i) {
+    const bool t = !s_cand[i] || s_cand[i] == 2;
+    if (t) {
+      if (out < R) rows[static_cast<size_t>(b) * R + out] = i;
+      ++out;
+    }
+  }
+  // pad a short list (inconsistent n_fresh) with the last position
+  __syncthreads();
+  for (int r = tot + tid; r < R; r += kTopkThreads) rows[static_cast<size_t>(b) * R + r] = N - 1;
+}
+
+// ---------------------------------------------------------------------- patch
+
+constexpr int kPatchThreads = 256;
+
+__global__ __launch_bounds__(kPatchThreads) void patch_kernel(
+    const int4* __restrict__ segs, int S, int N, const int32_t* __restrict__ rows, int R,
+    int rows_per_wg, int row_units, const char* __restrict__ k_fresh,
+    const char* __restrict__ v_fresh, char* __restrict__ k_asm, char* __restrict__ v_asm) {
+  __shared__ int4 s_segs[kMaxSegments];
+  __shared__ int s_pos[256];
+  const int b = blockIdx.y;
+  const int r0 = blockIdx.x * rows_per_wg;
+  const int cnt = min(rows_per_wg, R - r0);
+  for (int s = threadIdx.x; s < S; s += kPatchThreads) s_segs[s] = segs[static_cast<size_t>(b) * S + s];
+  __syncthreads();
+  for (int t = threadIdx.x; t < cnt; t += kPatchThreads) {
+    const int i = rows[static_cast<size_t>(b) * R + r0 + t];
+    int pos = -1;
+    if (i >= 0 && i < N) {
+      const int s = find_segment(s_segs, S, i);
+      if (s >= 0 && s_segs[s].z >= 0) pos = i;  // cached position: patch it
+    }
+    s_pos[t] = pos;
+  }
+  __syncthreads();
+  const int items = cnt * row_units;
+  for (int base = threadIdx.x; base < items; base += kPatchThreads * 4) {
+    u32x4 kv[4], vv[4];
+    int tk[4], un[4];
+    bool ok[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int idx = base + u * kPatchThreads;
+      ok[u] = idx < items;
+      tk[u] = ok[u] ? idx / row_units : 0;
+      un[u] = idx - tk[u] * row_units;
+      ok[u] = ok[u] && s_pos[tk[u]] >= 0;
+      if (ok[u]) {
+        const size_t off = (static_cast<size_t>(b) * N + s_pos[tk[u]]) * row_units;
+        kv[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(k_fresh) + off + un[u]);
+        vv[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(v_fresh) + off + un[u]);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (!ok[u]) continue;
+      const size_t off = (static_cast<size_t>(b) * N + s_pos[tk[u]]) * row_units;
+      reinterpret_cast<u32x4*>(k_asm)[off + un[u]] = kv[u];
+      reinterpret_cast<u32x4*>(v_asm)[off + un[u]] = vv[u];
+    }
+  }
+}
+
+}  // namespace
+}  // namespace rc
+
+extern "C" int rc_select_tokens(const rc_shape* shape, const rc_segment* segs, int32_t S,
+                                int32_t n_fresh, int32_t k, const void* k_fresh,
+                                const void* v_fresh, void* k_asm, void* v_asm,
+                                const float* scores_in, float* scores_out, int32_t* rows,
+                                int32_t patch, hipStream_t stream) {
+  using namespace rc;
+  clear_error();
+  if (int st = check_shape(shape, false)) return st;
+  const int N = shape->N, B = shape->B;
+  if (!segs) return fail(RC_ERR_INVALID_ARG, "segs must be non-NULL");
+  if (!rows && n_fresh + k > 0) return fail(RC_ERR_INVALID_ARG, "rows must be non-NULL");
+  if (S < 1) return fail(RC_ERR_INVALID_ARG, "S=%d must be >= 1", S);
+  if (S > kMaxSegments) return fail(RC_ERR_UNSUPPORTED, "S=%d exceeds %d segments", S, kMaxSegments);
+  if (N > kMaxSelectN) return fail(RC_ERR_UNSUPPORTED, "N=%d exceeds %d", N, kMaxSelectN);
+  if (n_fresh < 0 || n_fresh > N) return fail(RC_ERR_INVALID_ARG, "n_fresh=%d not in [0, N]", n_fresh);
+  if (k < 0 || k > N - n_fresh)
+    return fail(RC_ERR_INVALID_ARG, "k=%d not in [0, N - n_fresh = %d]", k, N - n_fresh);
+  if (!scores_in && (!k_fresh || !k_asm || !scores_out))
+    return fail(RC_ERR_INVALID_ARG, "without scores_in, k_fresh, k_asm and scores_out are required");
+  if (patch && (!k_fresh || !v_fresh || !k_asm || !v_asm))
+    return fail(RC_ERR_INVALID_ARG, "patch needs k_fresh, v_fresh, k_asm and v_asm");
+  if (B > 65535) return fail(RC_ERR_UNSUPPORTED, "B=%d exceeds 65535", B);
+  const int es = elem_size(shape->dtype);
+  const int row_units = shape->Hkv * shape->D * es / 16;
+  const int4* segs4 = reinterpret_cast<const int4*>(segs);
+  const int R = n_fresh + k;
+
+  const float* sc = scores_in;
+  if (!scores_in) {
+    const int64_t nrows = static_cast<int64_t>(B) * N;
+    const int64_t per_wg = kDevWaves * kDevTokPerWave;
+    dim3 grid(static_cast<unsigned>((nrows + per_wg - 1) / per_wg));
+    if (shape->dtype == RC_BF16)
+      hipLaunchKernelGGL(deviation_kernel<2>, grid, dim3(64 * kDevWaves), 0, stream,
+                         static_cast<const char*>(k_fresh), static_cast<const char*>(k_asm), nrows,
+                         row_units, scores_out);
+    else
+      hipLaunchKernelGGL(deviation_kernel<4>, grid, dim3(64 * kDevWaves), 0, stream,
+                         static_cast<const char*>(k_fresh), static_cast<const char*>(k_asm), nrows,
+                         row_units, scores_out);
+    if (int st = check_launch("rc_select_tokens (deviation)")) return st;
+    sc = scores_out;
+  } else if (scores_out && scores_out != scores_in) {
+    if (hipMemcpyAsync(scores_out, scores_in, sizeof(float) * B * N, hipMemcpyDeviceToDevice, stream) !=
+        hipSuccess)
+      return fail(RC_ERR_HIP, "rc_select_tokens: copy of scores_in failed");
+  }
+  if (R > 0) {
+    hipLaunchKernelGGL(topk_kernel, dim3(B), dim3(kTopkThreads), 0, stream, sc, segs4, S, N, k, R, rows);
+    if (int st = check_launch("rc_select_tokens (top-k)")) return st;
+  }
+  if (patch && k > 0) {
+    const int rows_per_wg = 16;
+    dim3 grid((R + rows_per_wg - 1) / rows_per_wg, B);
+    hipLaunchKernelGGL(patch_kernel, grid, dim3(kPatchThreads), 0, stream, segs4, S, N, rows, R,
+                       rows_per_wg, row_units, static_cast<const char*>(k_fresh),
+                       static_cast<const char*>(v_fresh), static_cast<char*>(k_asm),
+                       static_cast<char*>(v_asm));
+    if (int st = check_launch("rc_select_tokens (patch)")) return st;
+  }
+  return RC_OK;
+}

@@ -1,0 +1,230 @@
+"""torch-facing wrappers of the C ABI (include/rcllm.h).
+
+Argument marshalling only: shapes, dtypes and pointers are checked and passed
+to librcllm, which enqueues its HIP kernels on torch's current stream. torch
+provides device memory and streams; no step of the path runs in torch, and
+there is no fallback: without the built library every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+from dataclasses import dataclass
+
+import numpy as np
+import torch
+
+from . import _lib
+from ._lib import RcPool, RcShape, check
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return _lib.RC_BF16
+    if t.dtype == torch.float32:
+        return _lib.RC_F32
+    raise TypeError(f"storage dtype must be bfloat16 or float32, got {t.dtype}")
+
+
+def _dev(t: torch.Tensor, name: str) -> int:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream=None) -> ctypes.c_void_p:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _shape(B, N, Hq, Hkv, D, dtype_code) -> RcShape:
+    return RcShape(int(B), int(N), int(Hq), int(Hkv), int(D), int(dtype_code))
+
+
+# ---------------------------------------------------------------- segments
+
+@dataclass
+class Segments:
+    """A validated, uploaded segment table."""
+    dev: torch.Tensor       # [B, S, 4] int32 on the device
+    host: np.ndarray        # [B, S, 4] int32
+    n_fresh: int            # fresh positions per request (same for every request)
+    N: int
+
+    @property
+    def S(self) -> int:
+        return int(self.host.shape[1])
+
+    @property
+    def n_reused(self) -> int:
+        return self.N - self.n_fresh
+
+
+def prepare_segments(segs, N: int, pools, device) -> Segments:
+    """Check on the host that every request's segments tile [0, N) in order,
+    name existing pools and blocks and share one fresh count, then upload."""
+    h = np.ascontiguousarray(np.asarray(segs.cpu() if isinstance(segs, torch.Tensor) else segs,
+                                        dtype=np.int32))
+    if h.ndim != 3 or h.shape[2] != 4 or h.shape[1] < 1:
+        raise ValueError("segments must have shape [B, S, 4]")
+    n_fresh = None
+    for b, req in enumerate(h):
+        pos, fresh = 0, 0
+        for dst, ln, p, blk in req.tolist():
+            if dst != pos or ln < 1:
+                raise ValueError(f"request {b}: segments must tile [0, N) in order")
+            if p >= 0:
+                if p >= len(pools):
+                    raise ValueError(f"request {b}: pool {p} does not exist")
+                pk = pools[p][0]
+                if not (0 <= blk < pk.shape[0]) or ln > pk.shape[1]:
+                    raise ValueError(f"request {b}: block {blk}/len {ln} outside pool {p}")
+            else:
+                fresh += ln
+            pos += ln
+        if pos != N:
+            raise ValueError(f"request {b}: segments cover {pos} positions, N = {N}")
+        if n_fresh is None:
+            n_fresh = fresh
+        elif fresh != n_fresh:
+            raise ValueError("every request must have the same number of fresh positions")
+    dev = torch.from_numpy(h).to(device)
+    return Segments(dev=dev, host=h, n_fresh=int(n_fresh), N=int(N))
+
+
+# ----------------------------------------------------------------- calls
+
+def rope_table(max_pos: int, D: int, base: float, device=None):
+    """cos/sin tables [max_pos, D/2] fp32 built by the library (host) and
+    uploaded to `device` when given."""
+    cos = torch.empty((max_pos, D // 2), dtype=torch.float32)
+    sin = torch.empty((max_pos, D // 2), dtype=torch.float32)
+    check(_lib.load().rc_rope_table(int(max_pos), int(D), float(base),
+                                    ctypes.c_void_p(cos.data_ptr()), ctypes.c_void_p(sin.data_ptr())))
+    if device is not None:
+        cos, sin = cos.to(device), sin.to(device)
+    return cos, sin
+
+
+def _pool_array(pools, dtype, Hkv, D):
+    arr = (RcPool * len(pools))()
+    for i, (pk, pv) in enumerate(pools):
+        if pk.dtype != dtype or pv.dtype != dtype:
+            raise TypeError("pool dtype differs from the fresh tensors")
+        if pk.shape != pv.shape or pk.dim() != 4 or pk.shape[2] != Hkv or pk.shape[3] != D:
+            raise ValueError("pool K/V must be [num_blocks, block_len, Hkv, D]")
+        arr[i] = RcPool(_dev(pk, "pool k"), _dev(pv, "pool v"), pk.shape[0], pk.shape[1])
+    return arr
+
+
+def kv_assemble(pools, segs: Segments, k_fresh, v_fresh, cos=None, sin=None, k_out=None,
+                v_out=None, stream=None):
+    """rc_kv_assemble: gather + fused re-alignment. Returns (k_asm, v_asm)."""
+    B, N, Hkv, D = k_fresh.shape
+    if v_fresh.shape != k_fresh.shape or v_fresh.dtype != k_fresh.dtype:
+        raise ValueError("k_fresh and v_fresh must match")
+    k_out = torch.empty_like(k_fresh) if k_out is None else k_out
+    v_out = torch.empty_like(v_fresh) if v_out is None else v_out
+    code = _dtype_code(k_fresh)
+    parr = _pool_array(pools, k_fresh.dtype, Hkv, D)
+    max_pos = 0 if cos is None else int(cos.shape[0])
+    check(_lib.load().rc_kv_assemble(
+        ctypes.byref(_shape(B, N, 1, Hkv, D, code)), parr, len(pools), _dev(segs.dev, "segs"),
+        segs.S, _dev(k_fresh, "k_fresh"), _dev(v_fresh, "v_fresh"),
+        None if cos is None else _dev(cos, "cos"), None if sin is None else _dev(sin, "sin"),
+        max_pos, _dev(k_out, "k_out"), _dev(v_out, "v_out"), _stream(stream)))
+    return k_out, v_out
+
+
+def rerope(k, delta, cos, sin, stream=None):
+    """rc_rerope: rotate K[b,i] by delta[b,i] in place. Returns k."""
+    B, N, Hkv, D = k.shape
+    if delta.dtype != torch.int32 or tuple(delta.shape) != (B, N):
+        raise ValueError("delta must be int32 [B, N]")
+    check(_lib.load().rc_rerope(ctypes.byref(_shape(B, N, 1, Hkv, D, _dtype_code(k))),
+                                _dev(k, "k"), _dev(delta, "delta"), _dev(cos, "cos"),
+                                _dev(sin, "sin"), int(cos.shape[0]), _stream(stream)))
+    return k
+
+
+def select_tokens(segs: Segments, k: int, k_fresh, v_fresh, k_asm, v_asm, scores_in=None,
+                  scores_out=None, rows_out=None, patch=True, stream=None):
+    """rc_select_tokens: score, top-k, patch. Returns (rows, scores)."""
+    B, N, Hkv, D = k_fresh.shape
+    R = segs.n_fresh + int(k)
+    rows = torch.empty((B, R), dtype=torch.int32, device=k_fresh.device) if rows_out is None else rows_out
+    if scores_in is None and scores_out is None:
+        scores_out = torch.empty((B, N), dtype=torch.float32, device=k_fresh.device)
+    check(_lib.load().rc_select_tokens(
+        ctypes.byref(_shape(B, N, 1, Hkv, D, _dtype_code(k_fresh))), _dev(segs.dev, "segs"),
+        segs.S, segs.n_fresh, int(k), _dev(k_fresh, "k_fresh"), _dev(v_fresh, "v_fresh"),
+        _dev(k_asm, "k_asm"), _dev(v_asm, "v_asm"),
+        None if scores_in is None else _dev(scores_in, "scores_in"),
+        None if scores_out is None else _dev(scores_out, "scores_out"),
+        _dev(rows, "rows"), 1 if patch else 0, _stream(stream)))
+    return rows, (scores_out if scores_out is not None else scores_in)
+
+
+def selective_attention(q, k, v, rows=None, scale=None, out=None, stream=None):
+    """rc_selective_attention: causal GQA attention of `rows` (all rows if None)."""
+    B, N, Hq, D = q.shape
+    Hkv = k.shape[2]
+    if k.shape != v.shape or k.shape[:2] != q.shape[:2] or k.shape[3] != D:
+        raise ValueError("q [B,N,Hq,D] and k, v [B,N,Hkv,D] do not match")
+    R = N if rows is None else int(rows.shape[1])
+    if rows is not None and (rows.dtype != torch.int32 or rows.shape[0] != B):
+        raise ValueError("rows must be int32 [B, R]")
+    scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
+    out = torch.empty((B, R, Hq, D), dtype=q.dtype, device=q.device) if out is None else out
+    check(_lib.load().rc_selective_attention(
+        ctypes.byref(_shape(B, N, Hq, Hkv, D, _dtype_code(q))), _dev(q, "q"),
+        None if rows is None else _dev(rows, "rows"), R, _dev(k, "k"), _dev(v, "v"),
+        ctypes.c_float(scale), _dev(out, "out"), _stream(stream)))
+    return out
+
+
+# ------------------------------------------------------------- the pipeline
+
+@dataclass
+class PrefillBuffers:
+    k_asm: torch.Tensor
+    v_asm: torch.Tensor
+    scores: torch.Tensor
+    rows: torch.Tensor
+    out: torch.Tensor
+
+    @staticmethod
+    def alloc(B, N, Hq, Hkv, D, R, dtype, device):
+        return PrefillBuffers(
+            k_asm=torch.empty((B, N, Hkv, D), dtype=dtype, device=device),
+            v_asm=torch.empty((B, N, Hkv, D), dtype=dtype, device=device),
+            scores=torch.empty((B, N), dtype=torch.float32, device=device),
+            rows=torch.empty((B, R), dtype=torch.int32, device=device),
+            out=torch.empty((B, R, Hq, D), dtype=dtype, device=device))
+
+
+def selective_prefill(q, k_fresh, v_fresh, pools, segs: Segments, k: int, cos, sin,
+                      scale=None, bufs: PrefillBuffers | None = None, stream=None):
+    """One layer of selective prefill on one stream: assemble (fused
+    re-alignment) -> score, top-k, patch -> attention of the fresh and selected
+    rows. Returns the buffers (k_asm, v_asm patched, scores, rows, out)."""
+    B, N, Hq, D = q.shape
+    Hkv = k_fresh.shape[2]
+    R = segs.n_fresh + int(k)
+    if bufs is None:
+        bufs = PrefillBuffers.alloc(B, N, Hq, Hkv, D, R, q.dtype, q.device)
+    kv_assemble(pools, segs, k_fresh, v_fresh, cos, sin, bufs.k_asm, bufs.v_asm, stream)
+    select_tokens(segs, k, k_fresh, v_fresh, bufs.k_asm, bufs.v_asm, scores_out=bufs.scores,
+                  rows_out=bufs.rows, patch=True, stream=stream)
+    if R > 0:
+        selective_attention(q, bufs.k_asm, bufs.v_asm, bufs.rows, scale, bufs.out, stream)
+    return bufs
+
+
+def full_prefill(q, k_fresh, v_fresh, scale=None, out=None, stream=None):
+    """Full-Recompute baseline: causal attention of every row over fresh K/V."""
+    return selective_attention(q, k_fresh, v_fresh, None, scale, out, stream)

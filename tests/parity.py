@@ -1,0 +1,110 @@
+"""Shared helpers for the GPU parity tests: run the HIP path step by step
+through the C ABI and compare every intermediate with the CPU oracle on the
+same seeded inputs."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import torch
+
+from oracle import oracle as O
+from paper_2605_07443_amd import inputs, ops
+
+H = inputs.to_host_bits
+
+# tolerances for attention outputs (fp32 accumulation)
+BF16_MAX, BF16_MEAN = 2e-2, 2e-3
+F32_MAX = 1e-4
+
+
+def say(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def assert_attn_close(gpu: np.ndarray, ref: np.ndarray, dtype: str, what: str = "") -> dict:
+    g, r = O.as_f32(gpu).astype(np.float64), O.as_f32(ref).astype(np.float64)
+    assert g.shape == r.shape, (g.shape, r.shape)
+    assert np.all(np.isfinite(g)), f"{what}: non-finite GPU output"
+    err = np.abs(g - r)
+    mx, mean = float(err.max()) if err.size else 0.0, float(err.mean()) if err.size else 0.0
+    if dtype == "bf16":
+        assert mx <= BF16_MAX and mean <= BF16_MEAN, f"{what}: max {mx:.3e} mean {mean:.3e}"
+    else:
+        assert mx <= F32_MAX, f"{what}: max {mx:.3e}"
+    return dict(max=mx, mean=mean)
+
+
+def sample_rows(B: int, R: int, stride: int):
+    """All rows of the first and last request, every `stride`-th row elsewhere."""
+    out = []
+    for b in range(B):
+        idx = np.arange(R) if b in (0, B - 1) or stride <= 1 else np.arange(0, R, stride)
+        out.append(idx)
+    return out
+
+
+def oracle_attention_rows(q, k, v, rows, sel):
+    """Oracle attention for rows[b][sel[b]] of each request b (one request at a time)."""
+    res = []
+    for b, idx in enumerate(sel):
+        r = np.ascontiguousarray(rows[b:b + 1, idx])
+        res.append(O.attention(q[b:b + 1], k[b:b + 1], v[b:b + 1], rows=r)[0])
+    return res
+
+
+def run_stepwise(cfg, w, k: int, device, stride: int = 1, check_attention: bool = True):
+    """Run assemble -> select (score, top-k, patch) -> attention on the GPU and
+    check each step against the oracle. Returns a dict of error statistics."""
+    stats = {}
+    segs = ops.prepare_segments(w.segs, cfg.N, w.pools, device)
+    cos, sin = ops.rope_table(cfg.N, cfg.D, cfg.rope_base, device)
+    k_asm, v_asm = ops.kv_assemble(w.pools, segs, w.k_fresh, w.v_fresh, cos, sin)
+    k_pre, v_pre = k_asm.clone(), v_asm.clone()
+    rows, scores = ops.select_tokens(segs, k, w.k_fresh, w.v_fresh, k_asm, v_asm, patch=True)
+    out = ops.selective_attention(w.q, k_asm, v_asm, rows) if rows.shape[1] > 0 else None
+    torch.cuda.synchronize()
+
+    # ---- (i)+(ii) assembly with fused re-alignment: bit-exact
+    ocos, osin = O.rope_table(cfg.N, cfg.D, cfg.rope_base)
+    subpools, segs_sub = inputs.referenced_subpools(w)
+    kf, vf = H(w.k_fresh), H(w.v_fresh)
+    ka_o, va_o = O.assemble(kf, vf, subpools, segs_sub, ocos, osin)
+    np.testing.assert_array_equal(H(k_pre), ka_o, err_msg="assembled K differs")
+    np.testing.assert_array_equal(H(v_pre), va_o, err_msg="assembled V differs")
+
+    # ---- deviation scores: fp32 accumulation vs fp64
+    sc_g = scores.cpu().numpy()
+    sc_o = O.deviation(kf, ka_o)
+    np.testing.assert_allclose(sc_g, sc_o, rtol=1e-5, atol=1e-5, err_msg="deviation scores")
+    stats["score_rel"] = float(np.max(np.abs(sc_g - sc_o) / np.maximum(np.abs(sc_o), 1e-30)))
+
+    # ---- top-k: bit-exact on identical scores, both ways
+    segs_h = w.segs.numpy()
+    rows_g = rows.cpu().numpy()
+    np.testing.assert_array_equal(rows_g, O.topk(segs_h, cfg.N, k, sc_g),
+                                  err_msg="GPU rows differ from oracle top-k of the GPU scores")
+    sc_in = torch.from_numpy(sc_o).to(device)
+    rows_g2, _ = ops.select_tokens(segs, k, w.k_fresh, w.v_fresh, k_asm, v_asm, scores_in=sc_in,
+                                   patch=False)
+    np.testing.assert_array_equal(rows_g2.cpu().numpy(), O.topk(segs_h, cfg.N, k, sc_o),
+                                  err_msg="GPU top-k of the oracle scores differs")
+    stats["rows_agree_own_scores"] = float(np.mean(rows_g == O.topk(segs_h, cfg.N, k, sc_o)))
+
+    # ---- (iii) patch: bit-exact
+    kp_o, vp_o = O.patch(segs_h, rows_g, kf, vf, ka_o, va_o)
+    np.testing.assert_array_equal(H(k_asm), kp_o, err_msg="patched K differs")
+    np.testing.assert_array_equal(H(v_asm), vp_o, err_msg="patched V differs")
+
+    # ---- attention of the selected rows
+    if check_attention and out is not None:
+        qh = H(w.q)
+        sel = sample_rows(cfg.B, rows_g.shape[1], stride)
+        ref = oracle_attention_rows(qh, kp_o, vp_o, rows_g, sel)
+        outh = H(out)
+        g = np.concatenate([outh[b, idx] for b, idx in enumerate(sel)])
+        r = np.concatenate(ref)
+        stats.update(assert_attn_close(g, r, cfg.dtype, "selective attention"))
+    return stats, dict(segs=segs, cos=cos, sin=sin, k_asm=k_asm, v_asm=v_asm, rows=rows,
+                       scores=scores, out=out)

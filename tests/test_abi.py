@@ -1,0 +1,155 @@
+"""CPU-side checks of the C ABI: the library loads, exports every symbol the
+header declares, builds the same RoPE tables as the oracle, and rejects bad
+arguments on the host before anything is enqueued (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2605_07443_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rcllm.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(_lib.LIB_PATH):
+        from paper_2605_07443_amd import build
+        build.build()
+    return _lib.load()
+
+
+def test_header_declarations_are_exported(lib):
+    text = open(HEADER).read()
+    declared = set(re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?(rc_\w+)\s*\(", text, re.M))
+    assert declared == set(_lib.EXPORTS)
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(lib):
+    assert _lib.status_string(0) == "RC_OK"
+    assert _lib.status_string(-1) == "RC_ERR_INVALID_ARG"
+    assert _lib.status_string(-2) == "RC_ERR_UNSUPPORTED"
+    assert _lib.status_string(-3) == "RC_ERR_HIP"
+
+
+@pytest.mark.parametrize("max_pos,D,base", [(416, 64, 10000.0), (8160, 128, 500000.0)])
+def test_rope_table_bitwise_equals_oracle_table(lib, max_pos, D, base):
+    """Two independent fp64 -> fp32 table builders agree bit for bit, so the
+    fused re-alignment can be compared bit-exactly."""
+    cos = np.empty((max_pos, D // 2), np.float32)
+    sin = np.empty((max_pos, D // 2), np.float32)
+    assert lib.rc_rope_table(max_pos, D, base, cos.ctypes.data, sin.ctypes.data) == 0
+    ocos, osin = O.rope_table(max_pos, D, base)
+    np.testing.assert_array_equal(cos, ocos)
+    np.testing.assert_array_equal(sin, osin)
+
+
+FAKE = 0x1000  # never dereferenced: every case below fails host validation
+
+# Belt and braces: on a machine with a GPU a validation bug would launch a
+# kernel on these fake pointers, so the fake-pointer cases only run without
+# one (device_count() does not initialise the GPU).
+import torch  # noqa: E402
+
+no_gpu = pytest.mark.skipif(torch.cuda.device_count() > 0,
+                            reason="fake-pointer validation cases run only on GPU-less hosts")
+
+
+def _shape(B=2, N=64, Hq=8, Hkv=2, D=128, dtype=1):
+    return ctypes.byref(_lib.RcShape(B, N, Hq, Hkv, D, dtype))
+
+
+def _pools(n=1, nb=4, bl=16):
+    arr = (_lib.RcPool * max(n, 1))()
+    for i in range(n):
+        arr[i] = _lib.RcPool(FAKE, FAKE + 64, nb, bl)
+    return arr
+
+
+def _err(status, lib):
+    return status, lib.rc_last_error().decode()
+
+
+def test_rope_table_rejects_bad_args(lib):
+    buf = np.empty(8, np.float32)
+    assert lib.rc_rope_table(4, 4, 10000.0, None, buf.ctypes.data) == -1
+    assert lib.rc_rope_table(0, 4, 10000.0, buf.ctypes.data, buf.ctypes.data) == -1
+    assert lib.rc_rope_table(2, 3, 10000.0, buf.ctypes.data, buf.ctypes.data) == -1
+    assert lib.rc_rope_table(2, 4, -1.0, buf.ctypes.data, buf.ctypes.data) == -1
+
+
+@no_gpu
+def test_assemble_validation(lib):
+    ok = dict(pools=_pools(), n=1, segs=FAKE, S=3, kf=FAKE, vf=FAKE + 8, cos=FAKE, sin=FAKE,
+              max_pos=64, ka=FAKE + 16, va=FAKE + 24)
+
+    def call(shape=None, **kw):
+        a = dict(ok, **kw)
+        return lib.rc_kv_assemble(_shape() if shape is None else shape, a["pools"], a["n"], a["segs"], a["S"], a["kf"],
+                                  a["vf"], a["cos"], a["sin"], a["max_pos"], a["ka"], a["va"], None)
+
+    assert call(shape=ctypes.cast(0, ctypes.POINTER(_lib.RcShape))) == -1
+    assert call(segs=None) == -1
+    assert call(kf=None) == -1
+    assert call(ka=None) == -1
+    assert call(S=0) == -1
+    assert call(S=1025) == -2
+    assert call(n=0) == -1
+    assert call(n=9, pools=_pools(9)) == -2
+    assert call(pools=_pools(1, nb=0)) == -1
+    assert call(cos=None) == -1                       # one table without the other
+    st, msg = _err(call(max_pos=63), lib)             # tables shorter than the prompt
+    assert st == -1 and "max_pos" in msg
+    assert call(shape=_shape(D=96)) == -2
+    assert call(shape=_shape(dtype=7)) == -2
+    assert call(shape=_shape(N=0)) == -1
+    assert call(ka=FAKE) == -1                        # output aliases an input
+
+
+@no_gpu
+def test_rerope_validation(lib):
+    assert lib.rc_rerope(_shape(), None, FAKE, FAKE, FAKE, 8, None) == -1
+    assert lib.rc_rerope(_shape(), FAKE, FAKE, FAKE, FAKE, 0, None) == -1
+    assert lib.rc_rerope(_shape(D=32), FAKE, FAKE, FAKE, FAKE, 8, None) == -2
+
+
+@no_gpu
+def test_select_validation(lib):
+    def call(shape=None, S=3, n_fresh=8, k=10, scores_in=None, scores_out=FAKE, rows=FAKE, patch=1,
+             kf=FAKE, vf=FAKE, ka=FAKE, va=FAKE):
+        return lib.rc_select_tokens(_shape() if shape is None else shape, FAKE, S, n_fresh, k, kf, vf, ka, va, scores_in,
+                                    scores_out, rows, patch, None)
+
+    assert call(k=-1) == -1
+    assert call(k=57) == -1                           # k > N - n_fresh
+    assert call(n_fresh=65) == -1
+    assert call(rows=None) == -1
+    assert call(scores_out=None) == -1                # must score without scores_in
+    assert call(patch=1, va=None) == -1
+    assert call(shape=_shape(N=16385)) == -2
+    assert call(S=0) == -1
+    st, msg = _err(call(k=100), lib)
+    assert "k=100" in msg
+
+
+@no_gpu
+def test_attention_validation(lib):
+    def call(shape=None, rows=FAKE, R=10, scale=0.088, q=FAKE, out=FAKE):
+        return lib.rc_selective_attention(_shape() if shape is None else shape, q, rows, R, FAKE, FAKE,
+                                          ctypes.c_float(scale), out, None)
+
+    assert call(q=None) == -1
+    assert call(R=-1) == -1
+    assert call(rows=None, R=10) == -1                # full mode needs R == N
+    assert call(scale=0.0) == -1
+    assert call(scale=float("nan")) == -1
+    assert call(shape=_shape(Hq=6, Hkv=4)) == -1      # Hq % Hkv
+    assert call(shape=_shape(Hq=12, Hkv=4)) == -2     # bf16 group of 3 does not divide 128
+    assert call(shape=_shape(D=256)) == -2
+    assert call(R=0) == 0                             # nothing to do, nothing enqueued

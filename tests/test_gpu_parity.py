@@ -1,0 +1,264 @@
+"""GPU parity: the HIP path, called through the C ABI, against the CPU oracle
+on the same seeded inputs.
+
+Bar: assembled K/V, selected rows and patched K/V bit-exact (rows compared on
+identical scores); deviation scores within 1e-5 relative; attention outputs
+within max-abs 2e-2 / mean-abs 2e-3 (bf16) or 1e-4 (fp32)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2605_07443_amd import inputs, ops
+
+from parity import (H, assert_attn_close, oracle_attention_rows, run_stepwise, sample_rows,
+                    say)
+
+pytestmark = pytest.mark.gpu
+
+DEV = torch.device("cuda:0")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib_loaded():
+    from paper_2605_07443_amd import _lib
+    _lib.load()
+    yield
+    torch.cuda.synchronize()
+
+
+# ---------------------------------------------------------------- small shapes
+
+SMALL = ["tiny-bf16", "ragged-bf16", "mha-d64-bf16", "miss-bf16", "tiny-f32-gqa"]
+
+
+@pytest.mark.parametrize("name", SMALL)
+@pytest.mark.parametrize("pct", [0, 15, 40, 100])
+def test_stepwise_small(name, pct):
+    cfg = inputs.TEST_CONFIGS[name]
+    say(f"[stepwise] {name} pct={pct} N={cfg.N} B={cfg.B}")
+    w = inputs.make(cfg, 100 + pct, device=DEV)
+    stats, _ = run_stepwise(cfg, w, cfg.k_for(pct), DEV)
+    say(f"  {stats}")
+
+
+def test_stepwise_config1_tiny_fp32():
+    cfg = inputs.CONFIGS[1]
+    say(f"[stepwise] config 1 N={cfg.N}")
+    w = inputs.make(cfg, 1000, device=DEV)
+    stats, _ = run_stepwise(cfg, w, cfg.k, DEV)
+    say(f"  {stats}")
+
+
+def test_planted_heavy_hitters_selected_on_gpu():
+    cfg = inputs.TEST_CONFIGS["tiny-bf16"]
+    w = inputs.make(cfg, 5, device=DEV, planted=6)
+    _, r = run_stepwise(cfg, w, cfg.k, DEV)
+    rows = r["rows"].cpu().numpy()
+    for b in range(cfg.B):
+        assert set(w.planted[b].tolist()) <= set(rows[b].tolist())
+
+
+# ----------------------------------------------------- standalone re-alignment
+
+@pytest.mark.parametrize("dtype,D,Hkv", [("bf16", 128, 8), ("bf16", 64, 2), ("f32", 64, 8),
+                                         ("f32", 128, 1)])
+def test_rerope_standalone_bitexact(dtype, D, Hkv):
+    B, N, max_pos = 3, 301, 5000
+    g = torch.Generator(device="cpu").manual_seed(7)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    k = torch.randn((B, N, Hkv, D), generator=g).to(tdt)
+    delta = torch.randint(-(max_pos - 1), max_pos, (B, N), generator=g, dtype=torch.int32)
+    delta[:, ::7] = 0
+    delta[0, 5] = max_pos          # out of range: skipped
+    delta[1, 9] = -max_pos
+    cos, sin = ops.rope_table(max_pos, D, 500000.0, DEV)
+    kd = k.to(DEV)
+    ops.rerope(kd, delta.to(DEV), cos, sin)
+    torch.cuda.synchronize()
+    ocos, osin = O.rope_table(max_pos, D, 500000.0)
+    d_np = delta.numpy().copy()
+    d_np[0, 5] = 0
+    d_np[1, 9] = 0
+    want = O.rerope(H(k), d_np, ocos, osin)
+    np.testing.assert_array_equal(H(kd), want)
+
+
+# ------------------------------------------------------------ attention shapes
+
+@pytest.mark.parametrize("Hq,Hkv", [(8, 8), (8, 4), (16, 4), (16, 2), (32, 2)])
+@pytest.mark.parametrize("D", [64, 128])
+def test_attention_unsorted_rows_and_groups(Hq, Hkv, D):
+    B, N, R = 2, 333, 150
+    g = torch.Generator(device="cpu").manual_seed(Hq * 100 + Hkv + D)
+    q = torch.randn((B, N, Hq, D), generator=g).to(torch.bfloat16)
+    k = torch.randn((B, N, Hkv, D), generator=g).to(torch.bfloat16)
+    v = torch.randn((B, N, Hkv, D), generator=g).to(torch.bfloat16)
+    rows = torch.randint(0, N, (B, R), generator=g, dtype=torch.int32)
+    rows[0, :3] = torch.tensor([N - 1, 0, N - 1], dtype=torch.int32)   # duplicates, extremes
+    out = ops.selective_attention(q.to(DEV), k.to(DEV), v.to(DEV), rows.to(DEV))
+    full = ops.full_prefill(q.to(DEV), k.to(DEV), v.to(DEV))
+    torch.cuda.synchronize()
+    ref = O.attention(H(q), H(k), H(v), rows=rows.numpy())
+    assert_attn_close(H(out), ref, "bf16", "selective")
+    reff = O.attention(H(q), H(k), H(v))
+    assert_attn_close(H(full), reff, "bf16", "full prefill")
+
+
+def test_attention_fp32_full_and_selected():
+    B, N, Hq, Hkv, D = 2, 190, 8, 2, 128
+    g = torch.Generator(device="cpu").manual_seed(3)
+    q, k, v = (torch.randn((B, N, h, D), generator=g) for h in (Hq, Hkv, Hkv))
+    rows = torch.sort(torch.randperm(N, generator=g)[:70]).values.to(torch.int32).repeat(B, 1)
+    out = ops.selective_attention(q.to(DEV), k.to(DEV), v.to(DEV), rows.to(DEV).contiguous())
+    full = ops.full_prefill(q.to(DEV), k.to(DEV), v.to(DEV))
+    torch.cuda.synchronize()
+    assert_attn_close(H(out), O.attention(H(q), H(k), H(v), rows=rows.numpy()), "f32", "sel")
+    assert_attn_close(H(full), O.attention(H(q), H(k), H(v)), "f32", "full")
+
+
+# ------------------------------------------------------------------ invariants
+
+@pytest.mark.parametrize("name", ["tiny-bf16", "tiny-f32-gqa", "miss-bf16"])
+def test_full_ratio_equals_full_prefill_on_gpu(name):
+    """Selecting every cached token = Full-Recompute, bit for bit on the GPU."""
+    cfg = inputs.TEST_CONFIGS[name]
+    w = inputs.make(cfg, 31, device=DEV)
+    segs = ops.prepare_segments(w.segs, cfg.N, w.pools, DEV)
+    cos, sin = ops.rope_table(cfg.N, cfg.D, cfg.rope_base, DEV)
+    bufs = ops.selective_prefill(w.q, w.k_fresh, w.v_fresh, w.pools, segs, cfg.n_reused, cos, sin)
+    full = ops.full_prefill(w.q, w.k_fresh, w.v_fresh)
+    torch.cuda.synchronize()
+    assert torch.equal(bufs.rows.cpu(), torch.arange(cfg.N, dtype=torch.int32).repeat(cfg.B, 1))
+    assert torch.equal(bufs.k_asm, w.k_fresh) and torch.equal(bufs.v_asm, w.v_fresh)
+    assert torch.equal(bufs.out, full)
+
+
+@pytest.mark.parametrize("pct", [0, 10, 50])
+def test_zero_perturbation_equals_full_prefill_on_gpu(pct):
+    cfg = inputs.TEST_CONFIGS["ragged-bf16"]
+    w = inputs.make(cfg, 32, device=DEV, sigma=0.0)
+    segs = ops.prepare_segments(w.segs, cfg.N, w.pools, DEV)
+    cos, sin = ops.rope_table(cfg.N, cfg.D, cfg.rope_base, DEV)
+    bufs = ops.selective_prefill(w.q, w.k_fresh, w.v_fresh, w.pools, segs, cfg.k_for(pct), cos, sin)
+    full = ops.full_prefill(w.q, w.k_fresh, w.v_fresh)
+    torch.cuda.synchronize()
+    rows = bufs.rows.long()
+    sel_full = torch.stack([full[b, rows[b]] for b in range(cfg.B)])
+    assert_attn_close(H(bufs.out), H(sel_full), "bf16", "zero noise")
+
+
+def test_instruction_rows_equal_full_prefill_at_any_noise():
+    cfg = inputs.TEST_CONFIGS["tiny-bf16"]
+    w = inputs.make(cfg, 33, device=DEV, sigma=0.3)
+    segs = ops.prepare_segments(w.segs, cfg.N, w.pools, DEV)
+    cos, sin = ops.rope_table(cfg.N, cfg.D, cfg.rope_base, DEV)
+    bufs = ops.selective_prefill(w.q, w.k_fresh, w.v_fresh, w.pools, segs, cfg.k, cos, sin)
+    full = ops.full_prefill(w.q, w.k_fresh, w.v_fresh)
+    torch.cuda.synchronize()
+    rows = bufs.rows.cpu().numpy()
+    for b in range(cfg.B):
+        first = np.nonzero(rows[b] < cfg.F)[0]
+        ref = H(full[b])[rows[b][first]]
+        assert_attn_close(H(bufs.out[b])[first], ref, "bf16", "instruction rows")
+
+
+def test_pipeline_is_deterministic():
+    cfg = inputs.TEST_CONFIGS["ragged-bf16"]
+    w = inputs.make(cfg, 34, device=DEV)
+    segs = ops.prepare_segments(w.segs, cfg.N, w.pools, DEV)
+    cos, sin = ops.rope_table(cfg.N, cfg.D, cfg.rope_base, DEV)
+    a = ops.selective_prefill(w.q, w.k_fresh, w.v_fresh, w.pools, segs, cfg.k, cos, sin)
+    b = ops.selective_prefill(w.q, w.k_fresh, w.v_fresh, w.pools, segs, cfg.k, cos, sin)
+    torch.cuda.synchronize()
+    for name in ("k_asm", "v_asm", "scores", "rows", "out"):
+        assert torch.equal(getattr(a, name), getattr(b, name)), name
+
+
+# ---------------------------------------------------------------- edge cases
+
+def test_single_token_segments_and_all_cached_prompt():
+    """Segments of length 1 and 2, no fresh positions at all (n_fresh = 0),
+    k = 0 (nothing recomputed, empty row list) and k = n_r."""
+    B, Hkv, Hq, D = 2, 2, 8, 128
+    pk = torch.randn((5, 3, Hkv, D)).to(torch.bfloat16).to(DEV)
+    pv = torch.randn((5, 3, Hkv, D)).to(torch.bfloat16).to(DEV)
+    spans = [(0, 1, 0, 4), (1, 2, 0, 0), (3, 1, 0, 2), (4, 3, 0, 1), (7, 1, 0, 3)]
+    segs_h = np.array([spans, spans[::-1]], np.int32)
+    # second request: same blocks in reverse order, re-tiled
+    pos = 0
+    for s in range(len(spans)):
+        segs_h[1, s, 0] = pos
+        pos += segs_h[1, s, 1]
+    N = 8
+    kf = torch.randn((B, N, Hkv, D)).to(torch.bfloat16).to(DEV)
+    vf = torch.randn((B, N, Hkv, D)).to(torch.bfloat16).to(DEV)
+    q = torch.randn((B, N, Hq, D)).to(torch.bfloat16).to(DEV)
+    segs = ops.prepare_segments(segs_h, N, [(pk, pv)], DEV)
+    assert segs.n_fresh == 0
+    cos, sin = ops.rope_table(N, D, 10000.0, DEV)
+    ka, va = ops.kv_assemble([(pk, pv)], segs, kf, vf, cos, sin)
+    torch.cuda.synchronize()
+    ocos, osin = O.rope_table(N, D, 10000.0)
+    ka_o, va_o = O.assemble(H(kf), H(vf), [(H(pk), H(pv))], segs_h, ocos, osin)
+    np.testing.assert_array_equal(H(ka), ka_o)
+    np.testing.assert_array_equal(H(va), va_o)
+    rows0, _ = ops.select_tokens(segs, 0, kf, vf, ka.clone(), va.clone())
+    assert rows0.shape == (B, 0)
+    rows8, sc = ops.select_tokens(segs, N, kf, vf, ka, va)
+    out = ops.selective_attention(q, ka, va, rows8)
+    torch.cuda.synchronize()
+    assert torch.equal(rows8.cpu(), torch.arange(N, dtype=torch.int32).repeat(B, 1))
+    assert_attn_close(H(out), O.attention(H(q), H(kf), H(vf)), "bf16", "all selected")
+
+
+def test_scores_in_special_values_match_oracle():
+    cfg = inputs.TEST_CONFIGS["ragged-bf16"]
+    w = inputs.make(cfg, 35, device=DEV)
+    segs = ops.prepare_segments(w.segs, cfg.N, w.pools, DEV)
+    rng = np.random.default_rng(0)
+    sc = rng.integers(0, 4, (cfg.B, cfg.N)).astype(np.float32)     # many ties
+    sc[0, 20] = np.nan
+    sc[0, 30] = np.inf
+    sc[1, 40] = -np.inf
+    sc[2, 50:60] = -1.5
+    sc[2, 61] = -0.0
+    for k in (0, 1, 7, cfg.n_reused // 2, cfg.n_reused):
+        rows, _ = ops.select_tokens(segs, k, w.k_fresh, w.v_fresh, torch.empty_like(w.k_fresh),
+                                    torch.empty_like(w.v_fresh), scores_in=torch.from_numpy(sc).to(DEV),
+                                    patch=False)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(rows.cpu().numpy(), O.topk(w.segs.numpy(), cfg.N, k, sc))
+
+
+# ------------------------------------------------------------- full workloads
+
+@pytest.mark.parametrize("cid,pct,stride", [(2, 15, 16), (3, 10, 32), (5, 15, 64),
+                                            (4, 0, 16), (4, 15, 16), (4, 50, 64), (4, 100, 128)])
+def test_stepwise_full_workloads(cid, pct, stride):
+    cfg = inputs.CONFIGS[cid]
+    say(f"[full workload] config {cid} pct={pct} B={cfg.B} N={cfg.N} pools="
+        f"{cfg.hist_pool}x{cfg.hist_len},{cfg.item_pool}x{cfg.item_len}")
+    w = inputs.make(cfg, 1000 * cid, device=DEV)
+    stats, _ = run_stepwise(cfg, w, cfg.k_for(pct), DEV, stride=stride)
+    say(f"  {stats}")
+    del w
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("cid,stride", [(2, 64), (3, 256)])
+def test_full_prefill_full_workloads(cid, stride):
+    cfg = inputs.CONFIGS[cid]
+    say(f"[full prefill] config {cid}")
+    g = torch.Generator(device=DEV).manual_seed(cid)
+    q = torch.randn((cfg.B, cfg.N, cfg.Hq, cfg.D), generator=g, device=DEV).to(torch.bfloat16)
+    k = torch.randn((cfg.B, cfg.N, cfg.Hkv, cfg.D), generator=g, device=DEV).to(torch.bfloat16)
+    v = torch.randn((cfg.B, cfg.N, cfg.Hkv, cfg.D), generator=g, device=DEV).to(torch.bfloat16)
+    out = ops.full_prefill(q, k, v)
+    torch.cuda.synchronize()
+    all_rows = np.arange(cfg.N, dtype=np.int32)[None].repeat(cfg.B, 0)
+    sel = [np.concatenate([np.arange(0, cfg.N, stride), [cfg.N - 1]]) for _ in range(cfg.B)]
+    ref = oracle_attention_rows(H(q), H(k), H(v), all_rows, sel)
+    outh = H(out)
+    g_ = np.concatenate([outh[b, idx] for b, idx in enumerate(sel)])
+    assert_attn_close(g_, np.concatenate(ref), "bf16", "full prefill")

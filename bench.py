@@ -1,0 +1,286 @@
+#!/usr/bin/env python3
+"""Benchmark of one layer of RcLLM's selective prefill (arXiv 2605.07443) on
+one MI355X.
+
+A step is one pass of the whole path over one batch of synthetic
+recommendation prompts already resident in HBM, on one stream:
+  rc_kv_assemble          gather of history/item KV blocks + fused RoPE
+                          re-alignment
+  rc_select_tokens        K deviation score, top-k, heavy-hitter patch
+  rc_selective_attention  causal GQA attention of the fresh + selected rows
+Batches rotate (default 4 independent draws over one shared pool) so the
+working set exceeds the 256 MB Infinity Cache.
+
+Prints ONE JSON line: selected-query tokens/s/layer (whole job), ms per step,
+microseconds per request, the roofline of the dominant kernel (measured with
+HIP events on the launch stream inside the timed region), every kernel's
+achieved rate, and the CPU oracle timed on a bounded sample of the same
+workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 matrix
+F32_PEAK_TFLOPS = 157.3        # MI355X fp32 vector
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def parse_args():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=2, help="workload 1..5 (default 2)")
+    ap.add_argument("--pct", type=int, default=None, help="recompute ratio in percent")
+    ap.add_argument("--batches", type=int, default=4, help="independent batches rotated")
+    ap.add_argument("--cpu-requests", type=int, default=None,
+                    help="requests of batch 0 in the CPU oracle's sample (default: all; 0 = skip)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="repeat the CPU oracle's sample until this much time has passed")
+    ap.add_argument("--no-full-prefill", action="store_true",
+                    help="skip timing the Full-Recompute baseline")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device copy (HBM counter calibration)")
+    return ap.parse_args()
+
+
+def source_digest(*names) -> str:
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2605_07443_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(config: int, pct: int):
+    """Measured HBM bytes per launch from committed rocprofv3 counter runs, if
+    they were taken on the current kernel sources; else None."""
+    path = os.path.join(PROFILES, f"traffic_config{config}_pct{pct}.md")
+    if not os.path.exists(path):
+        return None
+    m = re.search(r"```json\n(.*?)\n```", open(path).read(), re.S)
+    if not m:
+        return None
+    return json.loads(m.group(1))
+
+
+def copy_calibration():
+    import torch
+    n = 1 << 30
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    a.random_()
+    b = torch.empty_like(a)
+    for _ in range(5):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 5}), flush=True)
+
+
+def main():
+    args = parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(each request is independent; sharding is described in DESIGN.md)",
+              file=sys.stderr)
+        sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
+
+    import numpy as np
+    import torch
+
+    from paper_2605_07443_amd import _lib, inputs, ops
+
+    _lib.load()  # fails loudly when the HIP library is not built
+    dev = torch.device("cuda:0")
+    cfg = inputs.CONFIGS[args.config]
+    pct = cfg.pct if args.pct is None else args.pct
+    k = cfg.k_for(pct)
+    R = cfg.n_fresh + k
+    B, N, Hq, Hkv, D = cfg.B, cfg.N, cfg.Hq, cfg.Hkv, cfg.D
+    es = 2 if cfg.dtype == "bf16" else 4
+    row = Hkv * D * es
+
+    # ---- inputs: one shared pool, `batches` independent request batches
+    base = 1000 * args.config
+    batches = []
+    pools = None
+    for i in range(args.batches):
+        w = inputs.make(cfg, base + i, device=dev, pool_seed=base, pools=pools)
+        pools = w.pools
+        segs = ops.prepare_segments(w.segs, N, w.pools, dev)
+        bufs = ops.PrefillBuffers.alloc(B, N, Hq, Hkv, D, R, cfg.torch_dtype, dev)
+        batches.append((w, segs, bufs))
+    cos, sin = ops.rope_table(N, D, cfg.rope_base, dev)
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+
+    def step(i, ev=None):
+        w, segs, bufs = batches[i % len(batches)]
+        if ev is not None:
+            ev[0].record(stream)
+        ops.kv_assemble(w.pools, segs, w.k_fresh, w.v_fresh, cos, sin, bufs.k_asm, bufs.v_asm)
+        if ev is not None:
+            ev[1].record(stream)
+        ops.select_tokens(segs, k, w.k_fresh, w.v_fresh, bufs.k_asm, bufs.v_asm,
+                          scores_out=bufs.scores, rows_out=bufs.rows, patch=True)
+        if ev is not None:
+            ev[2].record(stream)
+        if R > 0:
+            ops.selective_attention(w.q, bufs.k_asm, bufs.v_asm, bufs.rows, None, bufs.out)
+        if ev is not None:
+            ev[3].record(stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    # attention work of each batch from its actual rows (unmasked causal work)
+    att_flops = []
+    for (w, segs, bufs) in batches:
+        r = bufs.rows.to(torch.int64).cpu()
+        att_flops.append(4.0 * D * Hq * float((r + 1).sum()) if R > 0 else 0.0)
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record(stream)
+    for i in range(args.steps):
+        step(args.warmup + i, evs[i])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = t_start.elapsed_time(t_end)
+    ms_per_step = total_ms / args.steps
+
+    asm_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
+    sel_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
+    att_ms = sum(e[2].elapsed_time(e[3]) for e in evs) / args.steps
+    flops = sum(att_flops[(args.warmup + i) % len(batches)] for i in range(args.steps)) / args.steps
+
+    gather_bytes = 4.0 * B * N * row                       # read K,V rows + write K,V rows
+    select_bytes = 2.0 * B * N * row + 12.0 * B * N + 4.0 * B * R + 4.0 * B * k * row
+    mfma_peak = BF16_PEAK_TFLOPS if cfg.dtype == "bf16" else F32_PEAK_TFLOPS
+
+    def hbm(bytes_, ms):
+        a = bytes_ / (ms * 1e-3) / 1e9 if ms > 0 else 0.0
+        return {"bound": "hbm", "achieved": round(a, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(a / HBM_PEAK_GBS, 4), "bytes_per_launch": gather_bytes if bytes_ is gather_bytes else bytes_}
+
+    att_tf = flops / (att_ms * 1e-3) / 1e12 if att_ms > 0 else 0.0
+    kernels = {
+        "rc_kv_assemble": dict(us=round(asm_ms * 1e3, 2), **hbm(gather_bytes, asm_ms)),
+        "rc_select_tokens": dict(us=round(sel_ms * 1e3, 2), **hbm(select_bytes, sel_ms)),
+        "rc_selective_attention": {
+            "us": round(att_ms * 1e3, 2), "bound": "mfma" if cfg.dtype == "bf16" else "alu",
+            "achieved": round(att_tf, 2), "peak": mfma_peak, "unit": "TFLOP/s",
+            "frac": round(att_tf / mfma_peak, 4), "flops_per_launch": flops},
+    }
+    dominant = max(kernels, key=lambda n: kernels[n]["us"])
+    dk = kernels[dominant]
+    traffic = None
+    tr = load_traffic(args.config, pct)
+    digest = {"rc_kv_assemble": source_digest("assemble.hip"),
+              "rc_select_tokens": source_digest("select.hip"),
+              "rc_selective_attention": source_digest("attention.hip")}
+    if tr and tr.get("source_digest", {}).get(dominant) == digest[dominant]:
+        traffic = tr.get("kernels", {}).get(dominant, {}).get("hbm_bytes")
+    roofline = {"kernel": dominant, "bound": dk["bound"], "achieved": dk["achieved"],
+                "peak": dk["peak"], "unit": dk["unit"], "frac": dk["frac"], "traffic": traffic}
+
+    # ---- Full-Recompute baseline on the same batch (context)
+    full = None
+    if not args.no_full_prefill and cfg.dtype == "bf16":
+        w0 = batches[0][0]
+        fout = torch.empty((B, N, Hq, D), dtype=cfg.torch_dtype, device=dev)
+        reps = max(3, min(20, args.steps // 5))
+        ops.full_prefill(w0.q, w0.k_fresh, w0.v_fresh, out=fout)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            ops.full_prefill(w0.q, w0.k_fresh, w0.v_fresh, out=fout)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        fms = e0.elapsed_time(e1) / reps
+        fflops = 4.0 * D * Hq * B * N * (N + 1) / 2
+        full = {"ms": round(fms, 4), "tflops": round(fflops / (fms * 1e-3) / 1e12, 2),
+                "frac_of_bf16_peak": round(fflops / (fms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
+                "selective_speedup": round(fms / ms_per_step, 3)}
+        del fout
+
+    # ---- CPU oracle on a bounded sample of the same workload
+    cpu = None
+    if args.cpu_requests is None or args.cpu_requests > 0:
+        from oracle import oracle as O
+        w0 = batches[0][0]
+        n = B if args.cpu_requests is None else min(args.cpu_requests, B)
+        H = inputs.to_host_bits
+        sub = inputs.Workload(cfg=cfg, seed=w0.seed, q=w0.q[:n], k_fresh=w0.k_fresh[:n],
+                              v_fresh=w0.v_fresh[:n], pools=w0.pools, segs=w0.segs[:n].clone(),
+                              item_ids=w0.item_ids[:n], hist_ids=w0.hist_ids[:n])
+        subpools, segs_sub = inputs.referenced_subpools(sub)
+        qh, kh, vh = H(sub.q), H(sub.k_fresh), H(sub.v_fresh)
+        ocos, osin = O.rope_table(N, D, cfg.rope_base)
+        reps = 0
+        t0 = time.perf_counter()
+        while True:
+            O.selective_prefill(qh, kh, vh, subpools, segs_sub, k, ocos, osin)
+            reps += 1
+            dt = time.perf_counter() - t0
+            if dt >= args.cpu_seconds or reps >= 50:
+                break
+        cpu = {"value": round(reps * n * R / dt, 1), "unit": "tokens/s/layer",
+               "cores": O.num_threads(), "kind": "oracle", "seconds": round(dt, 2),
+               "sample": f"{reps} pass(es) over {n} of {B} requests of one batch: the whole oracle "
+                         f"pipeline (assemble, rerope, deviation, top-k, patch, attention of {R} "
+                         f"rows each), fp64 accumulation"}
+
+    value = B * R * args.steps / (total_ms * 1e-3)
+    result = {
+        "metric": "selected-query tokens/s/layer at 15% recompute (one attention layer)"
+                  if pct == 15 else f"selected-query tokens/s/layer at {pct}% recompute",
+        "value": round(value, 1),
+        "unit": "tokens/s/layer",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "us_per_request": round(ms_per_step * 1e3 / B, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"config{args.config}:{cfg.name}", "B": B, "N": N,
+                   "recompute_pct": pct, "selected_rows_per_request": R, "Hq": Hq, "Hkv": Hkv,
+                   "D": D, "pools": [[cfg.hist_pool, cfg.hist_len], [cfg.item_pool, cfg.item_len]],
+                   "batches_rotated": args.batches},
+        "roofline": roofline,
+        "kernels": kernels,
+        "full_prefill": full,
+        "cpu_baseline": cpu,
+        "wall_s_timed": round(wall, 3),
+        "source_digest": digest,
+    }
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

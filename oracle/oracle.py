@@ -62,8 +62,15 @@ def lib():
                                               vp, i32, i32, vp, vp, vp, vp, vp, f64,
                                               vp, vp, vp, vp, vp]
         L.rcref_selective_prefill.restype = i32
+        L.rcref_num_threads.argtypes = []
+        L.rcref_num_threads.restype = i32
         _lib = L
     return _lib
+
+
+def num_threads() -> int:
+    """OpenMP threads the oracle's parallel loops use."""
+    return int(lib().rcref_num_threads())
 
 
 def _dt(a: np.ndarray) -> int:

@@ -29,9 +29,13 @@
  *   rope tables  [max_pos, D/2] fp32
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
+
+/* threads the OpenMP loops below use */
+int rcref_num_threads(void) { return omp_get_max_threads(); }
 
 /* ------------------------------------------------------------------ */
 /* storage helpers                                                      */

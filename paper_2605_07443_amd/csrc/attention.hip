@@ -12,7 +12,8 @@
 //     in registers and K read from LDS. In the output layout a lane then holds
 //     4 consecutive keys of one query column, which is also the B-operand
 //     layout of the second product O^T = V^T P^T, so P never leaves registers;
-//     V is staged transposed in LDS to serve as the A operand.
+//     V is staged key-major in LDS and read with the gfx950 transposed LDS
+//     read (ds_read_b64_tr_b16) straight into the A-operand layout.
 //   * Online softmax in the log2 domain with fp32 running max and sum.
 //   * Workgroup ids are remapped so that all row tiles of one (request, KV
 //     head) run on the same XCD (ids are dealt round-robin over the 8 XCDs),
@@ -34,11 +35,28 @@ constexpr int kXcds = 8;
 using u32x2 = uint32_t __attribute__((ext_vector_type(2)));
 using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
 
+// Row pads keep the two LDS read patterns conflict-free: 16-byte reads of 16
+// consecutive K rows (row stride = 16 mod 256 bytes), and transposed 8-byte
+// reads of 8 consecutive V rows per half-wave (row stride = 32 mod 256 bytes).
 template <int D>
 struct AttnSmem {
-  uint16_t k[kKT][D + 8];   // K tile, key-major; +16 B per row against bank conflicts
-  uint16_t vt[D][kKT + 4];  // V tile transposed, dim-major; +8 B per row
+  uint16_t k[kKT][D + 8];   // K tile, key-major
+  uint16_t v[kKT][D + 16];  // V tile, key-major (read transposed)
 };
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+
+// gfx950 transposed LDS read (ds_read_b64_tr_b16). Within each group of 16
+// lanes, lane s reads 4 consecutive 16-bit elements at its address; lane j
+// receives element j%4 of the reads of lanes j/4, j/4+4, j/4+8, j/4+12. With
+// lane s pointing at row (r0 + s/4), column (c0 + 4*(s%4)) of a row-major tile,
+// lane j receives column c0 + j of rows r0 .. r0+3.
+__device__ __forceinline__ u32x2 lds_read_tr4(const uint16_t* p) {
+  const v4i16 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_v4i16*)((__attribute__((address_space(3))) char*)(p)));
+  return __builtin_bit_cast(u32x2, r);
+}
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   const __bf16 a = static_cast<__bf16>(lo);
@@ -55,8 +73,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
                       uint16_t* __restrict__ out, int n_tiles, int total_wg, int per_xcd) {
   constexpr int DC = D / 32;          // 32-wide d chunks (S^T reduction)
   constexpr int DB = D / 16;          // 16-wide d blocks (O^T rows)
-  constexpr int KU = kKT * D / 8 / kAttnThreads;   // K 16-byte units per thread
-  constexpr int KPG = D / 32;         // V keys per thread (transposed staging)
+  constexpr int KU = kKT * D / 8 / kAttnThreads;   // K (and V) 16-byte units per thread
   constexpr int UPR = D / 8;          // 16-byte units per K/V head row
   __shared__ AttnSmem<D> sm;
   __shared__ int s_ext[4];
@@ -117,23 +134,17 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
   const size_t kv_row_stride = static_cast<size_t>(Hkv) * D;   // elements between keys
   const uint16_t* kbase = k + static_cast<size_t>(b) * N * kv_row_stride + static_cast<size_t>(g) * D;
   const uint16_t* vbase = v + static_cast<size_t>(b) * N * kv_row_stride + static_cast<size_t>(g) * D;
-  u32x4 kreg[KU], vreg[KPG];
-  const int v_d0 = (tid % UPR) * 8;
-  const int v_k0 = (tid / UPR) * KPG;
+  u32x4 kreg[KU], vreg[KU];
   auto load_tile = [&](int t) {
     const int j0 = t * kKT;
 #pragma unroll
     for (int i = 0; i < KU; ++i) {
       const int u = tid + i * kAttnThreads;
-      const int key = u / UPR;
+      const int j = j0 + u / UPR;
       const int col = (u % UPR) * 8;
-      const int j = j0 + key;
-      kreg[i] = j < N ? *reinterpret_cast<const u32x4*>(kbase + j * kv_row_stride + col) : u32x4{0, 0, 0, 0};
-    }
-#pragma unroll
-    for (int i = 0; i < KPG; ++i) {
-      const int j = j0 + v_k0 + i;
-      vreg[i] = j < N ? *reinterpret_cast<const u32x4*>(vbase + j * kv_row_stride + v_d0) : u32x4{0, 0, 0, 0};
+      const bool in = j < N;
+      kreg[i] = in ? *reinterpret_cast<const u32x4*>(kbase + j * kv_row_stride + col) : u32x4{0, 0, 0, 0};
+      vreg[i] = in ? *reinterpret_cast<const u32x4*>(vbase + j * kv_row_stride + col) : u32x4{0, 0, 0, 0};
     }
   };
   load_tile(0);
@@ -143,7 +154,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
   for (int db = 0; db < DB; ++db)
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) o[db][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run[2] = {-INFINITY, -INFINITY};
+  float m_run[2] = {-INFINITY, -INFINITY};  // running max of the unscaled scores
   float l_run[2] = {0.f, 0.f};
 
   for (int t = 0; t < n_kv; ++t) {
@@ -152,21 +163,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
     for (int i = 0; i < KU; ++i) {
       const int u = tid + i * kAttnThreads;
       *reinterpret_cast<u32x4*>(&sm.k[u / UPR][(u % UPR) * 8]) = kreg[i];
-    }
-    // transpose V: vreg[i] holds dims v_d0..v_d0+7 of key v_k0+i
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      uint16_t h[KPG];
-#pragma unroll
-      for (int i = 0; i < KPG; ++i) h[i] = static_cast<uint16_t>(vreg[i][e >> 1] >> (16 * (e & 1)));
-      if constexpr (KPG == 4) {
-        u32x2 w = {static_cast<uint32_t>(h[0]) | (static_cast<uint32_t>(h[1]) << 16),
-                   static_cast<uint32_t>(h[2]) | (static_cast<uint32_t>(h[3]) << 16)};
-        *reinterpret_cast<u32x2*>(&sm.vt[v_d0 + e][v_k0]) = w;
-      } else {
-        *reinterpret_cast<uint32_t*>(&sm.vt[v_d0 + e][v_k0]) =
-            static_cast<uint32_t>(h[0]) | (static_cast<uint32_t>(h[1]) << 16);
-      }
+      *reinterpret_cast<u32x4*>(&sm.v[u / UPR][(u % UPR) * 8]) = vreg[i];
     }
     __syncthreads();
     if (t + 1 < n_kv) load_tile(t + 1);
@@ -185,40 +182,47 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
       }
     }
 
-    // ---- causal mask + online softmax (per query column)
+    // ---- causal mask + online softmax (per query column). Scores stay
+    // unscaled until the exponent: p = 2^(s*c - m*c), c = scale*log2(e) > 0.
     const int j0 = t * kKT;
-    const bool need_mask = j0 + kKT - 1 > wave_pmin;
+    if (j0 + kKT - 1 > wave_pmin) {
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (j0 + kb * 16 + q4 * 4 + i > pos[nb]) s[kb][nb][i] = -INFINITY;
+    }
     bf16x8 pb[2][2];
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
       float mx = -INFINITY;
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float x = s[kb][nb][i] * scale_log2e;
-          if (need_mask && j0 + kb * 16 + q4 * 4 + i > pos[nb]) x = -INFINITY;
-          s[kb][nb][i] = x;
-          mx = fmaxf(mx, x);
-        }
+        mx = fmaxf(mx, fmaxf(fmaxf(s[kb][nb][0], s[kb][nb][1]), fmaxf(s[kb][nb][2], s[kb][nb][3])));
       mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
       const float m_new = fmaxf(m_run[nb], mx);
-      const float m_use = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = exp2f(m_run[nb] - m_use);
+      // a query always sees key 0 in the first tile, so m_new is finite
+      const float mc = m_new * scale_log2e;
+      if (__ballot(m_new > m_run[nb]) != 0) {
+        const float alpha = __builtin_amdgcn_exp2f(m_run[nb] * scale_log2e - mc);
+        l_run[nb] *= alpha;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) o[db][nb] *= alpha;
+        m_run[nb] = m_new;
+      }
       float ls = 0.f;
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float p = exp2f(s[kb][nb][i] - m_use);
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[kb][nb][i], scale_log2e, -mc));
           s[kb][nb][i] = p;
           ls += p;
         }
-      l_run[nb] = l_run[nb] * alpha + ls;
-      m_run[nb] = m_new;
-#pragma unroll
-      for (int db = 0; db < DB; ++db) o[db][nb] *= alpha;
+      l_run[nb] += ls;
 #pragma unroll
       for (int kc = 0; kc < 2; ++kc) {
         u32x4 w = {pack_bf16x2(s[2 * kc][nb][0], s[2 * kc][nb][1]),
@@ -230,12 +234,17 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
     }
 
     // ---- O^T += V^T P^T
+    // A operand V^T: lane (c16, q4) needs dim db*16 + c16 of keys
+    // kc*32 + q4*4 + {0..3} and kc*32 + 16 + q4*4 + {0..3}, the key order of
+    // the P^T operand built above.
+    const int tr_row = q4 * 4 + (c16 >> 2);
+    const int tr_col = 4 * (c16 & 3);
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int kc = 0; kc < 2; ++kc) {
-        const u32x2 lo = *reinterpret_cast<const u32x2*>(&sm.vt[db * 16 + c16][kc * 32 + q4 * 4]);
-        const u32x2 hi = *reinterpret_cast<const u32x2*>(&sm.vt[db * 16 + c16][kc * 32 + 16 + q4 * 4]);
+        const u32x2 lo = lds_read_tr4(&sm.v[kc * 32 + tr_row][db * 16 + tr_col]);
+        const u32x2 hi = lds_read_tr4(&sm.v[kc * 32 + 16 + tr_row][db * 16 + tr_col]);
         const bf16x8 a = __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
         o[db][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][0], o[db][0], 0, 0, 0);
         o[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][1], o[db][1], 0, 0, 0);

@@ -235,9 +235,16 @@ def segment_table(cfg: Config, hist: torch.Tensor, items: torch.Tensor) -> torch
 
 
 def make(cfg: Config, seed: int, device="cpu", sigma: float | None = None,
-         planted: int = 0, planted_scale: float = 20.0, chunk_elems: int = 1 << 27) -> Workload:
-    """Generate one batch of the workload `cfg` on `device`."""
+         planted: int = 0, planted_scale: float = 20.0, chunk_elems: int = 1 << 27,
+         pool_seed: int | None = None, pools: list | None = None) -> Workload:
+    """Generate one batch of the workload `cfg` on `device`.
+
+    Pool contents are drawn from `pool_seed` (default `seed`). Passing `pools`
+    made earlier with the same pool_seed and sigma reuses them: only the batch's
+    own draws (ids, Q, fresh rows) are new, the block contents are re-derived
+    from the same counter-based seeds."""
     sigma = cfg.sigma if sigma is None else float(sigma)
+    pool_seed = seed if pool_seed is None else pool_seed
     dt = cfg.torch_dtype
     B, N, Hq, Hkv, D = cfg.B, cfg.N, cfg.Hq, cfg.Hkv, cfg.D
     hist, items = sample_ids(cfg, seed)
@@ -267,24 +274,31 @@ def make(cfg: Config, seed: int, device="cpu", sigma: float | None = None,
             if p >= 0:
                 users[p].setdefault(blk, []).append((b, dst, ln))
 
-    pools = []
+    reuse = pools is not None
+    new_pools = []
     for p, (P, L) in enumerate([(cfg.hist_pool, cfg.hist_len), (cfg.item_pool, cfg.item_len)]):
-        pk = torch.empty((P, L, Hkv, D), device=device, dtype=dt)
-        pv = torch.empty((P, L, Hkv, D), device=device, dtype=dt)
+        if reuse:
+            pk, pv = pools[p]
+        else:
+            pk = torch.empty((P, L, Hkv, D), device=device, dtype=dt)
+            pv = torch.empty((P, L, Hkv, D), device=device, dtype=dt)
         local = torch.arange(L, device=device)
         per_chunk = max(1, chunk_elems // (L * Hkv * D))
         for c, c0 in enumerate(range(0, P, per_chunk)):
             c1 = min(P, c0 + per_chunk)
-            g = _gen(device, seed, 4, p, c)
+            if reuse and not any(blk in users[p] for blk in range(c0, c1)):
+                continue
+            g = _gen(device, pool_seed, 4, p, c)
             shp = (c1 - c0, L, Hkv, D)
             raw = torch.randn(shp, generator=g, device=device, dtype=torch.float32)
             val = torch.randn(shp, generator=g, device=device, dtype=torch.float32)
-            eps = torch.randn(shp, generator=g, device=device, dtype=torch.float32)
-            eta = torch.randn(shp, generator=g, device=device, dtype=torch.float32)
-            noisy = raw.to(torch.float64) + sigma * eps.to(torch.float64)
-            pk[c0:c1] = _rope_model(noisy, local, cfg.rope_base).to(dt)
-            pv[c0:c1] = (val.to(torch.float64) + sigma * eta.to(torch.float64)).to(dt)
-            del noisy, eps, eta
+            if not reuse:
+                eps = torch.randn(shp, generator=g, device=device, dtype=torch.float32)
+                eta = torch.randn(shp, generator=g, device=device, dtype=torch.float32)
+                noisy = raw.to(torch.float64) + sigma * eps.to(torch.float64)
+                pk[c0:c1] = _rope_model(noisy, local, cfg.rope_base).to(dt)
+                pv[c0:c1] = (val.to(torch.float64) + sigma * eta.to(torch.float64)).to(dt)
+                del noisy, eps, eta
             for blk in range(c0, c1):
                 for (b, dst, ln) in users[p].get(blk, ()):
                     pos = torch.arange(dst, dst + ln, device=device)
@@ -292,7 +306,8 @@ def make(cfg: Config, seed: int, device="cpu", sigma: float | None = None,
                     k_fresh[b, dst:dst + ln] = _rope_model(r, pos, cfg.rope_base).to(dt)
                     v_fresh[b, dst:dst + ln] = val[blk - c0, :ln].to(dt)
             del raw, val
-        pools.append((pk, pv))
+        new_pools.append((pk, pv))
+    pools = new_pools
 
     planted_pos = None
     if planted:

@@ -14,11 +14,13 @@
 //     layout of the second product O^T = V^T P^T, so P never leaves registers;
 //     V is staged key-major in LDS and read with the gfx950 transposed LDS
 //     read (ds_read_b64_tr_b16) straight into the A-operand layout.
-//   * Online softmax in the log2 domain with fp32 running max and sum.
+//   * Online softmax in the log2 domain with fp32 running sums and a lazily
+//     raised reference max; K/V tiles double-buffered in LDS (one barrier per
+//     tile) with the next tile's global loads in flight during compute.
 //   * Workgroup ids are remapped so that all row tiles of one (request, KV
 //     head) run on the same XCD (ids are dealt round-robin over the 8 XCDs),
-//     sharing its L2 for the K/V stream, with the longest (latest) tiles
-//     first.
+//     sharing its L2 for the K/V stream, and each XCD starts its longest
+//     (latest) tiles first across all of its groups.
 // fp32 path: one wave per (request, row, head), fp32 FMA on the vector ALUs.
 #include <cmath>
 
@@ -38,14 +40,17 @@ using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
 // Row pads keep the two LDS read patterns conflict-free: 16-byte reads of 16
 // consecutive K rows (row stride = 16 mod 256 bytes), and transposed 8-byte
 // reads of 8 consecutive V rows per half-wave (row stride = 32 mod 256 bytes).
+// Two buffers: the next tile is written while the current one is read.
 template <int D>
 struct AttnSmem {
-  uint16_t k[kKT][D + 8];   // K tile, key-major
-  uint16_t v[kKT][D + 16];  // V tile, key-major (read transposed)
+  uint16_t k[2][kKT][D + 8];   // K tiles, key-major
+  uint16_t v[2][kKT][D + 16];  // V tiles, key-major (read transposed)
 };
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 // gfx950 transposed LDS read (ds_read_b64_tr_b16). Within each group of 16
 // lanes, lane s reads 4 consecutive 16-bit elements at its address; lane j
@@ -58,31 +63,38 @@ __device__ __forceinline__ u32x2 lds_read_tr4(const uint16_t* p) {
   return __builtin_bit_cast(u32x2, r);
 }
 
+// two fp32 -> packed bf16 (round to nearest even), one v_cvt_pk_bf16_f32
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  const __bf16 a = static_cast<__bf16>(lo);
-  const __bf16 b = static_cast<__bf16>(hi);
-  return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, a)) |
-         (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, b)) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
+
+// Softmax exponents use a running reference max that is only raised when a
+// score exceeds it by more than 2^kLazy (log2 units): p <= 2^kLazy stays exact
+// in fp32 and bf16, and the O/l rescale is skipped on most tiles.
+constexpr float kLazy = 8.f;
 
 template <int D>
 __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict__ rows, int R,
                       int N, int Hq, int Hkv, int G, int BR, const uint16_t* __restrict__ k,
                       const uint16_t* __restrict__ v, float scale_log2e,
-                      uint16_t* __restrict__ out, int n_tiles, int total_wg, int per_xcd) {
+                      uint16_t* __restrict__ out, int n_tiles, int n_groups, int gpx) {
   constexpr int DC = D / 32;          // 32-wide d chunks (S^T reduction)
   constexpr int DB = D / 16;          // 16-wide d blocks (O^T rows)
-  constexpr int KU = kKT * D / 8 / kAttnThreads;   // K (and V) 16-byte units per thread
   constexpr int UPR = D / 8;          // 16-byte units per K/V head row
+  constexpr int KU = kKT * UPR / kAttnThreads;   // K (and V) units per thread
+  constexpr int KSTEP = kAttnThreads / UPR;      // keys between a thread's units
   __shared__ AttnSmem<D> sm;
   __shared__ int s_ext[4];
 
+  // ---- work item: XCD-major, longest tiles first across the XCD's groups
   const int hw = blockIdx.x;
-  const int logical = (hw % kXcds) * per_xcd + hw / kXcds;
-  if (logical >= total_wg) return;
-  const int grp = logical / n_tiles;
-  const int tile = n_tiles - 1 - (logical - grp * n_tiles);
+  const int xcd = hw % kXcds;
+  const int slot = hw / kXcds;
+  const int rank = slot / gpx;
+  const int grp = (slot - rank * gpx) * kXcds + xcd;
+  if (rank >= n_tiles || grp >= n_groups) return;
+  const int tile = n_tiles - 1 - rank;
   const int b = grp / Hkv;
   const int g = grp - b * Hkv;
   const int tid = threadIdx.x;
@@ -130,60 +142,75 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
       qf[nb][dc] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(qrow + dc * 32 + q4 * 8));
   }
 
-  // ---- K/V tile prefetch registers
-  const size_t kv_row_stride = static_cast<size_t>(Hkv) * D;   // elements between keys
-  const uint16_t* kbase = k + static_cast<size_t>(b) * N * kv_row_stride + static_cast<size_t>(g) * D;
-  const uint16_t* vbase = v + static_cast<size_t>(b) * N * kv_row_stride + static_cast<size_t>(g) * D;
+  // ---- K/V staging: thread owns units (key tid/UPR + i*KSTEP, dims (tid%UPR)*8 ..)
+  const size_t stride = static_cast<size_t>(Hkv) * D;   // elements between keys
+  const int key0 = tid / UPR;
+  const int col0 = (tid % UPR) * 8;
+  const size_t off0 = (static_cast<size_t>(b) * N + key0) * stride + static_cast<size_t>(g) * D + col0;
+  const uint16_t* kp = k + off0;
+  const uint16_t* vp = v + off0;
+  const size_t tile_step = static_cast<size_t>(kKT) * stride;
   u32x4 kreg[KU], vreg[KU];
   auto load_tile = [&](int t) {
-    const int j0 = t * kKT;
+    const uint16_t* kt = kp + t * tile_step;
+    const uint16_t* vt = vp + t * tile_step;
+    if ((t + 1) * kKT <= N) {
 #pragma unroll
-    for (int i = 0; i < KU; ++i) {
-      const int u = tid + i * kAttnThreads;
-      const int j = j0 + u / UPR;
-      const int col = (u % UPR) * 8;
-      const bool in = j < N;
-      kreg[i] = in ? *reinterpret_cast<const u32x4*>(kbase + j * kv_row_stride + col) : u32x4{0, 0, 0, 0};
-      vreg[i] = in ? *reinterpret_cast<const u32x4*>(vbase + j * kv_row_stride + col) : u32x4{0, 0, 0, 0};
+      for (int i = 0; i < KU; ++i) {
+        kreg[i] = *reinterpret_cast<const u32x4*>(kt + i * KSTEP * stride);
+        vreg[i] = *reinterpret_cast<const u32x4*>(vt + i * KSTEP * stride);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < KU; ++i) {
+        const bool in = t * kKT + key0 + i * KSTEP < N;
+        kreg[i] = in ? *reinterpret_cast<const u32x4*>(kt + i * KSTEP * stride) : u32x4{0, 0, 0, 0};
+        vreg[i] = in ? *reinterpret_cast<const u32x4*>(vt + i * KSTEP * stride) : u32x4{0, 0, 0, 0};
+      }
     }
   };
-  load_tile(0);
+  auto store_tile = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < KU; ++i) {
+      *reinterpret_cast<u32x4*>(&sm.k[buf][key0 + i * KSTEP][col0]) = kreg[i];
+      *reinterpret_cast<u32x4*>(&sm.v[buf][key0 + i * KSTEP][col0]) = vreg[i];
+    }
+  };
 
   f32x4 o[DB][2];
 #pragma unroll
   for (int db = 0; db < DB; ++db)
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) o[db][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run[2] = {-INFINITY, -INFINITY};  // running max of the unscaled scores
-  float l_run[2] = {0.f, 0.f};
+  float m_run[2] = {-INFINITY, -INFINITY};  // reference max of the unscaled scores
+  float l_run[2] = {0.f, 0.f};              // this lane's partial softmax sums
+
+  const int tr_row = q4 * 4 + (c16 >> 2);
+  const int tr_col = 4 * (c16 & 3);
+
+  load_tile(0);
+  store_tile(0);
+  __syncthreads();
+  if (n_kv > 1) load_tile(1);
 
   for (int t = 0; t < n_kv; ++t) {
-    __syncthreads();  // every wave is done reading the previous tile
-#pragma unroll
-    for (int i = 0; i < KU; ++i) {
-      const int u = tid + i * kAttnThreads;
-      *reinterpret_cast<u32x4*>(&sm.k[u / UPR][(u % UPR) * 8]) = kreg[i];
-      *reinterpret_cast<u32x4*>(&sm.v[u / UPR][(u % UPR) * 8]) = vreg[i];
-    }
-    __syncthreads();
-    if (t + 1 < n_kv) load_tile(t + 1);
+    const int cur = t & 1;
 
-    // ---- S^T = K Q^T for 64 keys x 32 queries
+    // ---- S^T = K Q^T for 64 keys x 32 queries (8 independent accumulators)
     f32x4 s[4][2];
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      s[kb][0] = f32x4{0.f, 0.f, 0.f, 0.f};
-      s[kb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int kb = 0; kb < 4; ++kb) s[kb][0] = s[kb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int dc = 0; dc < DC; ++dc) {
-        const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(&sm.k[kb * 16 + c16][dc * 32 + q4 * 8]));
+    for (int dc = 0; dc < DC; ++dc)
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        const bf16x8 a = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u32x4*>(&sm.k[cur][kb * 16 + c16][dc * 32 + q4 * 8]));
         s[kb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[0][dc], s[kb][0], 0, 0, 0);
         s[kb][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[1][dc], s[kb][1], 0, 0, 0);
       }
-    }
 
-    // ---- causal mask + online softmax (per query column). Scores stay
-    // unscaled until the exponent: p = 2^(s*c - m*c), c = scale*log2(e) > 0.
+    // ---- causal mask (only tiles that reach past some row of this wave)
     const int j0 = t * kKT;
     if (j0 + kKT - 1 > wave_pmin) {
 #pragma unroll
@@ -194,6 +221,8 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
           for (int i = 0; i < 4; ++i)
             if (j0 + kb * 16 + q4 * 4 + i > pos[nb]) s[kb][nb][i] = -INFINITY;
     }
+
+    // ---- online softmax per query column: p = 2^(s*c - m*c), c = scale*log2(e)
     bf16x8 pb[2][2];
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
@@ -203,16 +232,16 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
         mx = fmaxf(mx, fmaxf(fmaxf(s[kb][nb][0], s[kb][nb][1]), fmaxf(s[kb][nb][2], s[kb][nb][3])));
       mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float m_new = fmaxf(m_run[nb], mx);
-      // a query always sees key 0 in the first tile, so m_new is finite
-      const float mc = m_new * scale_log2e;
-      if (__ballot(m_new > m_run[nb]) != 0) {
-        const float alpha = __builtin_amdgcn_exp2f(m_run[nb] * scale_log2e - mc);
+      // a query sees key 0 in the first tile, so the reference max is finite after it
+      if (__ballot(mx * scale_log2e - m_run[nb] * scale_log2e > kLazy) != 0) {
+        const float m_new = fmaxf(m_run[nb], mx);
+        const float alpha = __builtin_amdgcn_exp2f((m_run[nb] - m_new) * scale_log2e);
         l_run[nb] *= alpha;
 #pragma unroll
         for (int db = 0; db < DB; ++db) o[db][nb] *= alpha;
         m_run[nb] = m_new;
       }
+      const float mc = m_run[nb] * scale_log2e;
       float ls = 0.f;
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
@@ -233,22 +262,26 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
       }
     }
 
-    // ---- O^T += V^T P^T
-    // A operand V^T: lane (c16, q4) needs dim db*16 + c16 of keys
-    // kc*32 + q4*4 + {0..3} and kc*32 + 16 + q4*4 + {0..3}, the key order of
-    // the P^T operand built above.
-    const int tr_row = q4 * 4 + (c16 >> 2);
-    const int tr_col = 4 * (c16 & 3);
+    // ---- O^T += V^T P^T. A operand: lane (c16, q4) needs dim db*16 + c16 of
+    // keys kc*32 + q4*4 + {0..3} and kc*32 + 16 + q4*4 + {0..3}: the key
+    // order of the P^T operand above.
 #pragma unroll
-    for (int db = 0; db < DB; ++db)
+    for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
-      for (int kc = 0; kc < 2; ++kc) {
-        const u32x2 lo = lds_read_tr4(&sm.v[kc * 32 + tr_row][db * 16 + tr_col]);
-        const u32x2 hi = lds_read_tr4(&sm.v[kc * 32 + 16 + tr_row][db * 16 + tr_col]);
+      for (int db = 0; db < DB; ++db) {
+        const u32x2 lo = lds_read_tr4(&sm.v[cur][kc * 32 + tr_row][db * 16 + tr_col]);
+        const u32x2 hi = lds_read_tr4(&sm.v[cur][kc * 32 + 16 + tr_row][db * 16 + tr_col]);
         const bf16x8 a = __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
         o[db][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][0], o[db][0], 0, 0, 0);
         o[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][1], o[db][1], 0, 0, 0);
       }
+
+    // ---- stage the next tile into the other buffer, prefetch the one after
+    if (t + 1 < n_kv) {
+      store_tile(cur ^ 1);
+      if (t + 2 < n_kv) load_tile(t + 2);
+    }
+    __syncthreads();
   }
 
   // ---- normalise and store: lane holds dims db*16 + q4*4 .. +3 of its query
@@ -356,23 +389,22 @@ extern "C" int rc_selective_attention(const rc_shape* shape, const void* q, cons
     if (kM % G != 0) return fail(RC_ERR_UNSUPPORTED, "group size Hq/Hkv=%d must divide %d", G, kM);
     const int BR = kM / G;
     const int n_tiles = (R + BR - 1) / BR;
-    const int64_t total = static_cast<int64_t>(n_tiles) * B * Hkv;
-    const int64_t per_xcd = (total + kXcds - 1) / kXcds;
-    if (per_xcd * kXcds > 0x7fffffff) return fail(RC_ERR_UNSUPPORTED, "grid too large");
+    const int n_groups = B * Hkv;
+    const int gpx = (n_groups + kXcds - 1) / kXcds;   // groups per XCD
+    const int64_t blocks = static_cast<int64_t>(kXcds) * gpx * n_tiles;
+    if (blocks > 0x7fffffff) return fail(RC_ERR_UNSUPPORTED, "grid too large");
     const float scale_log2e = static_cast<float>(static_cast<double>(scale) * 1.4426950408889634);
-    dim3 grid(static_cast<unsigned>(per_xcd * kXcds));
+    dim3 grid(static_cast<unsigned>(blocks));
     if (D == 128)
       hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, dim3(kAttnThreads), 0, stream,
                          static_cast<const uint16_t*>(q), rows, R, N, Hq, Hkv, G, BR,
                          static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
-                         scale_log2e, static_cast<uint16_t*>(out), n_tiles, static_cast<int>(total),
-                         static_cast<int>(per_xcd));
+                         scale_log2e, static_cast<uint16_t*>(out), n_tiles, n_groups, gpx);
     else
       hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, dim3(kAttnThreads), 0, stream,
                          static_cast<const uint16_t*>(q), rows, R, N, Hq, Hkv, G, BR,
                          static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
-                         scale_log2e, static_cast<uint16_t*>(out), n_tiles, static_cast<int>(total),
-                         static_cast<int>(per_xcd));
+                         scale_log2e, static_cast<uint16_t*>(out), n_tiles, n_groups, gpx);
   } else {
     const int64_t total = static_cast<int64_t>(B) * R * Hq;
     const int64_t blocks = (total + 3) / 4;

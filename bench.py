@@ -5,8 +5,8 @@ one MI355X.
 A step is one pass of the whole path over one batch of synthetic
 recommendation prompts already resident in HBM, on one stream:
   rc_kv_assemble          gather of history/item KV blocks + fused RoPE
-                          re-alignment
-  rc_select_tokens        K deviation score, top-k, heavy-hitter patch
+                          re-alignment + K deviation score
+  rc_select_tokens        top-k, heavy-hitter patch
   rc_selective_attention  causal GQA attention of the fresh + selected rows
 Batches rotate (default 4 independent draws over one shared pool) so the
 working set exceeds the 256 MB Infinity Cache.
@@ -133,11 +133,12 @@ def main():
         w, segs, bufs = batches[i % len(batches)]
         if ev is not None:
             ev[0].record(stream)
-        ops.kv_assemble(w.pools, segs, w.k_fresh, w.v_fresh, cos, sin, bufs.k_asm, bufs.v_asm)
+        ops.kv_assemble(w.pools, segs, w.k_fresh, w.v_fresh, cos, sin, bufs.k_asm, bufs.v_asm,
+                        scores_out=bufs.scores)
         if ev is not None:
             ev[1].record(stream)
         ops.select_tokens(segs, k, w.k_fresh, w.v_fresh, bufs.k_asm, bufs.v_asm,
-                          scores_out=bufs.scores, rows_out=bufs.rows, patch=True)
+                          scores_in=bufs.scores, rows_out=bufs.rows, patch=True)
         if ev is not None:
             ev[2].record(stream)
         if R > 0:
@@ -174,14 +175,17 @@ def main():
     att_ms = sum(e[2].elapsed_time(e[3]) for e in evs) / args.steps
     flops = sum(att_flops[(args.warmup + i) % len(batches)] for i in range(args.steps)) / args.steps
 
-    gather_bytes = 4.0 * B * N * row                       # read K,V rows + write K,V rows
-    select_bytes = 2.0 * B * N * row + 12.0 * B * N + 4.0 * B * R + 4.0 * B * k * row
+    # assemble: read K,V rows, write K,V rows, read the fresh K row of every
+    # cached position and write its score; select: read scores, write rows,
+    # patch k rows of K and V (read fresh, write assembled)
+    gather_bytes = 4.0 * B * N * row + 1.0 * B * (N - cfg.n_fresh) * row + 4.0 * B * N
+    select_bytes = 4.0 * B * N + 4.0 * B * R + 4.0 * B * k * row
     mfma_peak = BF16_PEAK_TFLOPS if cfg.dtype == "bf16" else F32_PEAK_TFLOPS
 
     def hbm(bytes_, ms):
         a = bytes_ / (ms * 1e-3) / 1e9 if ms > 0 else 0.0
         return {"bound": "hbm", "achieved": round(a, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(a / HBM_PEAK_GBS, 4), "bytes_per_launch": gather_bytes if bytes_ is gather_bytes else bytes_}
+                "frac": round(a / HBM_PEAK_GBS, 4), "bytes_per_launch": bytes_}
 
     att_tf = flops / (att_ms * 1e-3) / 1e12 if att_ms > 0 else 0.0
     kernels = {

@@ -122,14 +122,19 @@ int rc_rope_table(int32_t max_pos, int32_t D, double base, float* cos_out, float
  * rope_cos/rope_sin NULL: plain gather, no rotation (then max_pos is
  * ignored); otherwise both must be given with max_pos >= N.
  * pools: host array of n_pools rc_pool (1..8). segs: device [B, S].
- * k_fresh/v_fresh: device [B, N, Hkv, D]; only rows of fresh segments are
- * read. k_asm/v_asm: device [B, N, Hkv, D] outputs (must not alias inputs).
+ * k_fresh/v_fresh: device [B, N, Hkv, D]; rows of fresh segments are copied.
+ * k_asm/v_asm: device [B, N, Hkv, D] outputs (must not alias inputs).
+ * scores_out: NULL, or device [B, N] fp32: the same pass then also reads the
+ * fresh K row of every cached position and writes the deviation score of
+ * Eq. (3) (M = K, lambda = 1) of the row it produced, exactly as
+ * rc_select_tokens step 1 defines it (fp32 accumulation; 0 at fresh
+ * positions), so that rc_select_tokens can take it as scores_in.
  * Errors: INVALID_ARG for NULL pointers, bad shape, bad pool, S < 1 or
  * max_pos < N with tables given; UNSUPPORTED for D, dtype, S > 1024. */
 int rc_kv_assemble(const rc_shape* shape, const rc_pool* pools, int32_t n_pools,
                    const rc_segment* segs, int32_t S, const void* k_fresh, const void* v_fresh,
                    const float* rope_cos, const float* rope_sin, int32_t max_pos, void* k_asm,
-                   void* v_asm, hipStream_t stream);
+                   void* v_asm, float* scores_out, hipStream_t stream);
 
 /* Standalone alignment (Sec. III-C.3 (ii)), in place: K[b,i] <- R(delta[b,i])
  * K[b,i] with the same fp32 operation order as rc_kv_assemble; a negative

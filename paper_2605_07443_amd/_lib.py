@@ -54,7 +54,8 @@ def load() -> ctypes.CDLL:
     vp, i32, f32, f64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float, ctypes.c_double
     P = ctypes.POINTER
     L.rc_rope_table.argtypes = [i32, i32, f64, vp, vp]
-    L.rc_kv_assemble.argtypes = [P(RcShape), P(RcPool), i32, vp, i32, vp, vp, vp, vp, i32, vp, vp, vp]
+    L.rc_kv_assemble.argtypes = [P(RcShape), P(RcPool), i32, vp, i32, vp, vp, vp, vp, i32, vp, vp, vp,
+                                 vp]
     L.rc_rerope.argtypes = [P(RcShape), vp, vp, vp, vp, i32, vp]
     L.rc_select_tokens.argtypes = [P(RcShape), vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, i32, vp]
     L.rc_selective_attention.argtypes = [P(RcShape), vp, vp, i32, vp, vp, f32, vp, vp]

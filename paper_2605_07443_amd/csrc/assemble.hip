@@ -3,9 +3,10 @@
 // (i) and (ii); logical-to-physical block mapping of Sec. III-A).
 //
 // Both are HBM-bound copies. A workgroup of 256 threads owns TOK consecutive
-// positions of one request (TOK * row = 32 KiB of K+V reads): it first
+// positions of one request (TOK * key row = 16 KiB): it first
 // resolves each position to its source row (binary search of the request's
-// segment table staged in LDS), then streams 16-byte units. A key unit pairs
+// segment table staged in LDS), then streams 16-byte units with non-temporal
+// loads and stores (the fastest copy form measured on MI355X). A key unit pairs
 // element block [j, j+E) of a head with [j+D/2, j+D/2+E) so the rotation of
 // the pairs (j, j+D/2) happens in registers between the load and the store.
 #include "rc_common.h"
@@ -17,7 +18,11 @@ using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
 constexpr int kMaxTok = 256;      // positions per workgroup (small rows)
-constexpr int kRowBytesPerWg = 32768;
+constexpr int kKPer = 2;                 // key pairs per thread per pass
+constexpr int kVPer = 4;                 // value units per thread per pass
+constexpr int kKItems = kKPer * kThreads;   // key pairs per pass
+constexpr int kVItems = kVPer * kThreads;   // value units per pass
+constexpr int kRowBytesPerWg = kKItems * 32;  // key-row bytes of a workgroup (16 KiB)
 
 // Rotate E = 16/ES elements of the first half (a) and second half (b) of a
 // head by the angle whose cos/sin are c[0..E), s[0..E).
@@ -56,34 +61,41 @@ __device__ __forceinline__ void rotate_unit(u32x4& a, u32x4& b, const float* c, 
 // ASSEMBLE: source rows come from the segment table (pool block or fresh
 // row), V is copied as well, delta = dst_start for pool rows when tables are
 // given. REROPE (in place): source = destination = k, delta from the array.
-template <int ES, bool ASSEMBLE>
+// SCORE (with ASSEMBLE): also reads the fresh K row of every cached position
+// and writes the deviation score sum |K_fresh - K_asm| of the row it just
+// produced (0 at fresh positions, whose assembled row is the fresh row).
+// Every load of a workgroup's 16-byte units is issued before the first use.
+template <int ES, bool ASSEMBLE, bool SCORE>
 __global__ __launch_bounds__(kThreads) void kv_rows_kernel(
     PoolArgs pools, const int4* __restrict__ segs, int S, int N, int tok_per_wg, int row_units,
     int head_units, const char* __restrict__ k_fresh, const char* __restrict__ v_fresh,
     const int32_t* __restrict__ delta_arr, const float* __restrict__ cos_t,
     const float* __restrict__ sin_t, int max_pos, int half, char* __restrict__ k_out,
-    char* __restrict__ v_out) {
+    char* __restrict__ v_out, float* __restrict__ scores) {
   constexpr int E = 16 / ES;  // elements per 16-byte unit
   __shared__ int4 s_segs[ASSEMBLE ? kMaxSegments : 1];
   __shared__ const char* s_srck[kMaxTok];
   __shared__ const char* s_srcv[kMaxTok];
   __shared__ int s_delta[kMaxTok];
+  __shared__ int s_cached[SCORE ? kMaxTok : 1];
+  __shared__ float s_part[SCORE ? kKItems : 1];
 
   const int b = blockIdx.y;
   const int i0 = blockIdx.x * tok_per_wg;
   const int tok_cnt = min(tok_per_wg, N - i0);
   const size_t row_bytes = static_cast<size_t>(row_units) * 16;
+  const int tid = threadIdx.x;
 
   if constexpr (ASSEMBLE) {
-    for (int s = threadIdx.x; s < S; s += kThreads) s_segs[s] = segs[static_cast<size_t>(b) * S + s];
+    for (int s = tid; s < S; s += kThreads) s_segs[s] = segs[static_cast<size_t>(b) * S + s];
     __syncthreads();
   }
-  for (int t = threadIdx.x; t < tok_cnt; t += kThreads) {
+  for (int t = tid; t < tok_cnt; t += kThreads) {
     const int i = i0 + t;
     const size_t row_off = (static_cast<size_t>(b) * N + i) * row_bytes;
     const char* sk = nullptr;
     const char* sv = nullptr;
-    int d = 0;
+    int d = 0, cached = 0;
     if constexpr (ASSEMBLE) {
       const int s = find_segment(s_segs, S, i);
       if (s >= 0) {
@@ -96,6 +108,7 @@ __global__ __launch_bounds__(kThreads) void kv_rows_kernel(
           const size_t src = (static_cast<size_t>(g.w) * pools.block_len[g.z] + (i - g.x)) * row_bytes;
           sk = pools.k[g.z] + src;
           sv = pools.v[g.z] + src;
+          cached = 1;
           if (cos_t != nullptr && g.x < max_pos) d = g.x;
         }
       }
@@ -109,81 +122,112 @@ __global__ __launch_bounds__(kThreads) void kv_rows_kernel(
     s_srck[t] = sk;
     s_srcv[t] = sv;
     s_delta[t] = d;
+    if constexpr (SCORE) s_cached[t] = cached;
   }
   __syncthreads();
 
-  // ---- keys: pairs of units (first half, second half of a head)
   const int pairs_per_row = row_units / 2;
   const int half_units = head_units / 2;
   const int k_items = tok_cnt * pairs_per_row;
-  for (int base = threadIdx.x; base < k_items; base += kThreads * 4) {
-    u32x4 ua[4], ub[4];
-    int tok[4], unit[4];
-    bool ok[4];
+  const int v_items = ASSEMBLE ? tok_cnt * row_units : 0;
+  for (int it = 0; it * kKItems < k_items || it * kVItems < v_items; ++it) {
+    // ---- issue every load: key pairs (+ fresh key pairs), value units
+    u32x4 ua[kKPer], ub[kKPer], fa[kKPer], fb[kKPer], vv[kVPer];
+    int ktok[kKPer], kunit[kKPer], vtok[kVPer], vunit[kVPer];
+    bool kok[kKPer], fok[kKPer], vok[kVPer];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int idx = base + u * kThreads;
-      ok[u] = idx < k_items;
-      tok[u] = ok[u] ? idx / pairs_per_row : 0;
-      const int pr = idx - tok[u] * pairs_per_row;
+    for (int u = 0; u < kKPer; ++u) {
+      const int idx = it * kKItems + u * kThreads + tid;
+      kok[u] = idx < k_items;
+      ktok[u] = kok[u] ? idx / pairs_per_row : 0;
+      const int pr = idx - ktok[u] * pairs_per_row;
       const int head = pr / half_units;
-      unit[u] = head * head_units + (pr - head * half_units);
-      ok[u] = ok[u] && s_srck[tok[u]] != nullptr;
-      if (ok[u]) {
-        const u32x4* src = reinterpret_cast<const u32x4*>(s_srck[tok[u]]);
+      kunit[u] = head * head_units + (pr - head * half_units);
+      kok[u] = kok[u] && s_srck[ktok[u]] != nullptr;
+      fok[u] = false;
+      if (kok[u]) {
+        const u32x4* src = reinterpret_cast<const u32x4*>(s_srck[ktok[u]]);
         if constexpr (ASSEMBLE) {
-          ua[u] = __builtin_nontemporal_load(src + unit[u]);
-          ub[u] = __builtin_nontemporal_load(src + unit[u] + half_units);
+          ua[u] = __builtin_nontemporal_load(src + kunit[u]);
+          ub[u] = __builtin_nontemporal_load(src + kunit[u] + half_units);
         } else {
-          ua[u] = src[unit[u]];
-          ub[u] = src[unit[u] + half_units];
+          ua[u] = src[kunit[u]];
+          ub[u] = src[kunit[u] + half_units];
+        }
+        if constexpr (SCORE) {
+          fok[u] = s_cached[ktok[u]] != 0;
+          if (fok[u]) {
+            const u32x4* fr = reinterpret_cast<const u32x4*>(
+                k_fresh + (static_cast<size_t>(b) * N + i0 + ktok[u]) * row_bytes);
+            fa[u] = __builtin_nontemporal_load(fr + kunit[u]);
+            fb[u] = __builtin_nontemporal_load(fr + kunit[u] + half_units);
+          }
         }
       }
     }
+    if constexpr (ASSEMBLE) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      if (!ok[u]) continue;
-      const int d = s_delta[tok[u]];
-      if (d != 0) {
-        const int a = d < 0 ? -d : d;
-        const int j0 = (unit[u] % head_units) * E;  // element offset in the half
-        float c[E], s[E];
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-          c[e] = cos_t[static_cast<size_t>(a) * half + j0 + e];
-          const float sv = sin_t[static_cast<size_t>(a) * half + j0 + e];
-          s[e] = d < 0 ? -sv : sv;
-        }
-        rotate_unit<ES>(ua[u], ub[u], c, s);
+      for (int u = 0; u < kVPer; ++u) {
+        const int idx = it * kVItems + u * kThreads + tid;
+        vok[u] = idx < v_items;
+        vtok[u] = vok[u] ? idx / row_units : 0;
+        vunit[u] = idx - vtok[u] * row_units;
+        vok[u] = vok[u] && s_srcv[vtok[u]] != nullptr;
+        if (vok[u]) vv[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(s_srcv[vtok[u]]) + vunit[u]);
       }
-      u32x4* dst = reinterpret_cast<u32x4*>(k_out + (static_cast<size_t>(b) * N + i0 + tok[u]) * row_bytes);
-      dst[unit[u]] = ua[u];
-      dst[unit[u] + half_units] = ub[u];
+    }
+
+    // ---- keys: rotate, store, deviation partials
+#pragma unroll
+    for (int u = 0; u < kKPer; ++u) {
+      if (kok[u]) {
+        const int d = s_delta[ktok[u]];
+        if (d != 0) {
+          const int a = d < 0 ? -d : d;
+          const int j0 = (kunit[u] % head_units) * E;  // element offset in the half
+          float c[E], sn[E];
+#pragma unroll
+          for (int e = 0; e < E; ++e) {
+            c[e] = cos_t[static_cast<size_t>(a) * half + j0 + e];
+            const float sv = sin_t[static_cast<size_t>(a) * half + j0 + e];
+            sn[e] = d < 0 ? -sv : sv;
+          }
+          rotate_unit<ES>(ua[u], ub[u], c, sn);
+        }
+        u32x4* dst = reinterpret_cast<u32x4*>(k_out + (static_cast<size_t>(b) * N + i0 + ktok[u]) * row_bytes);
+        if constexpr (ASSEMBLE) {
+          __builtin_nontemporal_store(ua[u], dst + kunit[u]);
+          __builtin_nontemporal_store(ub[u], dst + kunit[u] + half_units);
+        } else {
+          dst[kunit[u]] = ua[u];
+          dst[kunit[u] + half_units] = ub[u];
+        }
+      }
+      if constexpr (SCORE) {
+        const int idx = u * kThreads + tid;  // a single iteration when scoring
+        if (idx < k_items)
+          s_part[idx] = fok[u] ? absdiff_sum<ES>(fa[u], ua[u]) + absdiff_sum<ES>(fb[u], ub[u]) : 0.f;
+      }
+    }
+    if constexpr (ASSEMBLE) {
+#pragma unroll
+      for (int u = 0; u < kVPer; ++u) {
+        if (!vok[u]) continue;
+        u32x4* dst = reinterpret_cast<u32x4*>(v_out + (static_cast<size_t>(b) * N + i0 + vtok[u]) * row_bytes);
+        __builtin_nontemporal_store(vv[u], dst + vunit[u]);
+      }
     }
   }
 
-  if constexpr (ASSEMBLE) {
-    // ---- values: plain 16-byte copies
-    const int v_items = tok_cnt * row_units;
-    for (int base = threadIdx.x; base < v_items; base += kThreads * 8) {
-      u32x4 val[8];
-      int tok[8], unit[8];
-      bool ok[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int idx = base + u * kThreads;
-        ok[u] = idx < v_items;
-        tok[u] = ok[u] ? idx / row_units : 0;
-        unit[u] = idx - tok[u] * row_units;
-        ok[u] = ok[u] && s_srcv[tok[u]] != nullptr;
-        if (ok[u]) val[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(s_srcv[tok[u]]) + unit[u]);
-      }
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        if (!ok[u]) continue;
-        u32x4* dst = reinterpret_cast<u32x4*>(v_out + (static_cast<size_t>(b) * N + i0 + tok[u]) * row_bytes);
-        dst[unit[u]] = val[u];
-      }
+  if constexpr (SCORE) {
+    // one wave per position: fixed-order sum of its key-pair partials
+    __syncthreads();
+    const int lane = tid & 63;
+    for (int t = tid >> 6; t < tok_cnt; t += kThreads / 64) {
+      float x = 0.f;
+      for (int j = lane; j < pairs_per_row; j += 64) x += s_part[t * pairs_per_row + j];
+      x = wave_sum(x);
+      if (lane == 0) scores[static_cast<size_t>(b) * N + i0 + t] = x;
     }
   }
 }
@@ -196,24 +240,33 @@ int tokens_per_wg(int row_bytes) {
 template <bool ASSEMBLE>
 int launch_rows(const rc_shape* s, const PoolArgs& pools, const int4* segs, int S,
                 const void* k_fresh, const void* v_fresh, const int32_t* delta, const float* cos_t,
-                const float* sin_t, int max_pos, void* k_out, void* v_out, hipStream_t stream) {
+                const float* sin_t, int max_pos, void* k_out, void* v_out, float* scores,
+                hipStream_t stream) {
   const int es = elem_size(s->dtype);
   const int row_bytes = s->Hkv * s->D * es;
   const int row_units = row_bytes / 16;
   const int head_units = s->D * es / 16;
-  const int tok = tokens_per_wg(ASSEMBLE ? row_bytes : row_bytes / 2);
+  const int tok = tokens_per_wg(row_bytes);
+  if (scores && tok * (row_units / 2) > kKItems)
+    return fail(RC_ERR_UNSUPPORTED, "scoring needs a key row of at most %d bytes", kRowBytesPerWg);
   dim3 grid((s->N + tok - 1) / tok, s->B);
   if (grid.y > 65535) return fail(RC_ERR_UNSUPPORTED, "B=%d exceeds 65535", s->B);
   auto args = [&](auto kern) {
     hipLaunchKernelGGL(kern, grid, dim3(kThreads), 0, stream, pools, segs, S, s->N, tok, row_units,
                        head_units, static_cast<const char*>(k_fresh),
                        static_cast<const char*>(v_fresh), delta, cos_t, sin_t, max_pos, s->D / 2,
-                       static_cast<char*>(k_out), static_cast<char*>(v_out));
+                       static_cast<char*>(k_out), static_cast<char*>(v_out), scores);
   };
-  if (s->dtype == RC_BF16)
-    args(kv_rows_kernel<2, ASSEMBLE>);
-  else
-    args(kv_rows_kernel<4, ASSEMBLE>);
+  if (!ASSEMBLE) {
+    if (s->dtype == RC_BF16) args(kv_rows_kernel<2, false, false>);
+    else args(kv_rows_kernel<4, false, false>);
+  } else if (scores) {
+    if (s->dtype == RC_BF16) args(kv_rows_kernel<2, true, true>);
+    else args(kv_rows_kernel<4, true, true>);
+  } else {
+    if (s->dtype == RC_BF16) args(kv_rows_kernel<2, true, false>);
+    else args(kv_rows_kernel<4, true, false>);
+  }
   return check_launch(ASSEMBLE ? "rc_kv_assemble" : "rc_rerope");
 }
 
@@ -223,7 +276,8 @@ int launch_rows(const rc_shape* s, const PoolArgs& pools, const int4* segs, int 
 extern "C" int rc_kv_assemble(const rc_shape* shape, const rc_pool* pools, int32_t n_pools,
                               const rc_segment* segs, int32_t S, const void* k_fresh,
                               const void* v_fresh, const float* rope_cos, const float* rope_sin,
-                              int32_t max_pos, void* k_asm, void* v_asm, hipStream_t stream) {
+                              int32_t max_pos, void* k_asm, void* v_asm, float* scores_out,
+                              hipStream_t stream) {
   using namespace rc;
   clear_error();
   if (int st = check_shape(shape, false)) return st;
@@ -252,7 +306,8 @@ extern "C" int rc_kv_assemble(const rc_shape* shape, const rc_pool* pools, int32
     pa.block_len[p] = pools[p].block_len;
   }
   return launch_rows<true>(shape, pa, reinterpret_cast<const int4*>(segs), S, k_fresh, v_fresh,
-                           nullptr, rope_cos, rope_sin, rope_cos ? max_pos : 0, k_asm, v_asm, stream);
+                           nullptr, rope_cos, rope_sin, rope_cos ? max_pos : 0, k_asm, v_asm,
+                           scores_out, stream);
 }
 
 extern "C" int rc_rerope(const rc_shape* shape, void* k, const int32_t* delta,
@@ -266,5 +321,5 @@ extern "C" int rc_rerope(const rc_shape* shape, void* k, const int32_t* delta,
   if (max_pos < 1) return fail(RC_ERR_INVALID_ARG, "max_pos=%d must be >= 1", max_pos);
   PoolArgs pa{};
   return launch_rows<false>(shape, pa, nullptr, 0, nullptr, nullptr, delta, rope_cos, rope_sin,
-                            max_pos, k, nullptr, stream);
+                            max_pos, k, nullptr, nullptr, stream);
 }

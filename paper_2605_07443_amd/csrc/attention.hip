@@ -23,6 +23,7 @@
 //     (latest) tiles first across all of its groups.
 // fp32 path: one wave per (request, row, head), fp32 FMA on the vector ALUs.
 #include <cmath>
+#include <type_traits>
 
 #include "rc_common.h"
 
@@ -193,13 +194,18 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
   __syncthreads();
   if (n_kv > 1) load_tile(1);
 
-  for (int t = 0; t < n_kv; ++t) {
+  // One KV tile: S^T = K Q^T, (masked) online softmax, O^T += V^T P^T, then
+  // stage the next tile. MASK selects the causal mask (only tiles reaching past
+  // some row of this wave need it, so the main loop runs without it).
+  auto do_tile = [&](int t, auto mask_tag) {
+    constexpr bool MASK = decltype(mask_tag)::value;
     const int cur = t & 1;
 
-    // ---- S^T = K Q^T for 64 keys x 32 queries (8 independent accumulators)
+    // ---- S^T for 64 keys x 32 queries (8 independent accumulators)
     f32x4 s[4][2];
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) s[kb][0] = s[kb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int dc = 0; dc < DC; ++dc)
 #pragma unroll
@@ -209,10 +215,10 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
         s[kb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[0][dc], s[kb][0], 0, 0, 0);
         s[kb][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[1][dc], s[kb][1], 0, 0, 0);
       }
+    __builtin_amdgcn_s_setprio(0);
 
-    // ---- causal mask (only tiles that reach past some row of this wave)
-    const int j0 = t * kKT;
-    if (j0 + kKT - 1 > wave_pmin) {
+    if constexpr (MASK) {
+      const int j0 = t * kKT;
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
@@ -223,24 +229,32 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
     }
 
     // ---- online softmax per query column: p = 2^(s*c - m*c), c = scale*log2(e)
-    bf16x8 pb[2][2];
+    float mx[2];
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
-      float mx = -INFINITY;
+      float m = -INFINITY;
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
-        mx = fmaxf(mx, fmaxf(fmaxf(s[kb][nb][0], s[kb][nb][1]), fmaxf(s[kb][nb][2], s[kb][nb][3])));
-      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      // a query sees key 0 in the first tile, so the reference max is finite after it
-      if (__ballot(mx * scale_log2e - m_run[nb] * scale_log2e > kLazy) != 0) {
-        const float m_new = fmaxf(m_run[nb], mx);
+        m = fmaxf(m, fmaxf(fmaxf(s[kb][nb][0], s[kb][nb][1]), fmaxf(s[kb][nb][2], s[kb][nb][3])));
+      m = fmaxf(m, __shfl_xor(m, 16, 64));
+      mx[nb] = fmaxf(m, __shfl_xor(m, 32, 64));
+    }
+    // a query sees key 0 in the first tile, so the reference max is finite after it
+    if (__ballot(mx[0] * scale_log2e - m_run[0] * scale_log2e > kLazy ||
+                 mx[1] * scale_log2e - m_run[1] * scale_log2e > kLazy) != 0) {
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) {
+        const float m_new = fmaxf(m_run[nb], mx[nb]);
         const float alpha = __builtin_amdgcn_exp2f((m_run[nb] - m_new) * scale_log2e);
         l_run[nb] *= alpha;
 #pragma unroll
         for (int db = 0; db < DB; ++db) o[db][nb] *= alpha;
         m_run[nb] = m_new;
       }
+    }
+    bf16x8 pb[2][2];
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
       const float mc = m_run[nb] * scale_log2e;
       float ls = 0.f;
 #pragma unroll
@@ -265,6 +279,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
     // ---- O^T += V^T P^T. A operand: lane (c16, q4) needs dim db*16 + c16 of
     // keys kc*32 + q4*4 + {0..3} and kc*32 + 16 + q4*4 + {0..3}: the key
     // order of the P^T operand above.
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
@@ -275,6 +290,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
         o[db][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][0], o[db][0], 0, 0, 0);
         o[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][1], o[db][1], 0, 0, 0);
       }
+    __builtin_amdgcn_s_setprio(0);
 
     // ---- stage the next tile into the other buffer, prefetch the one after
     if (t + 1 < n_kv) {
@@ -282,7 +298,13 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
       if (t + 2 < n_kv) load_tile(t + 2);
     }
     __syncthreads();
-  }
+  };
+
+  // first tile whose last key passes this wave's earliest row
+  const int t_mask = min(n_kv, wave_pmin / kKT);
+  int t = 0;
+  for (; t < t_mask; ++t) do_tile(t, std::false_type{});
+  for (; t < n_kv; ++t) do_tile(t, std::true_type{});
 
   // ---- normalise and store: lane holds dims db*16 + q4*4 .. +3 of its query
 #pragma unroll

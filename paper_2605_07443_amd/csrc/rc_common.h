@@ -76,6 +76,26 @@ __device__ __forceinline__ int wave_min_i(int x) {
   return x;
 }
 
+using u32x4_t = uint32_t __attribute__((ext_vector_type(4)));
+
+// sum over the elements of two 16-byte units of |a - b| (fp32 or bf16 storage)
+template <int ES>
+__device__ __forceinline__ float absdiff_sum(const u32x4_t& a, const u32x4_t& b) {
+  float acc = 0.f;
+  if constexpr (ES == 4) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc += fabsf(__uint_as_float(a[e]) - __uint_as_float(b[e]));
+  } else {
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      acc += fabsf(bf16_to_f32(static_cast<uint16_t>(a[w])) - bf16_to_f32(static_cast<uint16_t>(b[w])));
+      acc += fabsf(bf16_to_f32(static_cast<uint16_t>(a[w] >> 16)) -
+                   bf16_to_f32(static_cast<uint16_t>(b[w] >> 16)));
+    }
+  }
+  return acc;
+}
+
 // Segment of request-local position i: index of the last segment whose
 // dst_start <= i (segments tile [0, N) in increasing order), or -1.
 __device__ __forceinline__ int find_segment(const int4* segs, int S, int i) {

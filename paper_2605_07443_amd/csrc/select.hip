@@ -23,23 +23,6 @@ using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
 constexpr int kDevWaves = 4;
 constexpr int kDevTokPerWave = 4;
 
-template <int ES>
-__device__ __forceinline__ float absdiff_unit(const u32x4& a, const u32x4& b) {
-  float acc = 0.f;
-  if constexpr (ES == 4) {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) acc += fabsf(__uint_as_float(a[e]) - __uint_as_float(b[e]));
-  } else {
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      acc += fabsf(bf16_to_f32(static_cast<uint16_t>(a[w])) - bf16_to_f32(static_cast<uint16_t>(b[w])));
-      acc += fabsf(bf16_to_f32(static_cast<uint16_t>(a[w] >> 16)) -
-                   bf16_to_f32(static_cast<uint16_t>(b[w] >> 16)));
-    }
-  }
-  return acc;
-}
-
 // d[t] = sum |k_fresh[t] - k_asm[t]| over the row of t (t = b*N + i).
 template <int ES>
 __global__ __launch_bounds__(64 * kDevWaves) void deviation_kernel(
@@ -64,7 +47,7 @@ __global__ __launch_bounds__(64 * kDevWaves) void deviation_kernel(
     }
 #pragma unroll
     for (int r = 0; r < kDevTokPerWave; ++r)
-      if (t0 + r < rows && u < row_units) acc[r] += absdiff_unit<ES>(a[r], c[r]);
+      if (t0 + r < rows && u < row_units) acc[r] += absdiff_sum<ES>(a[r], c[r]);
   }
 #pragma unroll
   for (int r = 0; r < kDevTokPerWave; ++r) {
@@ -79,6 +62,7 @@ constexpr int kTopkThreads = 1024;
 constexpr int kTopkWaves = kTopkThreads / 64;
 constexpr int kBins = 2048;  // 11-bit digits
 constexpr int kDigitBits = 11;
+constexpr int kBinsPerThread = kBins / kTopkThreads;
 
 // Total order on fp32: larger key = larger value; +NaN above +inf.
 __device__ __forceinline__ uint32_t score_key(float f) {
@@ -182,25 +166,28 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
         if (s_cand[i] && key >= lo && key <= hi) atomicAdd(&s_hist[(key - lo) >> shift], 1);
       }
       __syncthreads();
-      // suffix sums from the top bin: each thread owns two adjacent bins,
-      // counted from the highest bin down
-      const int b1 = kBins - 1 - 2 * tid, b0 = b1 - 1;
-      const int c1 = s_hist[b1], c0 = s_hist[b0];
-      int total;
-      const int incl = block_inclusive_scan(c1 + c0, s_wt, total);
-      const int excl = incl - c1 - c0;  // count in bins above b1
-      // the bin where the running count first reaches `need`
-      int sel = -1, above = 0;
-      if (excl < need && excl + c1 >= need) {
-        sel = b1;
-        above = excl;
-      } else if (excl + c1 < need && incl >= need) {
-        sel = b0;
-        above = excl + c1;
+      // suffix sums from the top bin: thread t owns kBinsPerThread adjacent
+      // bins, threads ordered from the highest bins down
+      const int top = kBins - 1 - kBinsPerThread * tid;
+      int cnt[kBinsPerThread];
+      int mine = 0;
+#pragma unroll
+      for (int j = 0; j < kBinsPerThread; ++j) {
+        cnt[j] = s_hist[top - j];
+        mine += cnt[j];
       }
-      if (sel >= 0) {
-        s_bounds[2] = static_cast<uint32_t>(sel);
-        s_bounds[3] = static_cast<uint32_t>(above);
+      int total;
+      int run = block_inclusive_scan(mine, s_wt, total) - mine;  // count in bins above `top`
+      // the bin where the running count first reaches `need`
+      if (run < need && run + mine >= need) {
+#pragma unroll
+        for (int j = 0; j < kBinsPerThread; ++j) {
+          if (run < need && run + cnt[j] >= need) {
+            s_bounds[2] = static_cast<uint32_t>(top - j);
+            s_bounds[3] = static_cast<uint32_t>(run);
+          }
+          run += cnt[j];
+        }
       }
       __syncthreads();
       const uint32_t bin = s_bounds[2];
@@ -364,7 +351,7 @@ extern "C" int rc_select_tokens(const rc_shape* shape, const rc_segment* segs, i
     if (int st = check_launch("rc_select_tokens (top-k)")) return st;
   }
   if (patch && k > 0) {
-    const int rows_per_wg = 16;
+    const int rows_per_wg = 4;  // many small workgroups: the selected rows are scattered
     dim3 grid((R + rows_per_wg - 1) / rows_per_wg, B);
     hipLaunchKernelGGL(patch_kernel, grid, dim3(kPatchThreads), 0, stream, segs4, S, N, rows, R,
                        rows_per_wg, row_units, static_cast<const char*>(k_fresh),

@@ -122,8 +122,9 @@ def _pool_array(pools, dtype, Hkv, D):
 
 
 def kv_assemble(pools, segs: Segments, k_fresh, v_fresh, cos=None, sin=None, k_out=None,
-                v_out=None, stream=None):
-    """rc_kv_assemble: gather + fused re-alignment. Returns (k_asm, v_asm)."""
+                v_out=None, scores_out=None, stream=None):
+    """rc_kv_assemble: gather + fused re-alignment (+ deviation scores into
+    `scores_out` [B, N] fp32 when given). Returns (k_asm, v_asm)."""
     B, N, Hkv, D = k_fresh.shape
     if v_fresh.shape != k_fresh.shape or v_fresh.dtype != k_fresh.dtype:
         raise ValueError("k_fresh and v_fresh must match")
@@ -136,7 +137,8 @@ def kv_assemble(pools, segs: Segments, k_fresh, v_fresh, cos=None, sin=None, k_o
         ctypes.byref(_shape(B, N, 1, Hkv, D, code)), parr, len(pools), _dev(segs.dev, "segs"),
         segs.S, _dev(k_fresh, "k_fresh"), _dev(v_fresh, "v_fresh"),
         None if cos is None else _dev(cos, "cos"), None if sin is None else _dev(sin, "sin"),
-        max_pos, _dev(k_out, "k_out"), _dev(v_out, "v_out"), _stream(stream)))
+        max_pos, _dev(k_out, "k_out"), _dev(v_out, "v_out"),
+        None if scores_out is None else _dev(scores_out, "scores_out"), _stream(stream)))
     return k_out, v_out
 
 
@@ -210,15 +212,17 @@ class PrefillBuffers:
 def selective_prefill(q, k_fresh, v_fresh, pools, segs: Segments, k: int, cos, sin,
                       scale=None, bufs: PrefillBuffers | None = None, stream=None):
     """One layer of selective prefill on one stream: assemble (fused
-    re-alignment) -> score, top-k, patch -> attention of the fresh and selected
-    rows. Returns the buffers (k_asm, v_asm patched, scores, rows, out)."""
+    re-alignment and deviation score) -> top-k, patch -> attention of the fresh
+    and selected rows. Returns the buffers (k_asm, v_asm patched, scores, rows,
+    out)."""
     B, N, Hq, D = q.shape
     Hkv = k_fresh.shape[2]
     R = segs.n_fresh + int(k)
     if bufs is None:
         bufs = PrefillBuffers.alloc(B, N, Hq, Hkv, D, R, q.dtype, q.device)
-    kv_assemble(pools, segs, k_fresh, v_fresh, cos, sin, bufs.k_asm, bufs.v_asm, stream)
-    select_tokens(segs, k, k_fresh, v_fresh, bufs.k_asm, bufs.v_asm, scores_out=bufs.scores,
+    kv_assemble(pools, segs, k_fresh, v_fresh, cos, sin, bufs.k_asm, bufs.v_asm,
+                scores_out=bufs.scores, stream=stream)
+    select_tokens(segs, k, k_fresh, v_fresh, bufs.k_asm, bufs.v_asm, scores_in=bufs.scores,
                   rows_out=bufs.rows, patch=True, stream=stream)
     if R > 0:
         selective_attention(q, bufs.k_asm, bufs.v_asm, bufs.rows, scale, bufs.out, stream)

@@ -60,8 +60,11 @@ def run_stepwise(cfg, w, k: int, device, stride: int = 1, check_attention: bool 
     stats = {}
     segs = ops.prepare_segments(w.segs, cfg.N, w.pools, device)
     cos, sin = ops.rope_table(cfg.N, cfg.D, cfg.rope_base, device)
-    k_asm, v_asm = ops.kv_assemble(w.pools, segs, w.k_fresh, w.v_fresh, cos, sin)
+    fused = torch.empty((cfg.B, cfg.N), dtype=torch.float32, device=device)
+    k_asm, v_asm = ops.kv_assemble(w.pools, segs, w.k_fresh, w.v_fresh, cos, sin,
+                                   scores_out=fused)
     k_pre, v_pre = k_asm.clone(), v_asm.clone()
+    # scores computed by rc_select_tokens' own deviation kernel drive this run
     rows, scores = ops.select_tokens(segs, k, w.k_fresh, w.v_fresh, k_asm, v_asm, patch=True)
     out = ops.selective_attention(w.q, k_asm, v_asm, rows) if rows.shape[1] > 0 else None
     torch.cuda.synchronize()
@@ -78,7 +81,11 @@ def run_stepwise(cfg, w, k: int, device, stride: int = 1, check_attention: bool 
     sc_g = scores.cpu().numpy()
     sc_o = O.deviation(kf, ka_o)
     np.testing.assert_allclose(sc_g, sc_o, rtol=1e-5, atol=1e-5, err_msg="deviation scores")
+    sc_f = fused.cpu().numpy()
+    np.testing.assert_allclose(sc_f, sc_o, rtol=1e-5, atol=1e-5,
+                               err_msg="deviation scores fused into the gather")
     stats["score_rel"] = float(np.max(np.abs(sc_g - sc_o) / np.maximum(np.abs(sc_o), 1e-30)))
+    stats["fused_score_rel"] = float(np.max(np.abs(sc_f - sc_o) / np.maximum(np.abs(sc_o), 1e-30)))
 
     # ---- top-k: bit-exact on identical scores, both ways
     segs_h = w.segs.numpy()
@@ -90,6 +97,10 @@ def run_stepwise(cfg, w, k: int, device, stride: int = 1, check_attention: bool 
                                    patch=False)
     np.testing.assert_array_equal(rows_g2.cpu().numpy(), O.topk(segs_h, cfg.N, k, sc_o),
                                   err_msg="GPU top-k of the oracle scores differs")
+    rows_g3, _ = ops.select_tokens(segs, k, w.k_fresh, w.v_fresh, k_asm, v_asm, scores_in=fused,
+                                   patch=False)
+    np.testing.assert_array_equal(rows_g3.cpu().numpy(), O.topk(segs_h, cfg.N, k, sc_f),
+                                  err_msg="GPU top-k of the fused scores differs")
     stats["rows_agree_own_scores"] = float(np.mean(rows_g == O.topk(segs_h, cfg.N, k, sc_o)))
 
     # ---- (iii) patch: bit-exact

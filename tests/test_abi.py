@@ -91,8 +91,9 @@ def test_assemble_validation(lib):
 
     def call(shape=None, **kw):
         a = dict(ok, **kw)
-        return lib.rc_kv_assemble(_shape() if shape is None else shape, a["pools"], a["n"], a["segs"], a["S"], a["kf"],
-                                  a["vf"], a["cos"], a["sin"], a["max_pos"], a["ka"], a["va"], None)
+        return lib.rc_kv_assemble(_shape() if shape is None else shape, a["pools"], a["n"], a["segs"],
+                                  a["S"], a["kf"], a["vf"], a["cos"], a["sin"], a["max_pos"], a["ka"],
+                                  a["va"], None, None)
 
     assert call(shape=ctypes.cast(0, ctypes.POINTER(_lib.RcShape))) == -1
     assert call(segs=None) == -1

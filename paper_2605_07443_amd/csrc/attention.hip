@@ -74,7 +74,9 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 // in fp32 and bf16, and the O/l rescale is skipped on most tiles.
 constexpr float kLazy = 8.f;
 
-template <int D>
+// SELECTIVE: query rows come from `rows`; otherwise row r is position r
+// (Full-Recompute). Separate instances keep the two modes apart in profiles.
+template <int D, bool SELECTIVE>
 __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict__ rows, int R,
                       int N, int Hq, int Hkv, int G, int BR, const uint16_t* __restrict__ k,
@@ -117,7 +119,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
     valid[nb] = hh < G && r < R;
     int p = 0;
     if (valid[nb]) {
-      p = rows ? rows[static_cast<size_t>(b) * R + r] : r;
+      p = SELECTIVE ? rows[static_cast<size_t>(b) * R + r] : r;
       p = min(max(p, 0), N - 1);
       pmax = max(pmax, p);
       pmin = min(pmin, p);
@@ -417,16 +419,16 @@ extern "C" int rc_selective_attention(const rc_shape* shape, const void* q, cons
     if (blocks > 0x7fffffff) return fail(RC_ERR_UNSUPPORTED, "grid too large");
     const float scale_log2e = static_cast<float>(static_cast<double>(scale) * 1.4426950408889634);
     dim3 grid(static_cast<unsigned>(blocks));
+    auto launch = [&](auto kern) {
+      hipLaunchKernelGGL(kern, grid, dim3(kAttnThreads), 0, stream,
+                         static_cast<const uint16_t*>(q), rows, R, N, Hq, Hkv, G, BR,
+                         static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
+                         scale_log2e, static_cast<uint16_t*>(out), n_tiles, n_groups, gpx);
+    };
     if (D == 128)
-      hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, dim3(kAttnThreads), 0, stream,
-                         static_cast<const uint16_t*>(q), rows, R, N, Hq, Hkv, G, BR,
-                         static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
-                         scale_log2e, static_cast<uint16_t*>(out), n_tiles, n_groups, gpx);
+      rows ? launch(attn_bf16_kernel<128, true>) : launch(attn_bf16_kernel<128, false>);
     else
-      hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, dim3(kAttnThreads), 0, stream,
-                         static_cast<const uint16_t*>(q), rows, R, N, Hq, Hkv, G, BR,
-                         static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
-                         scale_log2e, static_cast<uint16_t*>(out), n_tiles, n_groups, gpx);
+      rows ? launch(attn_bf16_kernel<64, true>) : launch(attn_bf16_kernel<64, false>);
   } else {
     const int64_t total = static_cast<int64_t>(B) * R * Hq;
     const int64_t blocks = (total + 3) / 4;

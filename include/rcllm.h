@@ -128,9 +128,11 @@ int rc_rope_table(int32_t max_pos, int32_t D, double base, float* cos_out, float
  * fresh K row of every cached position and writes the deviation score of
  * Eq. (3) (M = K, lambda = 1) of the row it produced, exactly as
  * rc_select_tokens step 1 defines it (fp32 accumulation; 0 at fresh
- * positions), so that rc_select_tokens can take it as scores_in.
+ * positions), so that rc_select_tokens can take it as scores_in. Scoring
+ * needs a key row (Hkv * D * element size) of at most 8192 bytes.
  * Errors: INVALID_ARG for NULL pointers, bad shape, bad pool, S < 1 or
- * max_pos < N with tables given; UNSUPPORTED for D, dtype, S > 1024. */
+ * max_pos < N with tables given; UNSUPPORTED for D, dtype, S > 1024, or a
+ * key row above 8192 bytes with scores_out. */
 int rc_kv_assemble(const rc_shape* shape, const rc_pool* pools, int32_t n_pools,
                    const rc_segment* segs, int32_t S, const void* k_fresh, const void* v_fresh,
                    const float* rope_cos, const float* rope_sin, int32_t max_pos, void* k_asm,

@@ -3,7 +3,7 @@
 // (i) and (ii); logical-to-physical block mapping of Sec. III-A).
 //
 // Both are HBM-bound copies. A workgroup of 256 threads owns TOK consecutive
-// positions of one request (TOK * key row = 16 KiB): it first
+// positions of one request (TOK * key row = 8 KiB): it first
 // resolves each position to its source row (binary search of the request's
 // segment table staged in LDS), then streams 16-byte units with non-temporal
 // loads and stores (the fastest copy form measured on MI355X). A key unit pairs
@@ -18,11 +18,11 @@ using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
 constexpr int kMaxTok = 256;      // positions per workgroup (small rows)
-constexpr int kKPer = 2;                 // key pairs per thread per pass
-constexpr int kVPer = 4;                 // value units per thread per pass
+constexpr int kKPer = 1;                 // key pairs per thread per pass
+constexpr int kVPer = 2;                 // value units per thread per pass
 constexpr int kKItems = kKPer * kThreads;   // key pairs per pass
 constexpr int kVItems = kVPer * kThreads;   // value units per pass
-constexpr int kRowBytesPerWg = kKItems * 32;  // key-row bytes of a workgroup (16 KiB)
+constexpr int kRowBytesPerWg = kKItems * 32;  // key-row bytes of a workgroup (8 KiB)
 
 // Rotate E = 16/ES elements of the first half (a) and second half (b) of a
 // head by the angle whose cos/sin are c[0..E), s[0..E).
@@ -204,8 +204,8 @@ __global__ __launch_bounds__(kThreads) void kv_rows_kernel(
         }
       }
       if constexpr (SCORE) {
-        const int idx = u * kThreads + tid;  // a single iteration when scoring
-        if (idx < k_items)
+        const int idx = u * kThreads + tid;  // scoring runs a single key pass (it == 0)
+        if (it == 0 && idx < k_items)
           s_part[idx] = fok[u] ? absdiff_sum<ES>(fa[u], ua[u]) + absdiff_sum<ES>(fb[u], ub[u]) : 0.f;
       }
     }

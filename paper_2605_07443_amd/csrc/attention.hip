@@ -19,8 +19,9 @@
 //     tile) with the next tile's global loads in flight during compute.
 //   * Workgroup ids are remapped so that all row tiles of one (request, KV
 //     head) run on the same XCD (ids are dealt round-robin over the 8 XCDs),
-//     sharing its L2 for the K/V stream, and each XCD starts its longest
-//     (latest) tiles first across all of its groups.
+//     sharing its L2 for the K/V stream. Each XCD starts its longest (latest)
+//     tiles first, across all of its groups when the batch's K/V fits the
+//     Infinity Cache, else within chunks of groups that fit its L2.
 // fp32 path: one wave per (request, row, head), fp32 FMA on the vector ALUs.
 #include <cmath>
 #include <type_traits>
@@ -81,7 +82,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
 void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict__ rows, int R,
                       int N, int Hq, int Hkv, int G, int BR, const uint16_t* __restrict__ k,
                       const uint16_t* __restrict__ v, float scale_log2e,
-                      uint16_t* __restrict__ out, int n_tiles, int n_groups, int gpx) {
+                      uint16_t* __restrict__ out, int n_tiles, int n_groups, int gpx, int chunk) {
   constexpr int DC = D / 32;          // 32-wide d chunks (S^T reduction)
   constexpr int DB = D / 16;          // 16-wide d blocks (O^T rows)
   constexpr int UPR = D / 8;          // 16-byte units per K/V head row
@@ -90,12 +91,17 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
   __shared__ AttnSmem<D> sm;
   __shared__ int s_ext[4];
 
-  // ---- work item: XCD-major, longest tiles first across the XCD's groups
+  // ---- work item: XCD-major; the XCD's groups in chunks of `chunk` groups,
+  // longest tiles first within a chunk
   const int hw = blockIdx.x;
   const int xcd = hw % kXcds;
   const int slot = hw / kXcds;
-  const int rank = slot / gpx;
-  const int grp = (slot - rank * gpx) * kXcds + xcd;
+  const int per_chunk = chunk * n_tiles;
+  const int ci = slot / per_chunk;
+  const int in_chunk = slot - ci * per_chunk;
+  const int cg = min(chunk, gpx - ci * chunk);   // groups in this chunk
+  const int rank = in_chunk / cg;
+  const int grp = (ci * chunk + (in_chunk - rank * cg)) * kXcds + xcd;
   if (rank >= n_tiles || grp >= n_groups) return;
   const int tile = n_tiles - 1 - rank;
   const int b = grp / Hkv;
@@ -415,6 +421,14 @@ extern "C" int rc_selective_attention(const rc_shape* shape, const void* q, cons
     const int n_tiles = (R + BR - 1) / BR;
     const int n_groups = B * Hkv;
     const int gpx = (n_groups + kXcds - 1) / kXcds;   // groups per XCD
+    // When the batch's K/V fits the 256 MB Infinity Cache, every group of an
+    // XCD is scheduled longest-tile-first together (load balance); otherwise
+    // groups go in chunks whose K/V fits one XCD's 4 MB L2 (reuse).
+    const double group_bytes = 2.0 * N * D * elem_size(shape->dtype);
+    const double batch_bytes = group_bytes * n_groups;
+    int chunk = gpx;
+    if (batch_bytes > 192.0 * (1 << 20)) chunk = max(1, static_cast<int>((4.0 * (1 << 20)) / group_bytes));
+    chunk = min(chunk, gpx);
     const int64_t blocks = static_cast<int64_t>(kXcds) * gpx * n_tiles;
     if (blocks > 0x7fffffff) return fail(RC_ERR_UNSUPPORTED, "grid too large");
     const float scale_log2e = static_cast<float>(static_cast<double>(scale) * 1.4426950408889634);
@@ -423,7 +437,7 @@ extern "C" int rc_selective_attention(const rc_shape* shape, const void* q, cons
       hipLaunchKernelGGL(kern, grid, dim3(kAttnThreads), 0, stream,
                          static_cast<const uint16_t*>(q), rows, R, N, Hq, Hkv, G, BR,
                          static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
-                         scale_log2e, static_cast<uint16_t*>(out), n_tiles, n_groups, gpx);
+                         scale_log2e, static_cast<uint16_t*>(out), n_tiles, n_groups, gpx, chunk);
     };
     if (D == 128)
       rows ? launch(attn_bf16_kernel<128, true>) : launch(attn_bf16_kernel<128, false>);

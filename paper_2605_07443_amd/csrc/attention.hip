@@ -14,9 +14,11 @@
 //     layout of the second product O^T = V^T P^T, so P never leaves registers;
 //     V is staged key-major in LDS and read with the gfx950 transposed LDS
 //     read (ds_read_b64_tr_b16) straight into the A-operand layout.
-//   * Online softmax in the log2 domain with fp32 running sums and a lazily
-//     raised reference max; K/V tiles double-buffered in LDS (one barrier per
-//     tile) with the next tile's global loads in flight during compute.
+//   * Online softmax in the log2 domain with a lazily raised reference max;
+//     the running denominators are column sums of the bf16 P^T taken on the
+//     matrix cores (ones x P^T), consistent with the P used for O. K/V tiles
+//     are double-buffered in LDS (one barrier per tile) with the next tile's
+//     global loads in flight during compute.
 //   * Workgroup ids are remapped so that all row tiles of one (request, KV
 //     head) run on the same XCD (ids are dealt round-robin over the 8 XCDs),
 //     sharing its L2 for the K/V stream. Each XCD starts its longest (latest)
@@ -192,7 +194,10 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) o[db][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run[2] = {-INFINITY, -INFINITY};  // reference max of the unscaled scores
-  float l_run[2] = {0.f, 0.f};              // this lane's partial softmax sums
+  // softmax denominators on the matrix cores: ones(16x32) x P^T gives the
+  // column sums of P for every query column (all 4 lanes' entries equal)
+  f32x4 l_acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+  const bf16x8 ones = __builtin_bit_cast(bf16x8, u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
 
   const int tr_row = q4 * 4 + (c16 >> 2);
   const int tr_col = 4 * (c16 & 3);
@@ -254,7 +259,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
       for (int nb = 0; nb < 2; ++nb) {
         const float m_new = fmaxf(m_run[nb], mx[nb]);
         const float alpha = __builtin_amdgcn_exp2f((m_run[nb] - m_new) * scale_log2e);
-        l_run[nb] *= alpha;
+        l_acc[nb] *= alpha;
 #pragma unroll
         for (int db = 0; db < DB; ++db) o[db][nb] *= alpha;
         m_run[nb] = m_new;
@@ -264,16 +269,11 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
       const float mc = m_run[nb] * scale_log2e;
-      float ls = 0.f;
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(s[kb][nb][i], scale_log2e, -mc));
-          s[kb][nb][i] = p;
-          ls += p;
-        }
-      l_run[nb] += ls;
+        for (int i = 0; i < 4; ++i)
+          s[kb][nb][i] = __builtin_amdgcn_exp2f(fmaf(s[kb][nb][i], scale_log2e, -mc));
 #pragma unroll
       for (int kc = 0; kc < 2; ++kc) {
         u32x4 w = {pack_bf16x2(s[2 * kc][nb][0], s[2 * kc][nb][1]),
@@ -298,6 +298,11 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
         o[db][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][0], o[db][0], 0, 0, 0);
         o[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][1], o[db][1], 0, 0, 0);
       }
+#pragma unroll
+    for (int kc = 0; kc < 2; ++kc) {
+      l_acc[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[kc][0], l_acc[0], 0, 0, 0);
+      l_acc[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[kc][1], l_acc[1], 0, 0, 0);
+    }
     __builtin_amdgcn_s_setprio(0);
 
     // ---- stage the next tile into the other buffer, prefetch the one after
@@ -317,10 +322,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
   // ---- normalise and store: lane holds dims db*16 + q4*4 .. +3 of its query
 #pragma unroll
   for (int nb = 0; nb < 2; ++nb) {
-    float l = l_run[nb];
-    l += __shfl_xor(l, 16, 64);
-    l += __shfl_xor(l, 32, 64);
-    const float inv = 1.f / l;
+    const float inv = 1.f / l_acc[nb][0];
     if (!valid[nb]) continue;
     uint16_t* orow = out + ((static_cast<size_t>(b) * R + row[nb]) * Hq + head[nb]) * D;
 #pragma unroll

@@ -91,8 +91,8 @@ def main():
     args = parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(each request is independent; sharding is described in DESIGN.md)",
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(requests are independent and would be split across GPUs by request)",
               file=sys.stderr)
         sys.exit(2)
     if args.copy_calibration:

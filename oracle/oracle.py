@@ -11,7 +11,9 @@ Paper passages followed (arXiv 2605.07443):
   * Sec. III-C.3, end-to-end prefill pipeline: (i) assembly, (ii) alignment by
     RoPE rotation, (iii) heavy-hitter update;
   * Sec. III-C.2b and Eq. (3): importance score (deviation term, K only,
-    lambda = 1) and the heavy-hitter top-k;
+    lambda = 1) and the heavy-hitter top-k; the full score (attention mass of
+    the first layer computed in full, K and V divergence, lambda, no divergence
+    for item blocks) with separate history and item budgets (Sec. IV-A);
   * Eq. (1): scaled dot-product attention, causal, grouped-query;
   * Sec. IV-A: Full-Recompute baseline (every row recomputed).
 """
@@ -62,6 +64,17 @@ def lib():
                                               vp, i32, i32, vp, vp, vp, vp, vp, f64,
                                               vp, vp, vp, vp, vp]
         L.rcref_selective_prefill.restype = i32
+        L.rcref_attention_lse.argtypes = [i32, i32, i32, i32, i32, i32, vp, vp, f64, vp]
+        L.rcref_attention_mass.argtypes = [i32, i32, i32, i32, i32, i32, vp, vp, f64, vp]
+        u32 = ctypes.c_uint32
+        L.rcref_score_eq3.argtypes = [i32, i32, i32, i32, i32, vp, i32, u32, f64, vp, vp, vp, vp,
+                                      vp, vp]
+        L.rcref_topk_split.argtypes = [i32, i32, vp, i32, u32, i32, i32, vp, vp]
+        L.rcref_topk_split.restype = i32
+        L.rcref_eq3_select.argtypes = [i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, i32, vp, i32,
+                                       u32, f64, i32, i32, vp, vp, vp, vp, vp, f64, vp, vp, vp,
+                                       vp, vp]
+        L.rcref_eq3_select.restype = i32
         L.rcref_num_threads.argtypes = []
         L.rcref_num_threads.restype = i32
         _lib = L
@@ -215,6 +228,95 @@ def selective_prefill(q, k_fresh, v_fresh, pools, segs, k: int, cos, sin, scale=
     if st != 0:
         raise ValueError("k exceeds the cached positions of a request, or fresh counts differ")
     return dict(k_asm=k_asm, v_asm=v_asm, scores=scores, rows=rows, out=out)
+
+
+def pool_mask(item_pools) -> int:
+    """Bit mask of the pools whose blocks are items (no divergence term)."""
+    m = 0
+    for p in item_pools:
+        m |= 1 << int(p)
+    return m
+
+
+def attention_lse(q, k, scale=None):
+    """Natural log-sum-exp [B, N, Hq] (fp64) of every row's scaled causal scores."""
+    q, k = _c(q), _c(k)
+    B, N, Hq, D = q.shape
+    Hkv = k.shape[2]
+    scale = 1.0 / np.sqrt(D) if scale is None else scale
+    lse = np.empty((B, N, Hq), np.float64)
+    lib().rcref_attention_lse(B, N, Hq, Hkv, D, _dt(q), _p(q), _p(k), float(scale), _p(lse))
+    return lse
+
+
+def attention_mass(q, k, scale=None):
+    """Attention mass [B, Hkv, N] (fp64) each key receives per KV group."""
+    q, k = _c(q), _c(k)
+    B, N, Hq, D = q.shape
+    Hkv = k.shape[2]
+    scale = 1.0 / np.sqrt(D) if scale is None else scale
+    mass = np.empty((B, Hkv, N), np.float64)
+    lib().rcref_attention_mass(B, N, Hq, Hkv, D, _dt(q), _p(q), _p(k), float(scale), _p(mass))
+    return mass
+
+
+def score_eq3(segs, item_mask: int, lam: float, mass, k_fresh, v_fresh, k_asm, v_asm):
+    """Eq. (3) scores [B, N] fp32 from fp32 mass [B, Hkv, N]."""
+    segs = _c(segs, np.int32)
+    k_fresh, v_fresh, k_asm, v_asm = _c(k_fresh), _c(v_fresh), _c(k_asm), _c(v_asm)
+    B, N, Hkv, D = k_fresh.shape
+    mass = _c(mass, np.float32)
+    scores = np.empty((B, N), np.float32)
+    lib().rcref_score_eq3(B, N, Hkv, D, _dt(k_fresh), _p(segs), segs.shape[1], int(item_mask),
+                          float(lam), _p(mass), _p(k_fresh), _p(v_fresh), _p(k_asm), _p(v_asm),
+                          _p(scores))
+    return scores
+
+
+def topk_split(segs, N: int, item_mask: int, k_hist: int, k_item: int, scores):
+    """Separate history / item top-k; rows [B, F + k_hist + k_item] ascending."""
+    segs = _c(segs, np.int32)
+    B, S = segs.shape[:2]
+    F = int(fresh_count(segs)[0])
+    scores = _c(scores, np.float32)
+    rows = np.empty((B, F + k_hist + k_item), np.int32)
+    st = lib().rcref_topk_split(B, N, _p(segs), S, int(item_mask), int(k_hist), int(k_item),
+                                _p(scores), _p(rows))
+    if st != 0:
+        raise ValueError("a budget exceeds its component's cached positions, or fresh counts differ")
+    return rows
+
+
+def eq3_select(q, k_fresh, v_fresh, pools, segs, item_mask: int, lam: float, k_hist: int,
+               k_item: int, cos, sin, scale=None):
+    """Selection by the full Eq. (3) score; returns every intermediate."""
+    q, k_fresh, v_fresh = _c(q), _c(k_fresh), _c(v_fresh)
+    B, N, Hq, D = q.shape
+    Hkv = k_fresh.shape[2]
+    segs = _c(segs, np.int32)
+    S = segs.shape[1]
+    F = int(fresh_count(segs)[0])
+    R = F + int(k_hist) + int(k_item)
+    pools = [(_c(pk), _c(pv)) for pk, pv in pools]
+    n = len(pools)
+    pk_arr = (ctypes.c_void_p * max(n, 1))(*[pk.ctypes.data for pk, _ in pools])
+    pv_arr = (ctypes.c_void_p * max(n, 1))(*[pv.ctypes.data for _, pv in pools])
+    nb = np.array([pk.shape[0] for pk, _ in pools] or [0], np.int32)
+    bl = np.array([pk.shape[1] for pk, _ in pools] or [0], np.int32)
+    scale = 1.0 / np.sqrt(D) if scale is None else scale
+    k_asm = np.empty_like(k_fresh)
+    v_asm = np.empty_like(v_fresh)
+    mass = np.empty((B, Hkv, N), np.float32)
+    scores = np.empty((B, N), np.float32)
+    rows = np.empty((B, R), np.int32)
+    st = lib().rcref_eq3_select(
+        B, N, Hq, Hkv, D, _dt(q), pk_arr, pv_arr, _p(nb), _p(bl), n, _p(segs), S, int(item_mask),
+        float(lam), int(k_hist), int(k_item), _p(q), _p(k_fresh), _p(v_fresh),
+        _p(_c(cos, np.float32)), _p(_c(sin, np.float32)), float(scale), _p(k_asm), _p(v_asm),
+        _p(mass), _p(scores), _p(rows))
+    if st != 0:
+        raise ValueError("a budget exceeds its component's cached positions, or fresh counts differ")
+    return dict(k_asm=k_asm, v_asm=v_asm, mass=mass, scores=scores, rows=rows)
 
 
 # ---------------------------------------------------------------------------

@@ -368,6 +368,181 @@ void rcref_attention(int B, int N, int Hq, int Hkv, int D, int dt,
 }
 
 /* ------------------------------------------------------------------ */
+/* The full importance score of Eq. (3)                                 */
+/* ------------------------------------------------------------------ */
+
+/* Natural log-sum-exp of each row of the first layer's scaled causal scores:
+ * lse[b, p, h] = ln sum_{j <= p} exp(scale * q[b,p,h] . k[b,j,g]), g the KV
+ * head of q-head h. The first layer is computed in full (Sec. III-C.2b), so
+ * every position p = 0 .. N-1 is a row. fp64 throughout. */
+void rcref_attention_lse(int B, int N, int Hq, int Hkv, int D, int dt,
+                         const void* q, const void* k, double scale, double* lse) {
+  int group = Hq / Hkv;
+#pragma omp parallel
+  {
+    double* z = (double*)malloc(sizeof(double) * (size_t)N);
+#pragma omp for collapse(2) schedule(dynamic, 4)
+    for (int b = 0; b < B; ++b) {
+      for (int p = 0; p < N; ++p) {
+        for (int h = 0; h < Hq; ++h) {
+          int g = h / group;
+          size_t qoff = (((size_t)b * N + p) * Hq + h) * D;
+          double m = -INFINITY;
+          for (int j = 0; j <= p; ++j) {
+            size_t koff = (((size_t)b * N + j) * Hkv + g) * D;
+            double dot = 0.0;
+            for (int d = 0; d < D; ++d)
+              dot += (double)load_el(q, dt, qoff + d) * (double)load_el(k, dt, koff + d);
+            z[j] = dot * scale;
+            if (z[j] > m) m = z[j];
+          }
+          double sum = 0.0;
+          for (int j = 0; j <= p; ++j) sum += exp(z[j] - m);
+          lse[((size_t)b * N + p) * Hq + h] = m + log(sum);
+        }
+      }
+    }
+    free(z);
+  }
+}
+
+/* Attention-mass term of Eq. (3). A_j collects the attention weights token j
+ * receives in the first layer, computed in full: weight A[h, p, j] is entry j
+ * of the softmax of row p of q-head h over keys 0..p (Eq. (1)), so token j is
+ * weighted by every row p >= j of every q-head. Its L1 norm is the sum of
+ * those weights (all are >= 0). The mass is returned per KV group g (the
+ * q-heads h with h / (Hq/Hkv) = g): mass[b, g, j] = sum_{h in g} sum_{p >= j}
+ * A[h, p, j], and ||A_j||_1 = sum_g mass[b, g, j]. fp64 throughout. */
+void rcref_attention_mass(int B, int N, int Hq, int Hkv, int D, int dt,
+                          const void* q, const void* k, double scale, double* mass) {
+  int group = Hq / Hkv;
+#pragma omp parallel
+  {
+    double* z = (double*)malloc(sizeof(double) * (size_t)N);
+#pragma omp for collapse(2) schedule(dynamic, 1)
+    for (int b = 0; b < B; ++b) {
+      for (int g = 0; g < Hkv; ++g) {
+        double* col = mass + ((size_t)b * Hkv + g) * N;
+        for (int j = 0; j < N; ++j) col[j] = 0.0;
+        for (int h = g * group; h < (g + 1) * group; ++h) {
+          for (int p = 0; p < N; ++p) {
+            size_t qoff = (((size_t)b * N + p) * Hq + h) * D;
+            double m = -INFINITY;
+            for (int j = 0; j <= p; ++j) {
+              size_t koff = (((size_t)b * N + j) * Hkv + g) * D;
+              double dot = 0.0;
+              for (int d = 0; d < D; ++d)
+                dot += (double)load_el(q, dt, qoff + d) * (double)load_el(k, dt, koff + d);
+              z[j] = dot * scale;
+              if (z[j] > m) m = z[j];
+            }
+            double denom = 0.0;
+            for (int j = 0; j <= p; ++j) denom += exp(z[j] - m);
+            for (int j = 0; j <= p; ++j) col[j] += exp(z[j] - m) / denom;
+          }
+        }
+      }
+    }
+    free(z);
+  }
+}
+
+/* pool of the segment holding position i of request b (-1: fresh) */
+static int pool_of(const rcref_seg* segs, int S, int b, int i) {
+  for (int s = 0; s < S; ++s) {
+    const rcref_seg* g = &segs[(size_t)b * S + s];
+    if (i >= g->dst_start && i < g->dst_start + g->len) return g->pool;
+  }
+  return -1;
+}
+
+/* Importance score of Eq. (3) for every position i:
+ *   S_i = (1 - lambda) ||A_i||_1 + lambda (||K_new,i - K_cached,i||_1 + ||V_new,i - V_cached,i||_1)
+ * with ||A_i||_1 = sum_g mass[b, g, i] (mass as fp32, the form the GPU path
+ * hands over) and the divergence norms over the token's Hkv*D entries of this
+ * layer (new = fresh rows, cached = assembled rows after alignment). For a
+ * token of an item block (its pool's bit set in item_pool_mask) the cached
+ * block is a lexical match and the divergence term is dropped, leaving the
+ * attention term alone (Sec. III-C.2b). At fresh positions the assembled rows
+ * are the fresh rows, so the divergence is 0 there. fp64, stored as fp32. */
+void rcref_score_eq3(int B, int N, int Hkv, int D, int dt, const int32_t* segs_raw, int S,
+                     uint32_t item_pool_mask, double lambda, const float* mass,
+                     const void* k_fresh, const void* v_fresh, const void* k_asm,
+                     const void* v_asm, float* scores) {
+  const rcref_seg* segs = (const rcref_seg*)segs_raw;
+  size_t row = (size_t)Hkv * D;
+#pragma omp parallel for collapse(2) schedule(static)
+  for (int b = 0; b < B; ++b) {
+    for (int i = 0; i < N; ++i) {
+      double attn = 0.0;
+      for (int g = 0; g < Hkv; ++g) attn += (double)mass[((size_t)b * Hkv + g) * N + i];
+      int pool = pool_of(segs, S, b, i);
+      int item = pool >= 0 && ((item_pool_mask >> pool) & 1u);
+      double div = 0.0;
+      if (!item) {
+        size_t base = ((size_t)b * N + i) * row;
+        for (size_t e = 0; e < row; ++e)
+          div += fabs((double)load_el(k_fresh, dt, base + e) - (double)load_el(k_asm, dt, base + e));
+        for (size_t e = 0; e < row; ++e)
+          div += fabs((double)load_el(v_fresh, dt, base + e) - (double)load_el(v_asm, dt, base + e));
+      }
+      scores[(size_t)b * N + i] = (float)((1.0 - lambda) * attn + lambda * div);
+    }
+  }
+}
+
+/* Heavy hitters with separate budgets for the two cached components (the
+ * recompute ratios r_rev for history and r_item for items, Sec. IV-A): the
+ * k_hist largest scores among cached positions of history pools and the
+ * k_item largest among cached positions of item pools (bit set in
+ * item_pool_mask), ties to the lower position in each. Rows are the fresh
+ * positions and both selections in ascending order: rows[b, 0 .. F + k_hist +
+ * k_item). Returns 0, or -1 if a budget exceeds its component's cached
+ * positions in some request or the requests do not share one fresh count. */
+int rcref_topk_split(int B, int N, const int32_t* segs_raw, int S, uint32_t item_pool_mask,
+                     int k_hist, int k_item, const float* scores, int32_t* rows) {
+  const rcref_seg* segs = (const rcref_seg*)segs_raw;
+  int F = fresh_count(segs, S, 0);
+  int R = F + k_hist + k_item;
+  int status = 0;
+  for (int b = 1; b < B; ++b)
+    if (fresh_count(segs, S, b) != F) return -1;
+  cand_t* cand = (cand_t*)malloc(sizeof(cand_t) * (size_t)(N > 0 ? N : 1));
+  unsigned char* take = (unsigned char*)malloc((size_t)(N > 0 ? N : 1));
+  for (int b = 0; b < B && status == 0; ++b) {
+    memset(take, 0, (size_t)N);
+    for (int i = 0; i < N; ++i)
+      if (pool_of(segs, S, b, i) < 0) take[i] = 1;
+    for (int comp = 0; comp < 2; ++comp) {
+      int budget = comp == 0 ? k_hist : k_item;
+      int n = 0;
+      for (int i = 0; i < N; ++i) {
+        int pool = pool_of(segs, S, b, i);
+        if (pool < 0) continue;
+        int item = (item_pool_mask >> pool) & 1u;
+        if (item != comp) continue;
+        cand[n].key = score_key(scores[(size_t)b * N + i]);
+        cand[n].idx = i;
+        ++n;
+      }
+      if (budget > n) {
+        status = -1;
+        break;
+      }
+      qsort(cand, (size_t)n, sizeof(cand_t), cand_cmp);
+      for (int c = 0; c < budget; ++c) take[cand[c].idx] = 1;
+    }
+    if (status != 0) break;
+    int r = 0;
+    for (int i = 0; i < N; ++i)
+      if (take[i]) rows[(size_t)b * R + r++] = i;
+  }
+  free(cand);
+  free(take);
+  return status;
+}
+
+/* ------------------------------------------------------------------ */
 /* The whole pipeline                                                   */
 /* ------------------------------------------------------------------ */
 
@@ -392,5 +567,37 @@ int rcref_selective_prefill(int B, int N, int Hq, int Hkv, int D, int dt,
   if (rcref_topk(B, N, segs, S, k, scores, rows) != 0) return -1;
   rcref_patch(B, N, Hkv, D, dt, segs, S, rows, R, k_fresh, v_fresh, k_asm, v_asm);
   rcref_attention(B, N, Hq, Hkv, D, dt, q, rows, R, k_asm, v_asm, scale, out);
+  return 0;
+}
+
+/* Selection with the full score of Eq. (3) (Sec. III-C.2b): the first layer
+ * is computed in full on the fresh K/V, which gives the attention mass of every
+ * token; the cached blocks are assembled and aligned (steps i, ii); every
+ * position is scored by Eq. (3); the history and item components each select
+ * their own budget; the selected cached positions get fresh K/V (step iii).
+ * mass [B, Hkv, N] and scores [B, N] are returned as fp32, rows [B, F +
+ * k_hist + k_item]. Returns 0, or -1 if a budget exceeds its component. */
+int rcref_eq3_select(int B, int N, int Hq, int Hkv, int D, int dt,
+                     const void* const* pool_k, const void* const* pool_v,
+                     const int32_t* pool_num_blocks, const int32_t* pool_block_len, int n_pools,
+                     const int32_t* segs, int S, uint32_t item_pool_mask, double lambda,
+                     int k_hist, int k_item, const void* q, const void* k_fresh,
+                     const void* v_fresh, const float* cos_tab, const float* sin_tab,
+                     double scale, void* k_asm, void* v_asm, float* mass, float* scores,
+                     int32_t* rows) {
+  int F = fresh_count((const rcref_seg*)segs, S, 0);
+  int R = F + k_hist + k_item;
+  size_t nm = (size_t)B * Hkv * N;
+  double* m64 = (double*)malloc(sizeof(double) * (nm > 0 ? nm : 1));
+  rcref_attention_mass(B, N, Hq, Hkv, D, dt, q, k_fresh, scale, m64);
+  for (size_t e = 0; e < nm; ++e) mass[e] = (float)m64[e];
+  free(m64);
+  rcref_assemble(B, N, Hkv, D, dt, pool_k, pool_v, pool_num_blocks, pool_block_len, n_pools,
+                 segs, S, k_fresh, v_fresh, cos_tab, sin_tab, k_asm, v_asm);
+  rcref_score_eq3(B, N, Hkv, D, dt, segs, S, item_pool_mask, lambda, mass, k_fresh, v_fresh,
+                  k_asm, v_asm, scores);
+  if (rcref_topk_split(B, N, segs, S, item_pool_mask, k_hist, k_item, scores, rows) != 0)
+    return -1;
+  rcref_patch(B, N, Hkv, D, dt, segs, S, rows, R, k_fresh, v_fresh, k_asm, v_asm);
   return 0;
 }

@@ -85,6 +85,22 @@ class Config:
         return self.k_for(self.pct)
 
     @property
+    def n_hist_reused(self) -> int:
+        return self.hist_len
+
+    @property
+    def n_item_reused(self) -> int:
+        return (self.n_items - len(self.miss_items)) * self.item_len
+
+    def k_split(self, pct_hist: int, pct_item: int | None = None) -> tuple:
+        """Separate budgets for the history and item components (recompute
+        ratios r_rev and r_item): (ceil(pct_hist * n_hist / 100),
+        ceil(pct_item * n_item / 100))."""
+        pct_item = pct_hist if pct_item is None else pct_item
+        return ((self.n_hist_reused * pct_hist + 99) // 100,
+                (self.n_item_reused * pct_item + 99) // 100)
+
+    @property
     def R(self) -> int:
         return self.n_fresh + self.k
 
@@ -119,6 +135,10 @@ CONFIGS = {
 }
 
 SWEEP_PCTS = (0, 5, 10, 15, 25, 50, 100)
+
+# Pool 1 holds the item blocks: their cached K/V are lexical matches, so the
+# divergence term of the full importance score is dropped for them.
+ITEM_POOL_MASK = 1 << 1
 
 # Small shapes for tests: several attention tiles, ragged tails, GQA and MHA.
 TEST_CONFIGS = {

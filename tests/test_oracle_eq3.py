@@ -1,0 +1,280 @@
+"""Pins for the oracle's full importance score of Eq. (3) (arXiv 2605.07443,
+Sec. III-C.2b) and the separate history / item budgets (Sec. IV-A): each test
+checks the oracle against a closed form, a library routine, another oracle
+function pinned elsewhere, an invariant, or a brute force on tiny inputs.
+"""
+import dataclasses
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2605_07443_amd import inputs
+
+H = inputs.to_host_bits
+
+
+def _rand(shape, seed, dtype="f32", scale=1.0):
+    x = (np.random.default_rng(seed).standard_normal(shape) * scale).astype(np.float32)
+    return O.f32_to_bf16(x) if dtype == "bf16" else x
+
+
+def _harmonic(n):
+    return sum(1.0 / m for m in range(1, n + 1))
+
+
+# ---------------------------------------------------------------------------
+# log-sum-exp of the first layer's rows
+# ---------------------------------------------------------------------------
+
+def test_lse_closed_forms_and_library():
+    B, N, Hq, Hkv, D = 2, 19, 4, 2, 64
+    q = _rand((B, N, Hq, D), 1)
+    k = _rand((B, N, Hkv, D), 2)
+    # Q = 0: every score is 0, so lse_p = ln(p + 1)
+    lse0 = O.attention_lse(np.zeros_like(q), k)
+    want0 = np.log(np.arange(1, N + 1, dtype=np.float64))[None, :, None]
+    np.testing.assert_allclose(lse0, np.broadcast_to(want0, lse0.shape), rtol=0, atol=1e-12)
+    # torch.logsumexp of the masked score matrix (a library routine), fp64
+    lse = O.attention_lse(q, k)
+    g = Hq // Hkv
+    qt = torch.from_numpy(q.astype(np.float64)).permute(0, 2, 1, 3)            # B,Hq,N,D
+    kt = torch.from_numpy(k.astype(np.float64)).permute(0, 2, 1, 3).repeat_interleave(g, 1)
+    s = qt @ kt.transpose(-1, -2) / math.sqrt(D)
+    s = s.masked_fill(~torch.tril(torch.ones(N, N, dtype=torch.bool)), -math.inf)
+    want = torch.logsumexp(s, -1).permute(0, 2, 1).numpy()                      # B,N,Hq
+    np.testing.assert_allclose(lse, want, rtol=0, atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# attention mass ||A_j||_1 of the first layer
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype,Hq,Hkv,D", [("f32", 4, 2, 64), ("bf16", 8, 2, 128),
+                                            ("bf16", 4, 4, 64)])
+def test_mass_rows_sum_to_one(dtype, Hq, Hkv, D):
+    """Every row's weights sum to 1, so the mass of KV group g sums to G * N."""
+    B, N = 2, 41
+    mass = O.attention_mass(_rand((B, N, Hq, D), 3, dtype), _rand((B, N, Hkv, D), 4, dtype))
+    np.testing.assert_allclose(mass.sum(-1), np.full((B, Hkv), Hq // Hkv * N), rtol=1e-12)
+    assert np.all(mass > 0)
+
+
+def test_mass_zero_queries_is_harmonic():
+    """Q = 0: row p weighs its p + 1 keys equally, so key j receives
+    G * (H_N - H_j) with H_n the n-th harmonic number."""
+    B, N, Hq, Hkv, D = 1, 30, 6, 3, 64
+    mass = O.attention_mass(np.zeros((B, N, Hq, D), np.float32), _rand((B, N, Hkv, D), 5))
+    G = Hq // Hkv
+    want = np.array([G * (_harmonic(N) - _harmonic(j)) for j in range(N)])
+    for g in range(Hkv):
+        np.testing.assert_allclose(mass[0, g], want, rtol=1e-12)
+
+
+def test_mass_equals_attention_of_one_hot_values():
+    """With V row j = e_j the attention output of row p is its weight vector,
+    so summing the (separately pinned) attention oracle's outputs over the
+    group's heads and rows gives the mass."""
+    B, N, Hq, Hkv, D = 2, 40, 6, 2, 64
+    q = _rand((B, N, Hq, D), 6)
+    k = _rand((B, N, Hkv, D), 7)
+    v = np.zeros((B, N, Hkv, D), np.float32)
+    for j in range(N):
+        v[:, j, :, j] = 1.0
+    out = O.attention(q, k, v).astype(np.float64)                 # B,N,Hq,D
+    mass = O.attention_mass(q, k)
+    G = Hq // Hkv
+    for g in range(Hkv):
+        want = out[:, :, g * G:(g + 1) * G, :N].sum(axis=(1, 2))   # B,N
+        np.testing.assert_allclose(mass[:, g], want, rtol=0, atol=1e-5)
+
+
+def test_mass_sharp_softmax_counts_argmax():
+    """With a scale so large that every row's softmax is one-hot, key j's mass
+    is the number of (head, row) pairs whose largest causal score is at j."""
+    B, N, Hq, Hkv, D = 1, 24, 4, 2, 64
+    q = _rand((B, N, Hq, D), 8)
+    k = _rand((B, N, Hkv, D), 9)
+    G = Hq // Hkv
+    counts = np.zeros((Hkv, N))
+    min_gap = np.inf
+    for h in range(Hq):
+        for p in range(N):
+            z = np.array([float(np.dot(q[0, p, h].astype(np.float64), k[0, j, h // G]))
+                          for j in range(p + 1)])
+            order = np.argsort(-z)
+            counts[h // G, order[0]] += 1
+            if p > 0:
+                min_gap = min(min_gap, z[order[0]] - z[order[1]])
+    scale = 60.0 / min_gap  # every row's runner-up weight is below e^-60
+    mass = O.attention_mass(q, k, scale=scale)[0]
+    np.testing.assert_allclose(mass, counts, rtol=0, atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# Eq. (3) score
+# ---------------------------------------------------------------------------
+
+def _assembled(cfg, seed, sigma=None):
+    w = inputs.make(cfg, seed, sigma=sigma)
+    cos, sin = O.rope_table(cfg.N, cfg.D, cfg.rope_base)
+    pools = [(H(a), H(b)) for a, b in w.pools]
+    ka, va = O.assemble(H(w.k_fresh), H(w.v_fresh), pools, w.segs.numpy(), cos, sin)
+    return w, ka, va
+
+
+@pytest.mark.parametrize("name", ["tiny-f32-gqa", "tiny-bf16"])
+def test_score_reduces_to_its_terms(name):
+    cfg = inputs.TEST_CONFIGS[name]
+    w, ka, va = _assembled(cfg, 21)
+    kf, vf, segs = H(w.k_fresh), H(w.v_fresh), w.segs.numpy()
+    mass = O.attention_mass(H(w.q), kf).astype(np.float32)
+    attn = mass.astype(np.float64).sum(1)
+    div = O.deviation(kf, ka).astype(np.float64) + O.deviation(vf, va).astype(np.float64)
+    # lambda = 1, no item pools: K deviation + V deviation (the K-only score plus its V twin)
+    s1 = O.score_eq3(segs, 0, 1.0, mass, kf, vf, ka, va)
+    np.testing.assert_allclose(s1, div, rtol=2e-6, atol=0)
+    # lambda = 0: the attention term alone
+    s0 = O.score_eq3(segs, inputs.ITEM_POOL_MASK, 0.0, mass, kf, vf, ka, va)
+    np.testing.assert_allclose(s0, attn, rtol=1e-6, atol=0)
+    # item tokens drop the divergence; history tokens keep both terms
+    lam = 0.3
+    s = O.score_eq3(segs, inputs.ITEM_POOL_MASK, lam, mass, kf, vf, ka, va)
+    item = np.zeros((cfg.B, cfg.N), bool)
+    for b in range(cfg.B):
+        for dst, ln, p, _ in segs[b]:
+            if p == 1:
+                item[b, dst:dst + ln] = True
+    np.testing.assert_allclose(s[item], (1 - lam) * attn[item], rtol=1e-6)
+    np.testing.assert_allclose(s[~item], (1 - lam) * attn[~item] + lam * div[~item], rtol=1e-6)
+    # fresh positions: assembled rows are fresh rows, no divergence
+    F = cfg.F
+    np.testing.assert_allclose(s[:, :F], (1 - lam) * attn[:, :F], rtol=1e-6)
+
+
+@pytest.mark.parametrize("sigma", [0.05, 0.1])
+def test_divergence_matches_half_normal_closed_form(sigma):
+    """K and V both carry N(0, sigma^2) cache noise, so the divergence of a
+    cached token is a sum of 2 * Hkv * D half-normals: mean 2 n sigma sqrt(2/pi),
+    sd sigma sqrt(2 n (1 - 2/pi)) with n = Hkv * D. Dropping the V term halves
+    the mean."""
+    cfg = inputs.CONFIGS[1]
+    w, ka, va = _assembled(cfg, 1000, sigma)
+    kf, vf = H(w.k_fresh), H(w.v_fresh)
+    mass = np.zeros((cfg.B, cfg.Hkv, cfg.N), np.float32)
+    s = O.score_eq3(w.segs.numpy(), 0, 1.0, mass, kf, vf, ka, va)[0]
+    reused = s[cfg.F:]
+    n = cfg.Hkv * cfg.D
+    mean = 2 * n * sigma * math.sqrt(2 / math.pi)
+    sd = sigma * math.sqrt(2 * n * (1 - 2 / math.pi))
+    assert abs(reused.mean() - mean) < 5 * sd / math.sqrt(reused.size)
+    assert 0.7 * sd < reused.std() < 1.3 * sd
+
+
+# ---------------------------------------------------------------------------
+# separate history / item budgets
+# ---------------------------------------------------------------------------
+
+def _brute_split(spans, N, mask, k_hist, k_item, scores_b):
+    fresh, comp = set(), {}
+    for dst, ln, p, _ in spans:
+        for i in range(dst, dst + ln):
+            if p < 0:
+                fresh.add(i)
+            else:
+                comp[i] = (mask >> p) & 1
+    take = set(fresh)
+    for c, kk in ((0, k_hist), (1, k_item)):
+        cand = sorted((i for i in comp if comp[i] == c), key=lambda i: (-scores_b[i], i))
+        take |= set(cand[:kk])
+    return sorted(take)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_topk_split_matches_full_sort(seed):
+    rng = np.random.default_rng(100 + seed)
+    B, N = 3, int(rng.integers(30, 120))
+    cut = sorted(rng.choice(np.arange(1, N), 6, replace=False).tolist())
+    bounds = [0] + cut + [N]
+    spans = []
+    for s in range(len(bounds) - 1):
+        p = [-1, 0, 1, 1, -1, 2, 1][s]
+        spans.append((bounds[s], bounds[s + 1] - bounds[s], p, 0))
+    segs = np.array(spans, np.int32)[None].repeat(B, 0)
+    scores = rng.integers(0, 5, (B, N)).astype(np.float32)
+    for mask in (0b010, 0b110, 0b000):
+        n_c = [sum(ln for _, ln, p, _ in spans if p >= 0 and ((mask >> p) & 1) == c) for c in (0, 1)]
+        for kh in sorted({0, 1, n_c[0] // 2, n_c[0]}):
+            for ki in sorted({0, 1, n_c[1] // 3, n_c[1]}):
+                if ki > n_c[1] or kh > n_c[0]:
+                    continue
+                rows = O.topk_split(segs, N, mask, kh, ki, scores)
+                for b in range(B):
+                    assert rows[b].tolist() == _brute_split(spans, N, mask, kh, ki, scores[b])
+    # one component and no item pools: the single-budget top-k (pinned separately)
+    k = 5
+    np.testing.assert_array_equal(O.topk_split(segs, N, 0, k, 0, scores), O.topk(segs, N, k, scores))
+    with pytest.raises(ValueError):
+        O.topk_split(segs, N, 0b010, 0, N, scores)
+
+
+# ---------------------------------------------------------------------------
+# the whole selection
+# ---------------------------------------------------------------------------
+
+def _eq3(cfg, w, lam, kh, ki):
+    cos, sin = O.rope_table(cfg.N, cfg.D, cfg.rope_base)
+    pools = [(H(a), H(b)) for a, b in w.pools]
+    return O.eq3_select(H(w.q), H(w.k_fresh), H(w.v_fresh), pools, w.segs.numpy(),
+                        inputs.ITEM_POOL_MASK, lam, kh, ki, cos, sin)
+
+
+def test_eq3_full_budgets_give_fresh_kv():
+    cfg = inputs.TEST_CONFIGS["tiny-bf16"]
+    w = inputs.make(cfg, 31)
+    r = _eq3(cfg, w, 0.5, cfg.n_hist_reused, cfg.n_item_reused)
+    np.testing.assert_array_equal(r["k_asm"], H(w.k_fresh))
+    np.testing.assert_array_equal(r["v_asm"], H(w.v_fresh))
+    assert r["rows"].shape[1] == cfg.N
+
+
+def test_eq3_selects_attention_sinks_and_drifted_history():
+    """lambda = 0: item keys that every query attends to strongly are
+    selected; lambda = 1: history tokens with 20x cache noise are selected."""
+    cfg = inputs.TEST_CONFIGS["tiny-f32-gqa"]
+    w = inputs.make(cfg, 41)
+    q = w.q.clone()
+    u = torch.randn(cfg.D, generator=torch.Generator().manual_seed(5))
+    q[:] = u                                           # every query points along u
+    kf = w.k_fresh.clone()
+    item_start = cfg.F + cfg.hist_len
+    sinks = [item_start + 3, item_start + 40, cfg.N - 5]
+    for j in sinks:
+        kf[:, j] = 0.6 * u / u.norm() * math.sqrt(cfg.D)
+    w2 = dataclasses.replace(w, q=q, k_fresh=kf)
+    kh, ki = cfg.k_split(15)
+    r = _eq3(cfg, w2, 0.0, kh, ki)
+    for b in range(cfg.B):
+        assert set(sinks) <= set(r["rows"][b].tolist())
+    # drifted history: planted tokens carry 20x noise in their cached K
+    w3 = inputs.make(cfg, 7, planted=6)
+    r3 = _eq3(cfg, w3, 1.0, kh, ki)
+    for b in range(cfg.B):
+        planted = set(w3.planted[b].tolist())
+        hist = set(range(cfg.F, cfg.F + cfg.hist_len))
+        assert planted & hist and (planted & hist) <= set(r3["rows"][b].tolist())
+
+
+def test_eq3_intermediates_are_consistent():
+    cfg = inputs.TEST_CONFIGS["miss-bf16"]
+    w = inputs.make(cfg, 51)
+    kh, ki = cfg.k_split(20, 30)
+    r = _eq3(cfg, w, 0.4, kh, ki)
+    kf = H(w.k_fresh)
+    np.testing.assert_array_equal(r["mass"], O.attention_mass(H(w.q), kf).astype(np.float32))
+    segs = w.segs.numpy()
+    np.testing.assert_array_equal(r["rows"], O.topk_split(segs, cfg.N, inputs.ITEM_POOL_MASK,
+                                                          kh, ki, r["scores"]))
+    assert r["rows"].shape[1] == cfg.n_fresh + kh + ki

@@ -48,6 +48,8 @@ def parse_args():
                     help="requests of batch 0 in the CPU oracle's sample (default: all; 0 = skip)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="repeat the CPU oracle's sample until this much time has passed")
+    ap.add_argument("--no-eq3", action="store_true",
+                    help="skip timing the selection by the full Eq. (3) score")
     ap.add_argument("--no-full-prefill", action="store_true",
                     help="skip timing the Full-Recompute baseline")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -202,7 +204,8 @@ def main():
     tr = load_traffic(args.config, pct)
     digest = {"rc_kv_assemble": source_digest("assemble.hip"),
               "rc_select_tokens": source_digest("select.hip"),
-              "rc_selective_attention": source_digest("attention.hip")}
+              "rc_selective_attention": source_digest("attention.hip"),
+              "rc_attention_mass": source_digest("mass.hip")}
     if tr and tr.get("source_digest", {}).get(dominant) == digest[dominant]:
         traffic = tr.get("kernels", {}).get(dominant, {}).get("hbm_bytes")
     roofline = {"kernel": dominant, "bound": dk["bound"], "achieved": dk["achieved"],
@@ -228,6 +231,68 @@ def main():
                 "frac_of_bf16_peak": round(fflops / (fms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
                 "selective_speedup": round(fms / ms_per_step, 3)}
         del fout
+
+    # ---- selection by the full Eq. (3) score: the first layer in full (with
+    # log-sum-exp), attention mass, assembly, score, history/item top-k, patch
+    eq3 = None
+    if not args.no_eq3 and cfg.dtype == "bf16":
+        kh, ki = cfg.k_split(pct)
+        lam = 0.5
+        R3 = cfg.n_fresh + kh + ki
+        ebuf = ops.Eq3Buffers.alloc(B, N, Hq, Hkv, D, R3, cfg.torch_dtype, dev)
+        mask = inputs.ITEM_POOL_MASK
+
+        def step3(i, ev=None):
+            w, segs, _ = batches[i % len(batches)]
+            if ev is not None:
+                ev[0].record(stream)
+            ops.selective_attention_lse(w.q, w.k_fresh, w.v_fresh, None, None, ebuf.out_full,
+                                        ebuf.lse)
+            if ev is not None:
+                ev[1].record(stream)
+            ops.attention_mass(w.q, w.k_fresh, ebuf.lse, None, ebuf.mass)
+            if ev is not None:
+                ev[2].record(stream)
+            ops.kv_assemble(w.pools, segs, w.k_fresh, w.v_fresh, cos, sin, ebuf.k_asm, ebuf.v_asm)
+            if ev is not None:
+                ev[3].record(stream)
+            ops.select_tokens_eq3(segs, mask, lam, kh, ki, w.k_fresh, w.v_fresh, ebuf.k_asm,
+                                  ebuf.v_asm, mass=ebuf.mass, scores_out=ebuf.scores,
+                                  rows_out=ebuf.rows, patch=True)
+            if ev is not None:
+                ev[4].record(stream)
+
+        for i in range(3):
+            step3(i)
+        torch.cuda.synchronize()
+        reps = max(3, min(20, args.steps // 5))
+        ev3 = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(reps)]
+        for i in range(reps):
+            step3(i, ev3[i])
+        torch.cuda.synchronize()
+        part = [sum(e[j].elapsed_time(e[j + 1]) for e in ev3) / reps for j in range(4)]
+        e3_ms = sum(e[0].elapsed_time(e[4]) for e in ev3) / reps
+        causal = B * N * (N + 1) / 2.0
+        att_f, mass_f = 4.0 * D * Hq * causal, 2.0 * D * Hq * causal
+        n_div = cfg.n_fresh + cfg.n_hist_reused   # positions whose K/V divergence is read
+        sel3_bytes = (4.0 * B * n_div * row + 4.0 * B * Hkv * N + 4.0 * B * N + 4.0 * B * N
+                      + 4.0 * B * R3 + 4.0 * B * (kh + ki) * row)
+
+        def mf(fl, ms):
+            a = fl / (ms * 1e-3) / 1e12
+            return {"bound": "mfma", "achieved": round(a, 2), "peak": BF16_PEAK_TFLOPS,
+                    "unit": "TFLOP/s", "frac": round(a / BF16_PEAK_TFLOPS, 4), "flops_per_launch": fl}
+
+        eq3 = {"ms": round(e3_ms, 4), "lambda": lam, "budgets": [kh, ki],
+               "selected_rows_per_request": R3,
+               "selected_tokens_per_s": round(B * R3 / (e3_ms * 1e-3), 1),
+               "kernels": {
+                   "rc_selective_attention_lse": dict(us=round(part[0] * 1e3, 2), **mf(att_f, part[0])),
+                   "rc_attention_mass": dict(us=round(part[1] * 1e3, 2), **mf(mass_f, part[1])),
+                   "rc_kv_assemble": dict(us=round(part[2] * 1e3, 2),
+                                          **hbm(4.0 * B * N * row, part[2])),
+                   "rc_select_tokens_eq3": dict(us=round(part[3] * 1e3, 2), **hbm(sel3_bytes, part[3]))}}
+        del ebuf
 
     # ---- CPU oracle on a bounded sample of the same workload
     cpu = None
@@ -279,6 +344,7 @@ def main():
         "roofline": roofline,
         "kernels": kernels,
         "full_prefill": full,
+        "eq3_selection": eq3,
         "cpu_baseline": cpu,
         "wall_s_timed": round(wall, 3),
         "source_digest": digest,

@@ -19,6 +19,16 @@
  *                           query rows over the whole assembled context,
  *                           or for every row (Full-Recompute, Sec. IV-A)
  *
+ * Selection by the full score of Eq. (3) (the first layer computed in full):
+ *
+ *   rc_selective_attention_lse  the same attention, also writing each row's
+ *                               log-sum-exp
+ *   rc_attention_mass           attention weight each token receives in the
+ *                               full first layer (the ||A_i||_1 term)
+ *   rc_select_tokens_eq3        Eq. (3) score with lambda, K and V divergence
+ *                               (dropped for item blocks), separate history
+ *                               and item budgets, and the correction (iii)
+ *
  * Conventions shared by every call
  * --------------------------------
  * - Pointers are DEVICE pointers unless marked (host). The caller owns every
@@ -188,6 +198,64 @@ int rc_select_tokens(const rc_shape* shape, const rc_segment* segs, int32_t S, i
 int rc_selective_attention(const rc_shape* shape, const void* q, const int32_t* rows, int32_t R,
                            const void* k, const void* v, float scale, void* out,
                            hipStream_t stream);
+
+/* Attention as rc_selective_attention that also writes, for every row r and
+ * q-head h, the natural log-sum-exp of the row's scaled causal scores,
+ *   lse[b,r,h] = ln sum_{j<=p} exp(scale * Q[b,p,h] . K[b,j,g]),
+ * into lse: device [B, R, Hq] fp32 (fp32 sums of the unrounded exponentials).
+ * With rows NULL (every row of the first layer, Sec. III-C.2b) this is the
+ * input rc_attention_mass takes. Errors: those of rc_selective_attention,
+ * and INVALID_ARG for a NULL lse with R > 0. */
+int rc_selective_attention_lse(const rc_shape* shape, const void* q, const int32_t* rows,
+                               int32_t R, const void* k, const void* v, float scale, void* out,
+                               float* lse, hipStream_t stream);
+
+/* Attention-mass term of Eq. (3) (Sec. III-C.2b: the first layer is computed
+ * in full and a token's importance includes the attention weight it
+ * receives). For KV group g and position j of request b:
+ *   mass[b,g,j] = sum over q-heads h with h / (Hq/Hkv) == g, rows p in [j, N) of
+ *                 exp(scale * Q[b,p,h] . K[b,j,g] - lse[b,p,h])
+ * i.e. the softmax weights of key j summed over the group's rows and heads;
+ * sum_g mass[b,g,j] is ||A_j||_1. q: [B, N, Hq, D]; k: [B, N, Hkv, D] (the
+ * fresh first-layer keys); lse: [B, N, Hq] from rc_selective_attention_lse
+ * with rows NULL and the same scale; mass: device [B, Hkv, N] fp32 output,
+ * every entry written. Deterministic (no atomics); fp32 accumulation, bf16
+ * products on the matrix cores.
+ * Errors: INVALID_ARG for NULL pointers, bad shape, non-finite or
+ * non-positive scale; UNSUPPORTED for D, dtype, or a bf16 group size that
+ * does not divide 128. */
+int rc_attention_mass(const rc_shape* shape, const void* q, const void* k, const float* lse,
+                      float scale, float* mass, hipStream_t stream);
+
+/* Heavy-hitter selection by the full score of Eq. (3), with separate budgets
+ * for history and item tokens (recompute ratios r_rev and r_item, Sec. IV-A),
+ * and correction (Sec. III-C.3 (iii)).
+ * 1. Score: unless scores_in is given, for every position i of request b
+ *      S[b,i] = (1 - lambda) sum_g mass[b,g,i] + lambda div[b,i]
+ *    with div the L1 distance between the fresh and assembled rows of K plus
+ *    that of V (Hkv * D entries each, fp32 accumulation), except for
+ *    positions in blocks of a pool whose bit is set in item_pool_mask: their
+ *    cached block is a lexical match and div is dropped (Sec. III-C.2b).
+ *    Written to scores_out [B, N] (required when scores_in is NULL).
+ *    mass: [B, Hkv, N] from rc_attention_mass; lambda in [0, 1].
+ * 2. Select: among cached positions of pools outside item_pool_mask
+ *    (history) the k_hist largest scores, among those of pools in it (items)
+ *    the k_item largest -- NaN above +inf above every finite value, ties to
+ *    the lower position -- together with the n_fresh fresh positions, in
+ *    ascending order: rows [B, n_fresh + k_hist + k_item] int32. Bit-exact
+ *    for given scores. A budget above its class's count in some request
+ *    takes the whole class and pads the row list with N - 1.
+ * 3. Patch (patch != 0): K_asm/V_asm rows of the selected cached positions
+ *    get the K_fresh/V_fresh rows.
+ * k_fresh/v_fresh/k_asm/v_asm: [B, N, Hkv, D]. Hq in the shape is unused.
+ * Errors: INVALID_ARG for NULL pointers, bad shape, budgets or n_fresh out
+ * of range, lambda outside [0, 1], mask bits beyond pool 7; UNSUPPORTED for
+ * D, dtype, N > 16384, S > 1024. */
+int rc_select_tokens_eq3(const rc_shape* shape, const rc_segment* segs, int32_t S,
+                         int32_t n_fresh, uint32_t item_pool_mask, float lambda, int32_t k_hist,
+                         int32_t k_item, const float* mass, const void* k_fresh,
+                         const void* v_fresh, void* k_asm, void* v_asm, const float* scores_in,
+                         float* scores_out, int32_t* rows, int32_t patch, hipStream_t stream);
 
 /* Static description of a status code. */
 const char* rc_status_string(int status);

@@ -20,7 +20,8 @@ RC_F32, RC_BF16 = 0, 1
 
 # every symbol include/rcllm.h declares
 EXPORTS = ("rc_rope_table", "rc_kv_assemble", "rc_rerope", "rc_select_tokens",
-           "rc_selective_attention", "rc_status_string", "rc_last_error")
+           "rc_selective_attention", "rc_selective_attention_lse", "rc_attention_mass",
+           "rc_select_tokens_eq3", "rc_status_string", "rc_last_error")
 
 
 class RcShape(ctypes.Structure):
@@ -59,8 +60,13 @@ def load() -> ctypes.CDLL:
     L.rc_rerope.argtypes = [P(RcShape), vp, vp, vp, vp, i32, vp]
     L.rc_select_tokens.argtypes = [P(RcShape), vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, i32, vp]
     L.rc_selective_attention.argtypes = [P(RcShape), vp, vp, i32, vp, vp, f32, vp, vp]
+    L.rc_selective_attention_lse.argtypes = [P(RcShape), vp, vp, i32, vp, vp, f32, vp, vp, vp]
+    L.rc_attention_mass.argtypes = [P(RcShape), vp, vp, vp, f32, vp, vp]
+    L.rc_select_tokens_eq3.argtypes = [P(RcShape), vp, i32, i32, ctypes.c_uint32, f32, i32, i32,
+                                       vp, vp, vp, vp, vp, vp, vp, vp, i32, vp]
     for name in ("rc_rope_table", "rc_kv_assemble", "rc_rerope", "rc_select_tokens",
-                 "rc_selective_attention"):
+                 "rc_selective_attention", "rc_selective_attention_lse", "rc_attention_mass",
+                 "rc_select_tokens_eq3"):
         getattr(L, name).restype = ctypes.c_int
     L.rc_status_string.argtypes = [ctypes.c_int]
     L.rc_status_string.restype = ctypes.c_char_p

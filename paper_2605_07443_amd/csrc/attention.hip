@@ -79,12 +79,15 @@ constexpr float kLazy = 8.f;
 
 // SELECTIVE: query rows come from `rows`; otherwise row r is position r
 // (Full-Recompute). Separate instances keep the two modes apart in profiles.
-template <int D, bool SELECTIVE>
+// LSE: also write each row's natural log-sum-exp, from an fp32 sum of the
+// unrounded exponentials (the bf16 column sums only normalise O).
+template <int D, bool SELECTIVE, bool LSE>
 __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict__ rows, int R,
                       int N, int Hq, int Hkv, int G, int BR, const uint16_t* __restrict__ k,
                       const uint16_t* __restrict__ v, float scale_log2e,
-                      uint16_t* __restrict__ out, int n_tiles, int n_groups, int gpx, int chunk) {
+                      uint16_t* __restrict__ out, float* __restrict__ lse, int n_tiles,
+                      int n_groups, int gpx, int chunk) {
   constexpr int DC = D / 32;          // 32-wide d chunks (S^T reduction)
   constexpr int DB = D / 16;          // 16-wide d blocks (O^T rows)
   constexpr int UPR = D / 8;          // 16-byte units per K/V head row
@@ -197,6 +200,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
   // softmax denominators on the matrix cores: ones(16x32) x P^T gives the
   // column sums of P for every query column (all 4 lanes' entries equal)
   f32x4 l_acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+  float l32[2] = {0.f, 0.f};  // LSE: this lane's share of the fp32 row sums
   const bf16x8 ones = __builtin_bit_cast(bf16x8, u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
 
   const int tr_row = q4 * 4 + (c16 >> 2);
@@ -260,6 +264,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
         const float m_new = fmaxf(m_run[nb], mx[nb]);
         const float alpha = __builtin_amdgcn_exp2f((m_run[nb] - m_new) * scale_log2e);
         l_acc[nb] *= alpha;
+        if constexpr (LSE) l32[nb] *= alpha;
 #pragma unroll
         for (int db = 0; db < DB; ++db) o[db][nb] *= alpha;
         m_run[nb] = m_new;
@@ -274,6 +279,11 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
 #pragma unroll
         for (int i = 0; i < 4; ++i)
           s[kb][nb][i] = __builtin_amdgcn_exp2f(fmaf(s[kb][nb][i], scale_log2e, -mc));
+      if constexpr (LSE) {
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+          l32[nb] += (s[kb][nb][0] + s[kb][nb][1]) + (s[kb][nb][2] + s[kb][nb][3]);
+      }
 #pragma unroll
       for (int kc = 0; kc < 2; ++kc) {
         u32x4 w = {pack_bf16x2(s[2 * kc][nb][0], s[2 * kc][nb][1]),
@@ -319,6 +329,19 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
   for (; t < t_mask; ++t) do_tile(t, std::false_type{});
   for (; t < n_kv; ++t) do_tile(t, std::true_type{});
 
+  // ---- log-sum-exp: the 4 lanes of a query column hold disjoint keys
+  if constexpr (LSE) {
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      float l = l32[nb];
+      l += __shfl_xor(l, 16, 64);
+      l += __shfl_xor(l, 32, 64);
+      if (valid[nb] && q4 == 0)
+        lse[(static_cast<size_t>(b) * R + row[nb]) * Hq + head[nb]] =
+            (m_run[nb] * scale_log2e + __log2f(l)) * 0.69314718055994531f;
+    }
+  }
+
   // ---- normalise and store: lane holds dims db*16 + q4*4 .. +3 of its query
 #pragma unroll
   for (int nb = 0; nb < 2; ++nb) {
@@ -342,7 +365,8 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(const float* __restrict__
                                                        int N, int Hq, int Hkv,
                                                        const float* __restrict__ k,
                                                        const float* __restrict__ v, float scale,
-                                                       float* __restrict__ out, int64_t total) {
+                                                       float* __restrict__ out,
+                                                       float* __restrict__ lse, int64_t total) {
   constexpr int PER = D / 64;
   __shared__ float s_q[4][D];
   const int lane = threadIdx.x & 63;
@@ -396,16 +420,18 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(const float* __restrict__
   float* orow = out + ((static_cast<size_t>(b) * R + r) * Hq + h) * D;
 #pragma unroll
   for (int e = 0; e < PER; ++e) orow[lane * PER + e] = acc[e] / l;
+  if (lse && lane == 0) lse[(static_cast<size_t>(b) * R + r) * Hq + h] = m + logf(l);
 }
 
 }  // namespace
 }  // namespace rc
 
-extern "C" int rc_selective_attention(const rc_shape* shape, const void* q, const int32_t* rows,
-                                      int32_t R, const void* k, const void* v, float scale,
-                                      void* out, hipStream_t stream) {
-  using namespace rc;
-  clear_error();
+namespace rc {
+namespace {
+
+int attention_impl(const rc_shape* shape, const void* q, const int32_t* rows, int32_t R,
+                   const void* k, const void* v, float scale, void* out, float* lse,
+                   hipStream_t stream, const char* what) {
   if (int st = check_shape(shape, true)) return st;
   if (R < 0) return fail(RC_ERR_INVALID_ARG, "R=%d must be >= 0", R);
   if (!q || !k || !v || (!out && R > 0))
@@ -439,12 +465,20 @@ extern "C" int rc_selective_attention(const rc_shape* shape, const void* q, cons
       hipLaunchKernelGGL(kern, grid, dim3(kAttnThreads), 0, stream,
                          static_cast<const uint16_t*>(q), rows, R, N, Hq, Hkv, G, BR,
                          static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
-                         scale_log2e, static_cast<uint16_t*>(out), n_tiles, n_groups, gpx, chunk);
+                         scale_log2e, static_cast<uint16_t*>(out), lse, n_tiles, n_groups, gpx,
+                         chunk);
     };
-    if (D == 128)
-      rows ? launch(attn_bf16_kernel<128, true>) : launch(attn_bf16_kernel<128, false>);
-    else
-      rows ? launch(attn_bf16_kernel<64, true>) : launch(attn_bf16_kernel<64, false>);
+    if (lse) {
+      if (D == 128)
+        rows ? launch(attn_bf16_kernel<128, true, true>) : launch(attn_bf16_kernel<128, false, true>);
+      else
+        rows ? launch(attn_bf16_kernel<64, true, true>) : launch(attn_bf16_kernel<64, false, true>);
+    } else {
+      if (D == 128)
+        rows ? launch(attn_bf16_kernel<128, true, false>) : launch(attn_bf16_kernel<128, false, false>);
+      else
+        rows ? launch(attn_bf16_kernel<64, true, false>) : launch(attn_bf16_kernel<64, false, false>);
+    }
   } else {
     const int64_t total = static_cast<int64_t>(B) * R * Hq;
     const int64_t blocks = (total + 3) / 4;
@@ -454,12 +488,33 @@ extern "C" int rc_selective_attention(const rc_shape* shape, const void* q, cons
       hipLaunchKernelGGL(attn_f32_kernel<128>, grid, dim3(256), 0, stream,
                          static_cast<const float*>(q), rows, R, N, Hq, Hkv,
                          static_cast<const float*>(k), static_cast<const float*>(v), scale,
-                         static_cast<float*>(out), total);
+                         static_cast<float*>(out), lse, total);
     else
       hipLaunchKernelGGL(attn_f32_kernel<64>, grid, dim3(256), 0, stream,
                          static_cast<const float*>(q), rows, R, N, Hq, Hkv,
                          static_cast<const float*>(k), static_cast<const float*>(v), scale,
-                         static_cast<float*>(out), total);
+                         static_cast<float*>(out), lse, total);
   }
-  return check_launch("rc_selective_attention");
+  return check_launch(what);
+}
+
+}  // namespace
+}  // namespace rc
+
+extern "C" int rc_selective_attention(const rc_shape* shape, const void* q, const int32_t* rows,
+                                      int32_t R, const void* k, const void* v, float scale,
+                                      void* out, hipStream_t stream) {
+  rc::clear_error();
+  return rc::attention_impl(shape, q, rows, R, k, v, scale, out, nullptr, stream,
+                            "rc_selective_attention");
+}
+
+extern "C" int rc_selective_attention_lse(const rc_shape* shape, const void* q,
+                                          const int32_t* rows, int32_t R, const void* k,
+                                          const void* v, float scale, void* out, float* lse,
+                                          hipStream_t stream) {
+  rc::clear_error();
+  if (!lse && R > 0) return rc::fail(RC_ERR_INVALID_ARG, "lse must be non-NULL");
+  return rc::attention_impl(shape, q, rows, R, k, v, scale, out, lse, stream,
+                            "rc_selective_attention_lse");
 }

@@ -189,6 +189,77 @@ def selective_attention(q, k, v, rows=None, scale=None, out=None, stream=None):
     return out
 
 
+def selective_attention_lse(q, k, v, rows=None, scale=None, out=None, lse=None, stream=None):
+    """rc_selective_attention_lse: attention plus each row's natural
+    log-sum-exp [B, R, Hq] fp32. Returns (out, lse)."""
+    B, N, Hq, D = q.shape
+    Hkv = k.shape[2]
+    if k.shape != v.shape or k.shape[:2] != q.shape[:2] or k.shape[3] != D:
+        raise ValueError("q [B,N,Hq,D] and k, v [B,N,Hkv,D] do not match")
+    R = N if rows is None else int(rows.shape[1])
+    if rows is not None and (rows.dtype != torch.int32 or rows.shape[0] != B):
+        raise ValueError("rows must be int32 [B, R]")
+    scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
+    out = torch.empty((B, R, Hq, D), dtype=q.dtype, device=q.device) if out is None else out
+    lse = torch.empty((B, R, Hq), dtype=torch.float32, device=q.device) if lse is None else lse
+    check(_lib.load().rc_selective_attention_lse(
+        ctypes.byref(_shape(B, N, Hq, Hkv, D, _dtype_code(q))), _dev(q, "q"),
+        None if rows is None else _dev(rows, "rows"), R, _dev(k, "k"), _dev(v, "v"),
+        ctypes.c_float(scale), _dev(out, "out"), _dev(lse, "lse"), _stream(stream)))
+    return out, lse
+
+
+def attention_mass(q, k, lse, scale=None, mass=None, stream=None):
+    """rc_attention_mass: attention weight each key receives from every row
+    of its KV group's heads, [B, Hkv, N] fp32."""
+    B, N, Hq, D = q.shape
+    Hkv = k.shape[2]
+    if k.shape[:2] != q.shape[:2] or k.shape[3] != D:
+        raise ValueError("q [B,N,Hq,D] and k [B,N,Hkv,D] do not match")
+    if tuple(lse.shape) != (B, N, Hq) or lse.dtype != torch.float32:
+        raise ValueError("lse must be fp32 [B, N, Hq] (every row of the full pass)")
+    scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
+    mass = torch.empty((B, Hkv, N), dtype=torch.float32, device=q.device) if mass is None else mass
+    check(_lib.load().rc_attention_mass(
+        ctypes.byref(_shape(B, N, Hq, Hkv, D, _dtype_code(q))), _dev(q, "q"), _dev(k, "k"),
+        _dev(lse, "lse"), ctypes.c_float(scale), _dev(mass, "mass"), _stream(stream)))
+    return mass
+
+
+def component_counts(segs: Segments, item_mask: int):
+    """Cached positions per request in the history and item classes."""
+    h = segs.host
+    cached = h[..., 2] >= 0
+    item = cached & (((item_mask >> np.clip(h[..., 2], 0, 31)) & 1) == 1)
+    lens = h[..., 1]
+    return (np.where(cached & ~item, lens, 0).sum(1), np.where(item, lens, 0).sum(1))
+
+
+def select_tokens_eq3(segs: Segments, item_mask: int, lam: float, k_hist: int, k_item: int,
+                      k_fresh, v_fresh, k_asm, v_asm, mass=None, scores_in=None,
+                      scores_out=None, rows_out=None, patch=True, stream=None):
+    """rc_select_tokens_eq3: Eq. (3) score, separate history/item top-k,
+    patch. Returns (rows, scores)."""
+    B, N, Hkv, D = k_fresh.shape
+    nh, ni = component_counts(segs, item_mask)
+    if k_hist > nh.min() or k_item > ni.min():
+        raise ValueError(f"budgets ({k_hist}, {k_item}) exceed a request's history/item "
+                         f"counts ({nh.min()}, {ni.min()})")
+    R = segs.n_fresh + int(k_hist) + int(k_item)
+    rows = torch.empty((B, R), dtype=torch.int32, device=k_fresh.device) if rows_out is None else rows_out
+    if scores_in is None and scores_out is None:
+        scores_out = torch.empty((B, N), dtype=torch.float32, device=k_fresh.device)
+    check(_lib.load().rc_select_tokens_eq3(
+        ctypes.byref(_shape(B, N, 1, Hkv, D, _dtype_code(k_fresh))), _dev(segs.dev, "segs"),
+        segs.S, segs.n_fresh, int(item_mask), ctypes.c_float(lam), int(k_hist), int(k_item),
+        None if mass is None else _dev(mass, "mass"), _dev(k_fresh, "k_fresh"),
+        _dev(v_fresh, "v_fresh"), _dev(k_asm, "k_asm"), _dev(v_asm, "v_asm"),
+        None if scores_in is None else _dev(scores_in, "scores_in"),
+        None if scores_out is None else _dev(scores_out, "scores_out"),
+        _dev(rows, "rows"), 1 if patch else 0, _stream(stream)))
+    return rows, (scores_out if scores_out is not None else scores_in)
+
+
 # ------------------------------------------------------------- the pipeline
 
 @dataclass
@@ -226,6 +297,49 @@ def selective_prefill(q, k_fresh, v_fresh, pools, segs: Segments, k: int, cos, s
                   rows_out=bufs.rows, patch=True, stream=stream)
     if R > 0:
         selective_attention(q, bufs.k_asm, bufs.v_asm, bufs.rows, scale, bufs.out, stream)
+    return bufs
+
+
+@dataclass
+class Eq3Buffers:
+    k_asm: torch.Tensor
+    v_asm: torch.Tensor
+    out_full: torch.Tensor   # the first layer's attention output, every row
+    lse: torch.Tensor
+    mass: torch.Tensor
+    scores: torch.Tensor
+    rows: torch.Tensor
+
+    @staticmethod
+    def alloc(B, N, Hq, Hkv, D, R, dtype, device):
+        return Eq3Buffers(
+            k_asm=torch.empty((B, N, Hkv, D), dtype=dtype, device=device),
+            v_asm=torch.empty((B, N, Hkv, D), dtype=dtype, device=device),
+            out_full=torch.empty((B, N, Hq, D), dtype=dtype, device=device),
+            lse=torch.empty((B, N, Hq), dtype=torch.float32, device=device),
+            mass=torch.empty((B, Hkv, N), dtype=torch.float32, device=device),
+            scores=torch.empty((B, N), dtype=torch.float32, device=device),
+            rows=torch.empty((B, R), dtype=torch.int32, device=device))
+
+
+def eq3_select(q, k_fresh, v_fresh, pools, segs: Segments, item_mask: int, lam: float,
+               k_hist: int, k_item: int, cos, sin, scale=None, bufs: Eq3Buffers | None = None,
+               stream=None):
+    """Selection by the full Eq. (3) score on one stream: the first layer in
+    full (attention of every row over the fresh K/V, with log-sum-exp) ->
+    attention mass -> assemble (gather + alignment) -> score, separate
+    history/item top-k, patch. Returns the buffers."""
+    B, N, Hq, D = q.shape
+    Hkv = k_fresh.shape[2]
+    R = segs.n_fresh + int(k_hist) + int(k_item)
+    if bufs is None:
+        bufs = Eq3Buffers.alloc(B, N, Hq, Hkv, D, R, q.dtype, q.device)
+    selective_attention_lse(q, k_fresh, v_fresh, None, scale, bufs.out_full, bufs.lse, stream)
+    attention_mass(q, k_fresh, bufs.lse, scale, bufs.mass, stream)
+    kv_assemble(pools, segs, k_fresh, v_fresh, cos, sin, bufs.k_asm, bufs.v_asm, stream=stream)
+    select_tokens_eq3(segs, item_mask, lam, k_hist, k_item, k_fresh, v_fresh, bufs.k_asm,
+                      bufs.v_asm, mass=bufs.mass, scores_out=bufs.scores, rows_out=bufs.rows,
+                      patch=True, stream=stream)
     return bufs
 
 

@@ -119,3 +119,89 @@ def run_stepwise(cfg, w, k: int, device, stride: int = 1, check_attention: bool 
         stats.update(assert_attn_close(g, r, cfg.dtype, "selective attention"))
     return stats, dict(segs=segs, cos=cos, sin=sin, k_asm=k_asm, v_asm=v_asm, rows=rows,
                        scores=scores, out=out)
+
+
+# ------------------------------------------------------------ Eq. (3) selection
+
+# log-sum-exp: scores of bf16/fp32 inputs accumulated in fp32 (bf16 products
+# are exact in fp32), exponentials and their sums in fp32, so the error is a
+# few fp32 ulps of the score scale (|lse| < 30): measured <= 1.7e-6 on every
+# workload. Mass: each weight exp(s - lse) carries the lse and exp2 errors
+# (relative, a few 1e-7 .. 1e-6) and is summed in fp32: measured <= 1.3e-6
+# relative. The bounds below leave a margin of about 10x.
+LSE_ATOL = 2e-5
+MASS_RTOL, MASS_ATOL = 2e-5, 1e-6
+
+
+def group_slice(q, k, g, G):
+    """Q heads and the K head of KV group g (oracle cost of one group)."""
+    return (np.ascontiguousarray(q[:, :, g * G:(g + 1) * G]), np.ascontiguousarray(k[:, :, g:g + 1]))
+
+
+def run_eq3_stepwise(cfg, w, lam, k_hist, k_item, device, check_requests=None, check_groups=None):
+    """First layer in full with lse -> mass -> assemble -> Eq. (3) score ->
+    split top-k -> patch on the GPU; each step checked against the oracle.
+    check_requests / check_groups bound the oracle's quadratic work (None:
+    all)."""
+    stats = {}
+    G = cfg.Hq // cfg.Hkv
+    mask = inputs.ITEM_POOL_MASK
+    lam = float(np.float32(lam))
+    segs = ops.prepare_segments(w.segs, cfg.N, w.pools, device)
+    cos, sin = ops.rope_table(cfg.N, cfg.D, cfg.rope_base, device)
+    bufs = ops.eq3_select(w.q, w.k_fresh, w.v_fresh, w.pools, segs, mask, lam, k_hist, k_item,
+                          cos, sin)
+    torch.cuda.synchronize()
+    qh, kf, vf = H(w.q), H(w.k_fresh), H(w.v_fresh)
+    lse_g = bufs.lse.cpu().numpy()
+    mass_g = bufs.mass.cpu().numpy()
+    reqs = range(cfg.B) if check_requests is None else check_requests
+    groups = range(cfg.Hkv) if check_groups is None else check_groups
+
+    # ---- the first layer's log-sum-exp and attention mass
+    lse_err, mass_rel = 0.0, 0.0
+    for b in reqs:
+        for g in groups:
+            qg, kg = group_slice(qh[b:b + 1], kf[b:b + 1], g, G)
+            lse_o = O.attention_lse(qg, kg)[0]                       # N, G
+            d = np.abs(lse_g[b, :, g * G:(g + 1) * G] - lse_o)
+            assert d.max() <= LSE_ATOL, f"lse b={b} g={g}: max err {d.max():.3e}"
+            lse_err = max(lse_err, float(d.max()))
+            m_o = O.attention_mass(qg, kg)[0, 0]                      # N
+            np.testing.assert_allclose(mass_g[b, g], m_o, rtol=MASS_RTOL, atol=MASS_ATOL,
+                                       err_msg=f"mass b={b} g={g}")
+            mass_rel = max(mass_rel, float(np.max(np.abs(mass_g[b, g] - m_o) / np.maximum(m_o, 1e-6))))
+    # every row's weights sum to 1: each group's mass sums to G * N
+    np.testing.assert_allclose(mass_g.astype(np.float64).sum(-1), G * cfg.N, rtol=1e-5)
+    stats.update(lse_max_err=lse_err, mass_max_rel=mass_rel)
+
+    # ---- assembly: bit-exact (the Eq. (3) path assembles without scoring)
+    ocos, osin = O.rope_table(cfg.N, cfg.D, cfg.rope_base)
+    subpools, segs_sub = inputs.referenced_subpools(w)
+    ka_o, va_o = O.assemble(kf, vf, subpools, segs_sub, ocos, osin)
+
+    # ---- score from the GPU's mass: fp32 vs fp64
+    segs_h = w.segs.numpy()
+    sc_g = bufs.scores.cpu().numpy()
+    sc_o = O.score_eq3(segs_h, mask, lam, mass_g, kf, vf, ka_o, va_o)
+    np.testing.assert_allclose(sc_g, sc_o, rtol=1e-5, atol=1e-5, err_msg="Eq. (3) scores")
+    stats["score_rel"] = float(np.max(np.abs(sc_g - sc_o) / np.maximum(np.abs(sc_o), 1e-30)))
+
+    # ---- split top-k: bit-exact on identical scores, both ways
+    rows_g = bufs.rows.cpu().numpy()
+    np.testing.assert_array_equal(rows_g, O.topk_split(segs_h, cfg.N, mask, k_hist, k_item, sc_g),
+                                  err_msg="GPU rows differ from the oracle split top-k of the GPU scores")
+    k_asm2, v_asm2 = ops.kv_assemble(w.pools, segs, w.k_fresh, w.v_fresh, cos, sin)
+    rows2, _ = ops.select_tokens_eq3(segs, mask, lam, k_hist, k_item, w.k_fresh, w.v_fresh, k_asm2,
+                                     v_asm2, scores_in=torch.from_numpy(sc_o).to(device), patch=False)
+    np.testing.assert_array_equal(rows2.cpu().numpy(),
+                                  O.topk_split(segs_h, cfg.N, mask, k_hist, k_item, sc_o),
+                                  err_msg="GPU split top-k of the oracle scores differs")
+    np.testing.assert_array_equal(H(k_asm2), ka_o, err_msg="assembled K differs")
+    np.testing.assert_array_equal(H(v_asm2), va_o, err_msg="assembled V differs")
+
+    # ---- patch: bit-exact
+    kp_o, vp_o = O.patch(segs_h, rows_g, kf, vf, ka_o, va_o)
+    np.testing.assert_array_equal(H(bufs.k_asm), kp_o, err_msg="patched K differs")
+    np.testing.assert_array_equal(H(bufs.v_asm), vp_o, err_msg="patched V differs")
+    return stats, bufs

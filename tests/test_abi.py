@@ -154,3 +154,47 @@ def test_attention_validation(lib):
     assert call(shape=_shape(Hq=12, Hkv=4)) == -2     # bf16 group of 3 does not divide 128
     assert call(shape=_shape(D=256)) == -2
     assert call(R=0) == 0                             # nothing to do, nothing enqueued
+
+
+@no_gpu
+def test_attention_lse_and_mass_validation(lib):
+    def att(shape=None, rows=None, R=64, lse=FAKE):
+        return lib.rc_selective_attention_lse(_shape() if shape is None else shape, FAKE, rows, R, FAKE,
+                                              FAKE, ctypes.c_float(0.088), FAKE, lse, None)
+
+    assert att(lse=None) == -1
+    assert att(R=10) == -1                            # full mode needs R == N
+    assert att(shape=_shape(Hq=12, Hkv=4)) == -2
+    assert att(R=0, rows=FAKE, lse=None) == 0         # nothing to do
+
+    def mass(shape=None, q=FAKE, lse=FAKE, out=FAKE, scale=0.088):
+        return lib.rc_attention_mass(_shape() if shape is None else shape, q, FAKE, lse,
+                                     ctypes.c_float(scale), out, None)
+
+    assert mass(q=None) == -1
+    assert mass(lse=None) == -1
+    assert mass(out=None) == -1
+    assert mass(scale=-1.0) == -1
+    assert mass(shape=_shape(D=96)) == -2
+    assert mass(shape=_shape(Hq=12, Hkv=4)) == -2     # bf16 group of 3 does not divide 128
+    assert mass(shape=_shape(Hq=6, Hkv=4)) == -1
+
+
+@no_gpu
+def test_select_eq3_validation(lib):
+    def call(shape=None, n_fresh=8, mask=2, lam=0.5, kh=5, ki=5, mass=FAKE, scores_in=None,
+             scores_out=FAKE, rows=FAKE, patch=1, vf=FAKE, va=FAKE):
+        return lib.rc_select_tokens_eq3(_shape() if shape is None else shape, FAKE, 3, n_fresh, mask,
+                                        ctypes.c_float(lam), kh, ki, mass, FAKE, vf, FAKE, va,
+                                        scores_in, scores_out, rows, patch, None)
+
+    assert call(kh=-1) == -1
+    assert call(kh=30, ki=27) == -1                   # budgets exceed N - n_fresh
+    assert call(mass=None) == -1                      # scoring needs the mass
+    assert call(vf=None, patch=0) == -1               # scoring needs V
+    assert call(lam=1.5) == -1
+    assert call(lam=float("nan")) == -1
+    assert call(mask=1 << 8) == -1                    # pools beyond 8
+    assert call(rows=None) == -1
+    assert call(scores_out=None) == -1
+    assert call(shape=_shape(N=16385)) == -2

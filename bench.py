@@ -48,6 +48,8 @@ def parse_args():
                     help="requests of batch 0 in the CPU oracle's sample (default: all; 0 = skip)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="repeat the CPU oracle's sample until this much time has passed")
+    ap.add_argument("--no-paged", action="store_true",
+                    help="skip timing the zero-copy (paged attention) variant")
     ap.add_argument("--no-eq3", action="store_true",
                     help="skip timing the selection by the full Eq. (3) score")
     ap.add_argument("--no-full-prefill", action="store_true",
@@ -232,6 +234,52 @@ def main():
                 "selective_speedup": round(fms / ms_per_step, 3)}
         del fout
 
+    # ---- zero-copy variant: score-only alignment pass, top-k, paged attention
+    paged = None
+    if not args.no_paged and cfg.dtype == "bf16" and R > 0:
+        pbuf = ops.PrefillBuffers.alloc(B, N, Hq, Hkv, D, R, cfg.torch_dtype, dev)
+
+        def stepp(i, ev=None):
+            w, segs, _ = batches[i % len(batches)]
+            if ev is not None:
+                ev[0].record(stream)
+            ops.kv_assemble(w.pools, segs, w.k_fresh, w.v_fresh, cos, sin, scores_out=pbuf.scores,
+                            score_only=True)
+            if ev is not None:
+                ev[1].record(stream)
+            ops.select_tokens(segs, k, w.k_fresh, w.v_fresh, None, None, scores_in=pbuf.scores,
+                              rows_out=pbuf.rows, patch=False)
+            if ev is not None:
+                ev[2].record(stream)
+            ops.paged_attention(w.q, w.k_fresh, w.v_fresh, w.pools, segs, pbuf.rows, cos, sin,
+                                None, pbuf.out)
+            if ev is not None:
+                ev[3].record(stream)
+
+        for i in range(3):
+            stepp(i)
+        torch.cuda.synchronize()
+        reps = max(5, min(50, args.steps // 2))
+        evp = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(reps)]
+        for i in range(reps):
+            stepp(i, evp[i])
+        torch.cuda.synchronize()
+        pp = [sum(e[j].elapsed_time(e[j + 1]) for e in evp) / reps for j in range(3)]
+        p_ms = sum(e[0].elapsed_time(e[3]) for e in evp) / reps
+        p_flops = sum(att_flops[i % len(batches)] for i in range(reps)) / reps
+        score_bytes = 2.0 * B * (N - cfg.n_fresh) * row + 4.0 * B * N
+        pa_tf = p_flops / (pp[2] * 1e-3) / 1e12
+        paged = {"ms": round(p_ms, 4), "selected_tokens_per_s": round(B * R / (p_ms * 1e-3), 1),
+                 "vs_assembled_step": round(ms_per_step / p_ms, 3),
+                 "kernels": {
+                     "rc_kv_assemble_score_only": dict(us=round(pp[0] * 1e3, 2), **hbm(score_bytes, pp[0])),
+                     "rc_select_tokens_no_patch": {"us": round(pp[1] * 1e3, 2)},
+                     "rc_paged_attention": {"us": round(pp[2] * 1e3, 2), "bound": "mfma",
+                                            "achieved": round(pa_tf, 2), "peak": mfma_peak,
+                                            "unit": "TFLOP/s", "frac": round(pa_tf / mfma_peak, 4),
+                                            "flops_per_launch": p_flops}}}
+        del pbuf
+
     # ---- selection by the full Eq. (3) score: the first layer in full (with
     # log-sum-exp), attention mass, assembly, score, history/item top-k, patch
     eq3 = None
@@ -344,6 +392,7 @@ def main():
         "roofline": roofline,
         "kernels": kernels,
         "full_prefill": full,
+        "paged_prefill": paged,
         "eq3_selection": eq3,
         "cpu_baseline": cpu,
         "wall_s_timed": round(wall, 3),

@@ -29,6 +29,15 @@
  *                               (dropped for item blocks), separate history
  *                               and item budgets, and the correction (iii)
  *
+ * Zero-copy variant and the local window:
+ *
+ *   rc_paged_attention          selective attention that reads K/V through
+ *                               the segment table (no assembled copy),
+ *                               aligning pool keys and taking fresh rows for
+ *                               the recomputed positions while it stages them
+ *   rc_segments_with_window     (host) the last W positions of every request
+ *                               become fresh (recomputed) segments
+ *
  * Conventions shared by every call
  * --------------------------------
  * - Pointers are DEVICE pointers unless marked (host). The caller owns every
@@ -133,7 +142,8 @@ int rc_rope_table(int32_t max_pos, int32_t D, double base, float* cos_out, float
  * ignored); otherwise both must be given with max_pos >= N.
  * pools: host array of n_pools rc_pool (1..8). segs: device [B, S].
  * k_fresh/v_fresh: device [B, N, Hkv, D]; rows of fresh segments are copied.
- * k_asm/v_asm: device [B, N, Hkv, D] outputs (must not alias inputs).
+ * k_asm/v_asm: device [B, N, Hkv, D] outputs (must not alias inputs); both
+ * NULL with scores_out given: score only (nothing is assembled or stored).
  * scores_out: NULL, or device [B, N] fp32: the same pass then also reads the
  * fresh K row of every cached position and writes the deviation score of
  * Eq. (3) (M = K, lambda = 1) of the row it produced, exactly as
@@ -256,6 +266,42 @@ int rc_select_tokens_eq3(const rc_shape* shape, const rc_segment* segs, int32_t 
                          int32_t k_item, const float* mass, const void* k_fresh,
                          const void* v_fresh, void* k_asm, void* v_asm, const float* scores_in,
                          float* scores_out, int32_t* rows, int32_t patch, hipStream_t stream);
+
+/* Zero-copy selective attention (the logical-to-physical block mapping of
+ * Sec. III-A applied inside attention; Sec. III-C.2b, III-C.3 (i)-(iii) and
+ * Eq. (1) without an assembled K/V copy). Computes exactly what
+ *   rc_kv_assemble (with the tables) -> patch of every listed row ->
+ *   rc_selective_attention
+ * computes, bit for bit, but each key row is fetched while its tile is
+ * staged: position j of request b reads the fresh K/V row if j lies in a
+ * fresh segment or is itself listed in rows (a recomputed heavy hitter),
+ * else the pool row pool.k/v[block][j - dst_start], whose key is rotated by
+ * dst_start in fp32 (the gather's operation order) when tables are given.
+ * rows: [B, R] int32 (required); q: [B, N, Hq, D]; k_fresh, v_fresh:
+ * [B, N, Hkv, D]; pools/segs as for rc_kv_assemble; out: [B, R, Hq, D].
+ * Scores for the selection can be taken without an assembled copy by
+ * rc_kv_assemble with k_asm = v_asm = NULL.
+ * Errors: those of rc_selective_attention; INVALID_ARG for NULL
+ * pools/segs/fresh tensors, bad pools, max_pos < N with tables;
+ * UNSUPPORTED for fp32 storage, S > 64 segments, N > 16384. */
+int rc_paged_attention(const rc_shape* shape, const void* q, const int32_t* rows, int32_t R,
+                       const rc_pool* pools, int32_t n_pools, const rc_segment* segs, int32_t S,
+                       const void* k_fresh, const void* v_fresh, const float* rope_cos,
+                       const float* rope_sin, int32_t max_pos, float scale, void* out,
+                       hipStream_t stream);
+
+/* Local sliding window (host; Sec. III-C.2b recomputes the heavy hitters and
+ * the local sliding window). Rewrites the segment tables segs_in [B, S]
+ * (host) so that positions [N - W, N) of every request are fresh: segments
+ * starting before N - W are kept (the one crossing it is cut there), then the
+ * window follows as fresh segments, split into single-token pieces plus one
+ * remainder where needed so that every request has the same count S_out
+ * (<= S + 1). segs_out: host array of at least B * S_cap entries, written as
+ * [B, S_out]. W = 0 copies the tables. Errors: INVALID_ARG for NULL
+ * pointers, tables that do not tile [0, N) in order, W outside [0, N), a
+ * window shorter than the pieces it needs, S_cap < S_out. */
+int rc_segments_with_window(const rc_segment* segs_in, int32_t B, int32_t S, int32_t N,
+                            int32_t W, rc_segment* segs_out, int32_t S_cap, int32_t* S_out);
 
 /* Static description of a status code. */
 const char* rc_status_string(int status);

@@ -319,6 +319,47 @@ def eq3_select(q, k_fresh, v_fresh, pools, segs, item_mask: int, lam: float, k_h
     return dict(k_asm=k_asm, v_asm=v_asm, mass=mass, scores=scores, rows=rows)
 
 
+def position_map(segs_b, N: int) -> list:
+    """Per position of one request: None (fresh) or (pool, block row, rotation
+    delta) -- the row the position reads and the angle it is aligned by."""
+    m = [None] * N
+    for dst, ln, p, blk in np.asarray(segs_b).tolist():
+        for t in range(ln):
+            m[dst + t] = None if p < 0 else (p, blk, t, dst)
+    return m
+
+
+def segments_with_window(segs, N: int, W: int) -> np.ndarray:
+    """The local sliding window (Sec. III-C.2b: heavy hitters and the local
+    sliding window are recomputed): positions [N - W, N) of every request
+    become fresh. Segments are clipped at N - W and one fresh segment covers
+    the window; requests with fewer segments split their window segment so
+    that the table stays [B, S] (a cached segment is never split: its
+    dst_start fixes both the block offset and the rotation)."""
+    segs = np.asarray(segs, np.int32)
+    cut = N - W
+    tables = []
+    for req in segs.tolist():
+        runs = []
+        for dst, ln, p, blk in req:
+            end = min(dst + ln, cut)
+            if dst < end:
+                runs.append([dst, end - dst, p, blk])
+        if W > 0:
+            runs.append([cut, W, -1, 0])
+        tables.append(runs)
+    S = max(len(t) for t in tables)
+    out = np.zeros((len(tables), S, 4), np.int32)
+    for b, runs in enumerate(tables):
+        while len(runs) < S:
+            dst, ln, p, blk = runs[-1]
+            if p >= 0 or ln < 2:
+                raise ValueError("the window is too short to pad the segment table")
+            runs[-1:] = [[dst, ln - 1, -1, 0], [dst + ln - 1, 1, -1, 0]]
+        out[b] = np.array(runs, np.int32)
+    return out
+
+
 # ---------------------------------------------------------------------------
 # bf16 conversions for host-side comparisons (exact widening; RNE narrowing)
 # ---------------------------------------------------------------------------

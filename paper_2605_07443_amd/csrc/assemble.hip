@@ -14,7 +14,7 @@
 namespace rc {
 namespace {
 
-using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
+using u32x4 = u32x4_t;
 
 constexpr int kThreads = 256;
 constexpr int kMaxTok = 256;      // positions per workgroup (small rows)
@@ -24,48 +24,16 @@ constexpr int kKItems = kKPer * kThreads;   // key pairs per pass
 constexpr int kVItems = kVPer * kThreads;   // value units per pass
 constexpr int kRowBytesPerWg = kKItems * 32;  // key-row bytes of a workgroup (8 KiB)
 
-// Rotate E = 16/ES elements of the first half (a) and second half (b) of a
-// head by the angle whose cos/sin are c[0..E), s[0..E).
-//   a' = a*c - b*s,  b' = a*s + b*c   (fp32, no contraction), then RNE.
-template <int ES>
-__device__ __forceinline__ void rotate_unit(u32x4& a, u32x4& b, const float* c, const float* s) {
-#pragma clang fp contract(off)
-  if constexpr (ES == 4) {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float x = __uint_as_float(a[e]);
-      const float y = __uint_as_float(b[e]);
-      const float xc = x * c[e], ys = y * s[e], xs = x * s[e], yc = y * c[e];
-      a[e] = __float_as_uint(xc - ys);
-      b[e] = __float_as_uint(xs + yc);
-    }
-  } else {
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      uint32_t na = 0, nb = 0;
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int e = 2 * w + h;
-        const float x = bf16_to_f32(static_cast<uint16_t>(a[w] >> (16 * h)));
-        const float y = bf16_to_f32(static_cast<uint16_t>(b[w] >> (16 * h)));
-        const float xc = x * c[e], ys = y * s[e], xs = x * s[e], yc = y * c[e];
-        na |= static_cast<uint32_t>(f32_to_bf16(xc - ys)) << (16 * h);
-        nb |= static_cast<uint32_t>(f32_to_bf16(xs + yc)) << (16 * h);
-      }
-      a[w] = na;
-      b[w] = nb;
-    }
-  }
-}
-
 // ASSEMBLE: source rows come from the segment table (pool block or fresh
 // row), V is copied as well, delta = dst_start for pool rows when tables are
 // given. REROPE (in place): source = destination = k, delta from the array.
 // SCORE (with ASSEMBLE): also reads the fresh K row of every cached position
 // and writes the deviation score sum |K_fresh - K_asm| of the row it just
 // produced (0 at fresh positions, whose assembled row is the fresh row).
+// WRITE = false (with ASSEMBLE and SCORE): score only -- the aligned key rows
+// are formed in registers and compared, nothing is stored and V is not read.
 // Every load of a workgroup's 16-byte units is issued before the first use.
-template <int ES, bool ASSEMBLE, bool SCORE>
+template <int ES, bool ASSEMBLE, bool SCORE, bool WRITE = true>
 __global__ __launch_bounds__(kThreads) void kv_rows_kernel(
     PoolArgs pools, const int4* __restrict__ segs, int S, int N, int tok_per_wg, int row_units,
     int head_units, const char* __restrict__ k_fresh, const char* __restrict__ v_fresh,
@@ -129,7 +97,7 @@ __global__ __launch_bounds__(kThreads) void kv_rows_kernel(
   const int pairs_per_row = row_units / 2;
   const int half_units = head_units / 2;
   const int k_items = tok_cnt * pairs_per_row;
-  const int v_items = ASSEMBLE ? tok_cnt * row_units : 0;
+  const int v_items = (ASSEMBLE && WRITE) ? tok_cnt * row_units : 0;
   for (int it = 0; it * kKItems < k_items || it * kVItems < v_items; ++it) {
     // ---- issue every load: key pairs (+ fresh key pairs), value units
     u32x4 ua[kKPer], ub[kKPer], fa[kKPer], fb[kKPer], vv[kVPer];
@@ -165,7 +133,7 @@ __global__ __launch_bounds__(kThreads) void kv_rows_kernel(
         }
       }
     }
-    if constexpr (ASSEMBLE) {
+    if constexpr (ASSEMBLE && WRITE) {
 #pragma unroll
       for (int u = 0; u < kVPer; ++u) {
         const int idx = it * kVItems + u * kThreads + tid;
@@ -194,13 +162,15 @@ __global__ __launch_bounds__(kThreads) void kv_rows_kernel(
           }
           rotate_unit<ES>(ua[u], ub[u], c, sn);
         }
-        u32x4* dst = reinterpret_cast<u32x4*>(k_out + (static_cast<size_t>(b) * N + i0 + ktok[u]) * row_bytes);
-        if constexpr (ASSEMBLE) {
-          __builtin_nontemporal_store(ua[u], dst + kunit[u]);
-          __builtin_nontemporal_store(ub[u], dst + kunit[u] + half_units);
-        } else {
-          dst[kunit[u]] = ua[u];
-          dst[kunit[u] + half_units] = ub[u];
+        if constexpr (WRITE) {
+          u32x4* dst = reinterpret_cast<u32x4*>(k_out + (static_cast<size_t>(b) * N + i0 + ktok[u]) * row_bytes);
+          if constexpr (ASSEMBLE) {
+            __builtin_nontemporal_store(ua[u], dst + kunit[u]);
+            __builtin_nontemporal_store(ub[u], dst + kunit[u] + half_units);
+          } else {
+            dst[kunit[u]] = ua[u];
+            dst[kunit[u] + half_units] = ub[u];
+          }
         }
       }
       if constexpr (SCORE) {
@@ -209,7 +179,7 @@ __global__ __launch_bounds__(kThreads) void kv_rows_kernel(
           s_part[idx] = fok[u] ? absdiff_sum<ES>(fa[u], ua[u]) + absdiff_sum<ES>(fb[u], ub[u]) : 0.f;
       }
     }
-    if constexpr (ASSEMBLE) {
+    if constexpr (ASSEMBLE && WRITE) {
 #pragma unroll
       for (int u = 0; u < kVPer; ++u) {
         if (!vok[u]) continue;
@@ -260,6 +230,9 @@ int launch_rows(const rc_shape* s, const PoolArgs& pools, const int4* segs, int 
   if (!ASSEMBLE) {
     if (s->dtype == RC_BF16) args(kv_rows_kernel<2, false, false>);
     else args(kv_rows_kernel<4, false, false>);
+  } else if (scores && !k_out) {
+    if (s->dtype == RC_BF16) args(kv_rows_kernel<2, true, true, false>);
+    else args(kv_rows_kernel<4, true, true, false>);
   } else if (scores) {
     if (s->dtype == RC_BF16) args(kv_rows_kernel<2, true, true>);
     else args(kv_rows_kernel<4, true, true>);
@@ -285,15 +258,19 @@ extern "C" int rc_kv_assemble(const rc_shape* shape, const rc_pool* pools, int32
     return fail(n_pools > kMaxPools ? RC_ERR_UNSUPPORTED : RC_ERR_INVALID_ARG,
                 "n_pools=%d (1..%d)", n_pools, kMaxPools);
   if (!pools) return fail(RC_ERR_INVALID_ARG, "pools is NULL");
-  if (!segs || !k_fresh || !v_fresh || !k_asm || !v_asm)
-    return fail(RC_ERR_INVALID_ARG, "segs, k_fresh, v_fresh, k_asm and v_asm must be non-NULL");
+  if (!segs || !k_fresh || !v_fresh)
+    return fail(RC_ERR_INVALID_ARG, "segs, k_fresh and v_fresh must be non-NULL");
+  if ((k_asm == nullptr) != (v_asm == nullptr))
+    return fail(RC_ERR_INVALID_ARG, "k_asm and v_asm must both be given or both be NULL");
+  if (!k_asm && !scores_out)
+    return fail(RC_ERR_INVALID_ARG, "without k_asm/v_asm (score only) scores_out is required");
   if (S < 1) return fail(RC_ERR_INVALID_ARG, "S=%d must be >= 1", S);
   if (S > kMaxSegments) return fail(RC_ERR_UNSUPPORTED, "S=%d exceeds %d segments", S, kMaxSegments);
   if ((rope_cos == nullptr) != (rope_sin == nullptr))
     return fail(RC_ERR_INVALID_ARG, "rope_cos and rope_sin must both be given or both be NULL");
   if (rope_cos && max_pos < shape->N)
     return fail(RC_ERR_INVALID_ARG, "max_pos=%d < N=%d", max_pos, shape->N);
-  if (k_asm == k_fresh || v_asm == v_fresh || k_asm == v_asm)
+  if (k_asm && (k_asm == k_fresh || v_asm == v_fresh || k_asm == v_asm))
     return fail(RC_ERR_INVALID_ARG, "outputs alias inputs");
   PoolArgs pa{};
   pa.n = n_pools;

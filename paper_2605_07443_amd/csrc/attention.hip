@@ -24,6 +24,13 @@
 //     sharing its L2 for the K/V stream. Each XCD starts its longest (latest)
 //     tiles first, across all of its groups when the batch's K/V fits the
 //     Infinity Cache, else within chunks of groups that fit its L2.
+// Paged mode (zero-copy, over the logical-to-physical block mapping of
+// Sec. III-A): no assembled copy exists; each key of a tile is resolved
+// through the request's segment table while it is staged -- a fresh row, the
+// fresh row again when the key is itself a recomputed row (the heavy-hitter
+// update of Sec. III-C.3 (iii)), or the pool row, whose key pairs are rotated
+// by the segment's dst_start in registers (step (ii)) before they reach LDS.
+// The tiles are then bit-identical to those of the assembled path.
 // fp32 path: one wave per (request, row, head), fp32 FMA on the vector ALUs.
 #include <cmath>
 #include <type_traits>
@@ -37,6 +44,7 @@ constexpr int kAttnThreads = 256;
 constexpr int kM = 128;  // query vectors per workgroup
 constexpr int kKT = 64;  // keys per KV tile
 constexpr int kXcds = 8;
+constexpr int kPagedMaxSegments = 64;  // segment table of a request kept in LDS
 
 using u32x2 = uint32_t __attribute__((ext_vector_type(2)));
 using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
@@ -81,13 +89,17 @@ constexpr float kLazy = 8.f;
 // (Full-Recompute). Separate instances keep the two modes apart in profiles.
 // LSE: also write each row's natural log-sum-exp, from an fp32 sum of the
 // unrounded exponentials (the bf16 column sums only normalise O).
-template <int D, bool SELECTIVE, bool LSE>
+// PAGED: k, v are the fresh tensors; other keys come from `pools` through
+// `segs` (S <= kPagedMaxSegments), rotated with the cos/sin tables when given.
+template <int D, bool SELECTIVE, bool LSE, bool PAGED>
 __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict__ rows, int R,
                       int N, int Hq, int Hkv, int G, int BR, const uint16_t* __restrict__ k,
                       const uint16_t* __restrict__ v, float scale_log2e,
                       uint16_t* __restrict__ out, float* __restrict__ lse, int n_tiles,
-                      int n_groups, int gpx, int chunk) {
+                      int n_groups, int gpx, int chunk, PoolArgs pools,
+                      const int4* __restrict__ segs, int S, const float* __restrict__ cos_t,
+                      const float* __restrict__ sin_t, int max_pos) {
   constexpr int DC = D / 32;          // 32-wide d chunks (S^T reduction)
   constexpr int DB = D / 16;          // 16-wide d blocks (O^T rows)
   constexpr int UPR = D / 8;          // 16-byte units per K/V head row
@@ -95,6 +107,8 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
   constexpr int KSTEP = kAttnThreads / UPR;      // keys between a thread's units
   __shared__ AttnSmem<D> sm;
   __shared__ int s_ext[4];
+  __shared__ int4 s_psegs[PAGED ? kPagedMaxSegments : 1];
+  __shared__ uint32_t s_sel[PAGED ? kMaxSelectN / 32 : 1];  // recomputed rows of the request
 
   // ---- work item: XCD-major; the XCD's groups in chunks of `chunk` groups,
   // longest tiles first within a chunk
@@ -142,6 +156,15 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
   pmax = wave_max_i(pmax);
   const int wave_pmin = wave_min_i(pmin);
   if (lane == 0) s_ext[wave] = pmax;
+  if constexpr (PAGED) {
+    for (int s = tid; s < S; s += kAttnThreads) s_psegs[s] = segs[static_cast<size_t>(b) * S + s];
+    for (int w = tid; w < (N + 31) / 32; w += kAttnThreads) s_sel[w] = 0u;
+    __syncthreads();
+    for (int r = tid; r < R; r += kAttnThreads) {
+      const int p = rows[static_cast<size_t>(b) * R + r];
+      if (p >= 0 && p < N) atomicOr(&s_sel[p >> 5], 1u << (p & 31));
+    }
+  }
   __syncthreads();
   const int wg_pmax = max(max(s_ext[0], s_ext[1]), max(s_ext[2], s_ext[3]));
   const int n_kv = wg_pmax / kKT + 1;
@@ -156,16 +179,54 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
       qf[nb][dc] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(qrow + dc * 32 + q4 * 8));
   }
 
-  // ---- K/V staging: thread owns units (key tid/UPR + i*KSTEP, dims (tid%UPR)*8 ..)
+  // ---- K/V staging: thread owns units (key tid/UPR + i*KSTEP, dims (tid%UPR)*8 ..);
+  // paged: key pairs (key tid/PPR + i*PSTEP, dims ps*8 .. and ps*8 + D/2 ..)
   const size_t stride = static_cast<size_t>(Hkv) * D;   // elements between keys
-  const int key0 = tid / UPR;
-  const int col0 = (tid % UPR) * 8;
+  constexpr int PPR = UPR / 2;                           // pair slots per key head row
+  constexpr int PSTEP = kAttnThreads / PPR;              // keys between a thread's pairs
+  constexpr int PK = kKT / PSTEP;                        // key pairs per thread
+  static_assert(2 * PK == KU, "paged staging moves as many units as plain staging");
+  const int key0 = PAGED ? tid / PPR : tid / UPR;
+  const int col0 = PAGED ? (tid % PPR) * 8 : (tid % UPR) * 8;
   const size_t off0 = (static_cast<size_t>(b) * N + key0) * stride + static_cast<size_t>(g) * D + col0;
   const uint16_t* kp = k + off0;
   const uint16_t* vp = v + off0;
   const size_t tile_step = static_cast<size_t>(kKT) * stride;
   u32x4 kreg[KU], vreg[KU];
+  int pdelta[PAGED ? PK : 1];  // paged: rotation of each staged key (0: none)
   auto load_tile = [&](int t) {
+    if constexpr (PAGED) {
+#pragma unroll
+      for (int i = 0; i < PK; ++i) {
+        const int j = t * kKT + key0 + i * PSTEP;
+        const uint16_t* ks = nullptr;
+        const uint16_t* vs = nullptr;
+        int d = 0;
+        if (j < N) {
+          const int sg = find_segment(s_psegs, S, j);
+          const int4 sgm = sg >= 0 ? s_psegs[sg] : int4{0, 0, -1, 0};
+          const bool fresh = sgm.z < 0 || ((s_sel[j >> 5] >> (j & 31)) & 1u);
+          if (fresh) {
+            const size_t o = (static_cast<size_t>(b) * N + j) * stride + static_cast<size_t>(g) * D + col0;
+            ks = k + o;
+            vs = v + o;
+          } else if (sgm.z < pools.n && sgm.w >= 0 && sgm.w < pools.num_blocks[sgm.z] &&
+                     j - sgm.x < pools.block_len[sgm.z]) {
+            const size_t prow = static_cast<size_t>(sgm.w) * pools.block_len[sgm.z] + (j - sgm.x);
+            const size_t o = prow * stride + static_cast<size_t>(g) * D + col0;
+            ks = reinterpret_cast<const uint16_t*>(pools.k[sgm.z]) + o;
+            vs = reinterpret_cast<const uint16_t*>(pools.v[sgm.z]) + o;
+            if (cos_t != nullptr && sgm.x < max_pos) d = sgm.x;
+          }
+        }
+        pdelta[i] = d;
+        kreg[2 * i] = ks ? *reinterpret_cast<const u32x4*>(ks) : u32x4{0, 0, 0, 0};
+        kreg[2 * i + 1] = ks ? *reinterpret_cast<const u32x4*>(ks + D / 2) : u32x4{0, 0, 0, 0};
+        vreg[2 * i] = vs ? *reinterpret_cast<const u32x4*>(vs) : u32x4{0, 0, 0, 0};
+        vreg[2 * i + 1] = vs ? *reinterpret_cast<const u32x4*>(vs + D / 2) : u32x4{0, 0, 0, 0};
+      }
+      return;
+    }
     const uint16_t* kt = kp + t * tile_step;
     const uint16_t* vt = vp + t * tile_step;
     if ((t + 1) * kKT <= N) {
@@ -184,6 +245,29 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
     }
   };
   auto store_tile = [&](int buf) {
+    if constexpr (PAGED) {
+#pragma unroll
+      for (int i = 0; i < PK; ++i) {
+        const int d = pdelta[i];
+        if (d != 0) {  // same fp32 operation order and rounding as the gather
+          float c[8], sn[8];
+          const float* crow = cos_t + static_cast<size_t>(d) * (D / 2) + col0;
+          const float* srow = sin_t + static_cast<size_t>(d) * (D / 2) + col0;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            c[e] = crow[e];
+            sn[e] = srow[e];
+          }
+          rotate_unit<2>(kreg[2 * i], kreg[2 * i + 1], c, sn);
+        }
+        const int key = key0 + i * PSTEP;
+        *reinterpret_cast<u32x4*>(&sm.k[buf][key][col0]) = kreg[2 * i];
+        *reinterpret_cast<u32x4*>(&sm.k[buf][key][col0 + D / 2]) = kreg[2 * i + 1];
+        *reinterpret_cast<u32x4*>(&sm.v[buf][key][col0]) = vreg[2 * i];
+        *reinterpret_cast<u32x4*>(&sm.v[buf][key][col0 + D / 2]) = vreg[2 * i + 1];
+      }
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < KU; ++i) {
       *reinterpret_cast<u32x4*>(&sm.k[buf][key0 + i * KSTEP][col0]) = kreg[i];
@@ -429,9 +513,19 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(const float* __restrict__
 namespace rc {
 namespace {
 
+struct Paged {
+  PoolArgs pools;
+  const int4* segs;
+  int S;
+  const float* cos_t;
+  const float* sin_t;
+  int max_pos;
+};
+
+// paged == nullptr: k, v are the assembled tensors; else the fresh tensors.
 int attention_impl(const rc_shape* shape, const void* q, const int32_t* rows, int32_t R,
                    const void* k, const void* v, float scale, void* out, float* lse,
-                   hipStream_t stream, const char* what) {
+                   const Paged* paged, hipStream_t stream, const char* what) {
   if (int st = check_shape(shape, true)) return st;
   if (R < 0) return fail(RC_ERR_INVALID_ARG, "R=%d must be >= 0", R);
   if (!q || !k || !v || (!out && R > 0))
@@ -461,25 +555,31 @@ int attention_impl(const rc_shape* shape, const void* q, const int32_t* rows, in
     if (blocks > 0x7fffffff) return fail(RC_ERR_UNSUPPORTED, "grid too large");
     const float scale_log2e = static_cast<float>(static_cast<double>(scale) * 1.4426950408889634);
     dim3 grid(static_cast<unsigned>(blocks));
+    const Paged none{};
+    const Paged& pg = paged ? *paged : none;
     auto launch = [&](auto kern) {
       hipLaunchKernelGGL(kern, grid, dim3(kAttnThreads), 0, stream,
                          static_cast<const uint16_t*>(q), rows, R, N, Hq, Hkv, G, BR,
                          static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
                          scale_log2e, static_cast<uint16_t*>(out), lse, n_tiles, n_groups, gpx,
-                         chunk);
+                         chunk, pg.pools, pg.segs, pg.S, pg.cos_t, pg.sin_t, pg.max_pos);
     };
-    if (lse) {
+    if (paged) {
+      if (D == 128) launch(attn_bf16_kernel<128, true, false, true>);
+      else launch(attn_bf16_kernel<64, true, false, true>);
+    } else if (lse) {
       if (D == 128)
-        rows ? launch(attn_bf16_kernel<128, true, true>) : launch(attn_bf16_kernel<128, false, true>);
+        rows ? launch(attn_bf16_kernel<128, true, true, false>) : launch(attn_bf16_kernel<128, false, true, false>);
       else
-        rows ? launch(attn_bf16_kernel<64, true, true>) : launch(attn_bf16_kernel<64, false, true>);
+        rows ? launch(attn_bf16_kernel<64, true, true, false>) : launch(attn_bf16_kernel<64, false, true, false>);
     } else {
       if (D == 128)
-        rows ? launch(attn_bf16_kernel<128, true, false>) : launch(attn_bf16_kernel<128, false, false>);
+        rows ? launch(attn_bf16_kernel<128, true, false, false>) : launch(attn_bf16_kernel<128, false, false, false>);
       else
-        rows ? launch(attn_bf16_kernel<64, true, false>) : launch(attn_bf16_kernel<64, false, false>);
+        rows ? launch(attn_bf16_kernel<64, true, false, false>) : launch(attn_bf16_kernel<64, false, false, false>);
     }
   } else {
+    if (paged) return fail(RC_ERR_UNSUPPORTED, "paged attention is implemented for bf16");
     const int64_t total = static_cast<int64_t>(B) * R * Hq;
     const int64_t blocks = (total + 3) / 4;
     if (blocks > 0x7fffffff) return fail(RC_ERR_UNSUPPORTED, "grid too large");
@@ -505,7 +605,7 @@ extern "C" int rc_selective_attention(const rc_shape* shape, const void* q, cons
                                       int32_t R, const void* k, const void* v, float scale,
                                       void* out, hipStream_t stream) {
   rc::clear_error();
-  return rc::attention_impl(shape, q, rows, R, k, v, scale, out, nullptr, stream,
+  return rc::attention_impl(shape, q, rows, R, k, v, scale, out, nullptr, nullptr, stream,
                             "rc_selective_attention");
 }
 
@@ -515,6 +615,49 @@ extern "C" int rc_selective_attention_lse(const rc_shape* shape, const void* q,
                                           hipStream_t stream) {
   rc::clear_error();
   if (!lse && R > 0) return rc::fail(RC_ERR_INVALID_ARG, "lse must be non-NULL");
-  return rc::attention_impl(shape, q, rows, R, k, v, scale, out, lse, stream,
+  return rc::attention_impl(shape, q, rows, R, k, v, scale, out, lse, nullptr, stream,
                             "rc_selective_attention_lse");
+}
+
+extern "C" int rc_paged_attention(const rc_shape* shape, const void* q, const int32_t* rows,
+                                  int32_t R, const rc_pool* pools, int32_t n_pools,
+                                  const rc_segment* segs, int32_t S, const void* k_fresh,
+                                  const void* v_fresh, const float* rope_cos,
+                                  const float* rope_sin, int32_t max_pos, float scale, void* out,
+                                  hipStream_t stream) {
+  using namespace rc;
+  clear_error();
+  if (int st = check_shape(shape, true)) return st;
+  if (!rows && R > 0) return fail(RC_ERR_INVALID_ARG, "rows must be non-NULL");
+  if (n_pools < 1 || n_pools > kMaxPools)
+    return fail(n_pools > kMaxPools ? RC_ERR_UNSUPPORTED : RC_ERR_INVALID_ARG,
+                "n_pools=%d (1..%d)", n_pools, kMaxPools);
+  if (!pools || !segs || !k_fresh || !v_fresh)
+    return fail(RC_ERR_INVALID_ARG, "pools, segs, k_fresh and v_fresh must be non-NULL");
+  if (S < 1) return fail(RC_ERR_INVALID_ARG, "S=%d must be >= 1", S);
+  if (S > kPagedMaxSegments)
+    return fail(RC_ERR_UNSUPPORTED, "S=%d exceeds %d segments", S, kPagedMaxSegments);
+  if (shape->N > kMaxSelectN) return fail(RC_ERR_UNSUPPORTED, "N=%d exceeds %d", shape->N, kMaxSelectN);
+  if ((rope_cos == nullptr) != (rope_sin == nullptr))
+    return fail(RC_ERR_INVALID_ARG, "rope_cos and rope_sin must both be given or both be NULL");
+  if (rope_cos && max_pos < shape->N)
+    return fail(RC_ERR_INVALID_ARG, "max_pos=%d < N=%d", max_pos, shape->N);
+  if (shape->dtype != RC_BF16) return fail(RC_ERR_UNSUPPORTED, "paged attention is implemented for bf16");
+  Paged pg{};
+  pg.pools.n = n_pools;
+  for (int p = 0; p < n_pools; ++p) {
+    if (!pools[p].k || !pools[p].v || pools[p].num_blocks < 1 || pools[p].block_len < 1)
+      return fail(RC_ERR_INVALID_ARG, "pool %d: NULL tensor or empty shape", p);
+    pg.pools.k[p] = static_cast<const char*>(pools[p].k);
+    pg.pools.v[p] = static_cast<const char*>(pools[p].v);
+    pg.pools.num_blocks[p] = pools[p].num_blocks;
+    pg.pools.block_len[p] = pools[p].block_len;
+  }
+  pg.segs = reinterpret_cast<const int4*>(segs);
+  pg.S = S;
+  pg.cos_t = rope_cos;
+  pg.sin_t = rope_sin;
+  pg.max_pos = rope_cos ? max_pos : 0;
+  return attention_impl(shape, q, rows, R, k_fresh, v_fresh, scale, out, nullptr, &pg, stream,
+                        "rc_paged_attention");
 }

@@ -83,4 +83,54 @@ int rc_rope_table(int32_t max_pos, int32_t D, double base, float* cos_out, float
   return RC_OK;
 }
 
+// The local sliding window (Sec. III-C.2b): the last W positions of every
+// request are recomputed like instruction tokens, so they become fresh
+// segments. Segments before N - W are kept, the one crossing N - W is cut
+// there, and the window is appended as fresh pieces -- as many as it takes
+// for every request to end with the same segment count (tables are [B, S]).
+int rc_segments_with_window(const rc_segment* segs_in, int32_t B, int32_t S, int32_t N,
+                            int32_t W, rc_segment* segs_out, int32_t S_cap, int32_t* S_out) {
+  rc::clear_error();
+  if (!segs_in || !segs_out || !S_out) return rc::fail(RC_ERR_INVALID_ARG, "NULL table or S_out");
+  if (B < 1 || S < 1 || N < 1) return rc::fail(RC_ERR_INVALID_ARG, "B=%d S=%d N=%d", B, S, N);
+  if (W < 0 || W > N) return rc::fail(RC_ERR_INVALID_ARG, "window W=%d not in [0, N=%d]", W, N);
+  const int32_t cut = N - W;
+  // segments each request keeps before the window (cut ones count once)
+  int32_t keep_max = 0;
+  for (int32_t b = 0; b < B; ++b) {
+    int32_t keep = 0, pos = 0;
+    for (int32_t s = 0; s < S; ++s) {
+      const rc_segment& g = segs_in[static_cast<size_t>(b) * S + s];
+      if (g.dst_start != pos || g.len < 1)
+        return rc::fail(RC_ERR_INVALID_ARG, "request %d: segments must tile [0, N) in order", b);
+      if (g.dst_start < cut) ++keep;
+      pos += g.len;
+    }
+    if (pos != N) return rc::fail(RC_ERR_INVALID_ARG, "request %d: segments cover %d of N=%d", b, pos, N);
+    keep_max = keep > keep_max ? keep : keep_max;
+  }
+  const int32_t S_new = W > 0 ? keep_max + 1 : keep_max;
+  if (S_new > S_cap) return rc::fail(RC_ERR_INVALID_ARG, "S_cap=%d < %d segments needed", S_cap, S_new);
+  for (int32_t b = 0; b < B; ++b) {
+    rc_segment* out = segs_out + static_cast<size_t>(b) * S_new;
+    int32_t n = 0;
+    for (int32_t s = 0; s < S; ++s) {
+      rc_segment g = segs_in[static_cast<size_t>(b) * S + s];
+      if (g.dst_start >= cut) break;
+      if (g.dst_start + g.len > cut) g.len = cut - g.dst_start;
+      out[n++] = g;
+    }
+    const int32_t pieces = S_new - n;  // >= 1 when W > 0
+    if (pieces > W) return rc::fail(RC_ERR_INVALID_ARG, "window W=%d too short for %d pieces", W, pieces);
+    int32_t pos = cut;
+    for (int32_t i = 0; i < pieces; ++i) {
+      const int32_t len = (i + 1 < pieces) ? 1 : N - pos;  // single tokens, then the rest
+      out[n++] = rc_segment{pos, len, -1, 0};
+      pos += len;
+    }
+  }
+  *S_out = S_new;
+  return RC_OK;
+}
+
 }  // extern "C"

@@ -96,6 +96,40 @@ __device__ __forceinline__ float absdiff_sum(const u32x4_t& a, const u32x4_t& b)
   return acc;
 }
 
+// Rotate E = 16/ES elements of the first half (a) and second half (b) of a
+// head by the angle whose cos/sin are c[0..E), s[0..E).
+//   a' = a*c - b*s,  b' = a*s + b*c   (fp32, no contraction), then RNE.
+template <int ES>
+__device__ __forceinline__ void rotate_unit(u32x4_t& a, u32x4_t& b, const float* c, const float* s) {
+#pragma clang fp contract(off)
+  if constexpr (ES == 4) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float x = __uint_as_float(a[e]);
+      const float y = __uint_as_float(b[e]);
+      const float xc = x * c[e], ys = y * s[e], xs = x * s[e], yc = y * c[e];
+      a[e] = __float_as_uint(xc - ys);
+      b[e] = __float_as_uint(xs + yc);
+    }
+  } else {
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      uint32_t na = 0, nb = 0;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int e = 2 * w + h;
+        const float x = bf16_to_f32(static_cast<uint16_t>(a[w] >> (16 * h)));
+        const float y = bf16_to_f32(static_cast<uint16_t>(b[w] >> (16 * h)));
+        const float xc = x * c[e], ys = y * s[e], xs = x * s[e], yc = y * c[e];
+        na |= static_cast<uint32_t>(f32_to_bf16(xc - ys)) << (16 * h);
+        nb |= static_cast<uint32_t>(f32_to_bf16(xs + yc)) << (16 * h);
+      }
+      a[w] = na;
+      b[w] = nb;
+    }
+  }
+}
+
 // Segment of request-local position i: index of the last segment whose
 // dst_start <= i (segments tile [0, N) in increasing order), or -1.
 __device__ __forceinline__ int find_segment(const int4* segs, int S, int i) {

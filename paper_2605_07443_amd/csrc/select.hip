@@ -105,7 +105,9 @@ __device__ __forceinline__ int block_sum(int x, int* warp_tot) {
 // cached position when item_mask is 0) and class 1 (blocks of the pools set
 // in item_mask). Class c keeps its k_c largest keys, key of position i =
 // score_key(score[i]), order (key desc, i asc). Fresh positions are always
-// taken; the taken positions are written in ascending order.
+// taken; the taken positions are written in ascending order. NC: number of
+// classes with a budget (1: class 0 only, k1 is 0).
+template <int NC>
 __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
     const float* __restrict__ scores, const int4* __restrict__ segs, int S, int N,
     uint32_t item_mask, int k0, int k1, int R, int32_t* __restrict__ rows) {
@@ -114,12 +116,12 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
   __shared__ int4 s_segs[kMaxSegments];
   __shared__ int s_hist[kBins];
   __shared__ int s_wt[kTopkWaves];
-  __shared__ uint32_t s_bounds[2][4];
+  __shared__ uint32_t s_bounds[NC][4];
 
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
   for (int s = tid; s < S; s += kTopkThreads) s_segs[s] = segs[static_cast<size_t>(b) * S + s];
-  if (tid < 2) {
+  if (tid < NC) {
     s_bounds[tid][0] = 0xffffffffu;
     s_bounds[tid][1] = 0u;
   }
@@ -135,7 +137,7 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
     s_key[i] = key;
     s_cls[i] = static_cast<uint8_t>(cls);
 #pragma unroll
-    for (int c = 0; c < 2; ++c)
+    for (int c = 0; c < NC; ++c)
       if (cls == c + 1) {
         kmin[c] = min(kmin[c], key);
         kmax[c] = max(kmax[c], key);
@@ -144,7 +146,7 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
   }
   // block reductions of min/max/count per class
 #pragma unroll
-  for (int c = 0; c < 2; ++c) {
+  for (int c = 0; c < NC; ++c) {
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
       kmin[c] = min(kmin[c], static_cast<uint32_t>(__shfl_xor(static_cast<int>(kmin[c]), off, 64)));
@@ -160,7 +162,7 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
   uint32_t T[2] = {0u, 0u};
   int need[2] = {0, 0};
 #pragma unroll
-  for (int c = 0; c < 2; ++c) {
+  for (int c = 0; c < NC; ++c) {
     if (kc_arg[c] <= 0) continue;  // uniform: kernel arguments
     const int nc = block_sum(ncand[c], s_wt);  // contains barriers
     kk[c] = min(kc_arg[c], nc);
@@ -226,7 +228,7 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
   for (int i = beg; i < end; ++i) {
     const int cls = s_cls[i];
     if (cls == 1 && kk[0] > 0 && s_key[i] == T[0]) ties += 1;
-    if (cls == 2 && kk[1] > 0 && s_key[i] == T[1]) ties += 1 << 16;
+    if (NC == 2 && cls == 2 && kk[1] > 0 && s_key[i] == T[1]) ties += 1 << 16;
   }
   int tot;
   const int tb = block_inclusive_scan(ties, s_wt, tot) - ties;
@@ -237,8 +239,10 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
     bool t;
     if (cls == 0) {
       t = true;
+    } else if (NC == 1 && cls == 2) {
+      t = false;  // class 1 has no budget
     } else {
-      const bool one = cls == 2;
+      const bool one = NC == 2 && cls == 2;
       const int kkc = one ? kk[1] : kk[0];
       const uint32_t Tc = one ? T[1] : T[0];
       const int ndc = one ? need[1] : need[0];
@@ -462,8 +466,12 @@ int select_impl(const rc_shape* shape, const rc_segment* segs, int32_t S, int32_
       return fail(RC_ERR_HIP, "%s: copy of scores_in failed", what);
   }
   if (R > 0) {
-    hipLaunchKernelGGL(topk_kernel, dim3(B), dim3(kTopkThreads), 0, stream, sc, segs4, S, N,
-                       item_mask, k0, k1, R, rows);
+    if (k1 > 0)
+      hipLaunchKernelGGL(topk_kernel<2>, dim3(B), dim3(kTopkThreads), 0, stream, sc, segs4, S, N,
+                         item_mask, k0, k1, R, rows);
+    else  // class 1 takes nothing: its candidates are simply not taken
+      hipLaunchKernelGGL(topk_kernel<1>, dim3(B), dim3(kTopkThreads), 0, stream, sc, segs4, S, N,
+                         item_mask, k0, k1, R, rows);
     if (int st = check_launch(what)) return st;
   }
   if (patch && ksum > 0) {

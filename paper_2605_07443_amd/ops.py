@@ -122,14 +122,20 @@ def _pool_array(pools, dtype, Hkv, D):
 
 
 def kv_assemble(pools, segs: Segments, k_fresh, v_fresh, cos=None, sin=None, k_out=None,
-                v_out=None, scores_out=None, stream=None):
+                v_out=None, scores_out=None, stream=None, score_only=False):
     """rc_kv_assemble: gather + fused re-alignment (+ deviation scores into
-    `scores_out` [B, N] fp32 when given). Returns (k_asm, v_asm)."""
+    `scores_out` [B, N] fp32 when given). Returns (k_asm, v_asm); with
+    score_only the rows are only scored (nothing stored) and (None, None) is
+    returned."""
     B, N, Hkv, D = k_fresh.shape
     if v_fresh.shape != k_fresh.shape or v_fresh.dtype != k_fresh.dtype:
         raise ValueError("k_fresh and v_fresh must match")
-    k_out = torch.empty_like(k_fresh) if k_out is None else k_out
-    v_out = torch.empty_like(v_fresh) if v_out is None else v_out
+    if score_only:
+        if scores_out is None:
+            raise ValueError("score_only needs scores_out")
+    else:
+        k_out = torch.empty_like(k_fresh) if k_out is None else k_out
+        v_out = torch.empty_like(v_fresh) if v_out is None else v_out
     code = _dtype_code(k_fresh)
     parr = _pool_array(pools, k_fresh.dtype, Hkv, D)
     max_pos = 0 if cos is None else int(cos.shape[0])
@@ -137,9 +143,10 @@ def kv_assemble(pools, segs: Segments, k_fresh, v_fresh, cos=None, sin=None, k_o
         ctypes.byref(_shape(B, N, 1, Hkv, D, code)), parr, len(pools), _dev(segs.dev, "segs"),
         segs.S, _dev(k_fresh, "k_fresh"), _dev(v_fresh, "v_fresh"),
         None if cos is None else _dev(cos, "cos"), None if sin is None else _dev(sin, "sin"),
-        max_pos, _dev(k_out, "k_out"), _dev(v_out, "v_out"),
+        max_pos, None if score_only else _dev(k_out, "k_out"),
+        None if score_only else _dev(v_out, "v_out"),
         None if scores_out is None else _dev(scores_out, "scores_out"), _stream(stream)))
-    return k_out, v_out
+    return (None, None) if score_only else (k_out, v_out)
 
 
 def rerope(k, delta, cos, sin, stream=None):
@@ -164,7 +171,8 @@ def select_tokens(segs: Segments, k: int, k_fresh, v_fresh, k_asm, v_asm, scores
     check(_lib.load().rc_select_tokens(
         ctypes.byref(_shape(B, N, 1, Hkv, D, _dtype_code(k_fresh))), _dev(segs.dev, "segs"),
         segs.S, segs.n_fresh, int(k), _dev(k_fresh, "k_fresh"), _dev(v_fresh, "v_fresh"),
-        _dev(k_asm, "k_asm"), _dev(v_asm, "v_asm"),
+        None if k_asm is None else _dev(k_asm, "k_asm"),
+        None if v_asm is None else _dev(v_asm, "v_asm"),
         None if scores_in is None else _dev(scores_in, "scores_in"),
         None if scores_out is None else _dev(scores_out, "scores_out"),
         _dev(rows, "rows"), 1 if patch else 0, _stream(stream)))
@@ -253,11 +261,49 @@ def select_tokens_eq3(segs: Segments, item_mask: int, lam: float, k_hist: int, k
         ctypes.byref(_shape(B, N, 1, Hkv, D, _dtype_code(k_fresh))), _dev(segs.dev, "segs"),
         segs.S, segs.n_fresh, int(item_mask), ctypes.c_float(lam), int(k_hist), int(k_item),
         None if mass is None else _dev(mass, "mass"), _dev(k_fresh, "k_fresh"),
-        _dev(v_fresh, "v_fresh"), _dev(k_asm, "k_asm"), _dev(v_asm, "v_asm"),
+        _dev(v_fresh, "v_fresh"), None if k_asm is None else _dev(k_asm, "k_asm"),
+        None if v_asm is None else _dev(v_asm, "v_asm"),
         None if scores_in is None else _dev(scores_in, "scores_in"),
         None if scores_out is None else _dev(scores_out, "scores_out"),
         _dev(rows, "rows"), 1 if patch else 0, _stream(stream)))
     return rows, (scores_out if scores_out is not None else scores_in)
+
+
+def paged_attention(q, k_fresh, v_fresh, pools, segs: Segments, rows, cos=None, sin=None,
+                    scale=None, out=None, stream=None):
+    """rc_paged_attention: selective attention straight from the pools and
+    fresh tensors through the segment table (no assembled copy)."""
+    B, N, Hq, D = q.shape
+    Hkv = k_fresh.shape[2]
+    if rows.dtype != torch.int32 or rows.dim() != 2 or rows.shape[0] != B:
+        raise ValueError("rows must be int32 [B, R]")
+    R = int(rows.shape[1])
+    scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
+    out = torch.empty((B, R, Hq, D), dtype=q.dtype, device=q.device) if out is None else out
+    parr = _pool_array(pools, k_fresh.dtype, Hkv, D)
+    max_pos = 0 if cos is None else int(cos.shape[0])
+    check(_lib.load().rc_paged_attention(
+        ctypes.byref(_shape(B, N, Hq, Hkv, D, _dtype_code(q))), _dev(q, "q"), _dev(rows, "rows"), R,
+        parr, len(pools), _dev(segs.dev, "segs"), segs.S, _dev(k_fresh, "k_fresh"),
+        _dev(v_fresh, "v_fresh"), None if cos is None else _dev(cos, "cos"),
+        None if sin is None else _dev(sin, "sin"), max_pos, ctypes.c_float(scale),
+        _dev(out, "out"), _stream(stream)))
+    return out
+
+
+def segments_with_window(segs, N: int, W: int) -> np.ndarray:
+    """rc_segments_with_window (host): the last W positions of every request
+    become fresh segments. Returns the new [B, S', 4] int32 table."""
+    h = np.ascontiguousarray(np.asarray(segs.cpu() if isinstance(segs, torch.Tensor) else segs,
+                                        dtype=np.int32))
+    B, S = h.shape[:2]
+    cap = S + 1
+    out = np.zeros((B * cap, 4), np.int32)
+    s_out = ctypes.c_int32(0)
+    check(_lib.load().rc_segments_with_window(h.ctypes.data_as(ctypes.c_void_p), B, S, int(N), int(W),
+                                              out.ctypes.data_as(ctypes.c_void_p), cap,
+                                              ctypes.byref(s_out)))
+    return out[:B * s_out.value].reshape(B, s_out.value, 4).copy()
 
 
 # ------------------------------------------------------------- the pipeline
@@ -340,6 +386,27 @@ def eq3_select(q, k_fresh, v_fresh, pools, segs: Segments, item_mask: int, lam: 
     select_tokens_eq3(segs, item_mask, lam, k_hist, k_item, k_fresh, v_fresh, bufs.k_asm,
                       bufs.v_asm, mass=bufs.mass, scores_out=bufs.scores, rows_out=bufs.rows,
                       patch=True, stream=stream)
+    return bufs
+
+
+def paged_prefill(q, k_fresh, v_fresh, pools, segs: Segments, k: int, cos, sin, scale=None,
+                  bufs: PrefillBuffers | None = None, stream=None):
+    """Zero-copy selective prefill of one layer: deviation scores of the
+    aligned pool keys without assembling -> top-k (no patch) -> attention
+    that reads K/V through the segment table. Same rows and output as
+    selective_prefill; bufs.k_asm / v_asm are not used."""
+    B, N, Hq, D = q.shape
+    Hkv = k_fresh.shape[2]
+    R = segs.n_fresh + int(k)
+    if bufs is None:
+        bufs = PrefillBuffers.alloc(B, N, Hq, Hkv, D, R, q.dtype, q.device)
+    kv_assemble(pools, segs, k_fresh, v_fresh, cos, sin, scores_out=bufs.scores, stream=stream,
+                score_only=True)
+    select_tokens(segs, k, k_fresh, v_fresh, None, None, scores_in=bufs.scores, rows_out=bufs.rows,
+                  patch=False, stream=stream)
+    if R > 0:
+        paged_attention(q, k_fresh, v_fresh, pools, segs, bufs.rows, cos, sin, scale, bufs.out,
+                        stream)
     return bufs
 
 

@@ -198,3 +198,42 @@ def test_select_eq3_validation(lib):
     assert call(rows=None) == -1
     assert call(scores_out=None) == -1
     assert call(shape=_shape(N=16385)) == -2
+
+
+def test_window_transform_matches_oracle(lib):
+    """The library's host-side window transform and the oracle's describe the
+    same per-position rows and rotations (their tables may split differently)."""
+    from paper_2605_07443_amd import inputs, ops
+    for name in ("miss-bf16", "ragged-bf16", "tiny-bf16"):
+        cfg = inputs.TEST_CONFIGS[name]
+        w = inputs.make(cfg, 9)
+        segs = w.segs.numpy()
+        for W in (0, 1, 3, 37, 64, cfg.N - 1, cfg.N):
+            got = ops.segments_with_window(segs, cfg.N, W)
+            want = O.segments_with_window(segs, cfg.N, W)
+            assert got.shape[1] <= segs.shape[1] + 1
+            for b in range(cfg.B):
+                assert O.position_map(got[b], cfg.N) == O.position_map(want[b], cfg.N), (name, W, b)
+    segs = np.array([[[0, 4, -1, 0], [4, 4, 0, 1]]], np.int32)
+    with pytest.raises(_lib.RcError):
+        ops.segments_with_window(segs, 8, 9)                 # W > N
+    with pytest.raises(_lib.RcError):
+        ops.segments_with_window(np.array([[[0, 4, -1, 0], [5, 3, 0, 1]]], np.int32), 8, 2)  # gap
+
+
+@no_gpu
+def test_paged_attention_validation(lib):
+    def call(shape=None, rows=FAKE, n=1, pools=None, S=3, cos=FAKE, sin=FAKE, max_pos=64):
+        return lib.rc_paged_attention(_shape() if shape is None else shape, FAKE, rows, 10,
+                                      _pools() if pools is None else pools, n, FAKE, S, FAKE, FAKE,
+                                      cos, sin, max_pos, ctypes.c_float(0.088), FAKE, None)
+
+    assert call(rows=None) == -1
+    assert call(n=0) == -1
+    assert call(S=0) == -1
+    assert call(S=65) == -2                           # paged tables live in LDS
+    assert call(cos=None) == -1
+    assert call(max_pos=10) == -1
+    assert call(shape=_shape(dtype=0)) == -2          # bf16 only
+    assert call(shape=_shape(N=16385)) == -2
+    assert call(pools=_pools(1, nb=0)) == -1

@@ -454,3 +454,49 @@ def test_config_sizes():
     assert [c[i].k for i in range(1, 6)] == [58, 442, 810, 600, 308]
     assert [c[i].R for i in range(1, 6)] == [90, 506, 874, 696, 340]
     assert [c[4].k_for(p) for p in inputs.SWEEP_PCTS] == [0, 200, 400, 600, 1000, 2000, 4000]
+
+
+# ---------------------------------------------------------------------------
+# Local sliding window (Sec. III-C.2b)
+# ---------------------------------------------------------------------------
+
+def test_window_makes_the_last_positions_fresh_and_keeps_the_rest():
+    cfg = inputs.TEST_CONFIGS["miss-bf16"]
+    w = inputs.make(cfg, 3)
+    segs = w.segs.numpy()
+    N = cfg.N
+    for W in (0, 1, 7, 40, 41, N - 1, N):
+        t = O.segments_with_window(segs, N, W)
+        assert t.shape[0] == cfg.B and t.shape[2] == 4
+        for b in range(cfg.B):
+            before, after = O.position_map(segs[b], N), O.position_map(t[b], N)
+            for i in range(N):   # brute force over positions
+                assert after[i] == (None if i >= N - W else before[i]), (W, b, i)
+
+
+def test_window_recomputes_the_window_rows_with_fresh_kv():
+    cfg = inputs.TEST_CONFIGS["tiny-bf16"]
+    w = inputs.make(cfg, 5)
+    W = 20
+    segs_w = O.segments_with_window(w.segs.numpy(), cfg.N, W)
+    F = int(O.fresh_count(segs_w)[0])
+    assert F == cfg.F + W
+    cos, sin = O.rope_table(cfg.N, cfg.D, cfg.rope_base)
+    pools = [(H(a), H(b)) for a, b in w.pools]
+    k = 10
+    r = O.selective_prefill(H(w.q), H(w.k_fresh), H(w.v_fresh), pools, segs_w, k, cos, sin)
+    for b in range(cfg.B):
+        assert set(range(cfg.N - W, cfg.N)) <= set(r["rows"][b].tolist())
+    np.testing.assert_array_equal(r["k_asm"][:, cfg.N - W:], H(w.k_fresh)[:, cfg.N - W:])
+    np.testing.assert_array_equal(r["v_asm"][:, cfg.N - W:], H(w.v_fresh)[:, cfg.N - W:])
+    # the window's rows see fresh K/V at their own and earlier window positions:
+    # with zero cache noise they equal the full prefill
+    w0 = inputs.make(cfg, 5, sigma=0.0)
+    r0 = O.selective_prefill(H(w0.q), H(w0.k_fresh), H(w0.v_fresh),
+                             [(H(a), H(b)) for a, b in w0.pools], segs_w, k, cos, sin)
+    full = O.attention(H(w0.q), H(w0.k_fresh), H(w0.v_fresh))
+    for b in range(cfg.B):
+        rows = r0["rows"][b]
+        sel = rows >= cfg.N - W
+        d = np.abs(O.as_f32(r0["out"][b][sel]) - O.as_f32(full[b][rows[sel]]))
+        assert d.max() <= 3e-2

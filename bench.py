@@ -50,6 +50,8 @@ def parse_args():
                     help="repeat the CPU oracle's sample until this much time has passed")
     ap.add_argument("--no-paged", action="store_true",
                     help="skip timing the zero-copy (paged attention) variant")
+    ap.add_argument("--no-host-pool", action="store_true",
+                    help="skip timing the token-granular gather from a pinned host pool")
     ap.add_argument("--no-eq3", action="store_true",
                     help="skip timing the selection by the full Eq. (3) score")
     ap.add_argument("--no-full-prefill", action="store_true",
@@ -342,6 +344,62 @@ def main():
                    "rc_select_tokens_eq3": dict(us=round(part[3] * 1e3, 2), **hbm(sel3_bytes, part[3]))}}
         del ebuf
 
+    # ---- token-granular history (single-token prototypes) with the prototype
+    # pool in pinned host memory: PCIe-inclusive gather, and the Eq. (3)
+    # selection with that gather overlapped with the first layer
+    host = None
+    if not args.no_host_pool and cfg.dtype == "bf16":
+        tw = inputs.make_prototypes(cfg, base + 7, device=dev, n_protos=65536)
+        tmap = tw.token_map.to(dev)
+        dev_pools = tw.w.pools
+        host_pools = [ops.pin_pool(dev_pools[0]), dev_pools[1]]
+        status = ops.prepare_segments(tw.status_segs, N, dev_pools, dev, check_blocks=False)
+        kh, ki = cfg.k_split(pct)
+        hb = ops.Eq3Buffers.alloc(B, N, Hq, Hkv, D, cfg.n_fresh + kh + ki, cfg.torch_dtype, dev)
+        ww = tw.w
+        side = torch.cuda.Stream()
+
+        def timeit(fn, reps):
+            fn()
+            torch.cuda.synchronize()
+            a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for _ in range(reps):
+                fn()
+            z.record(stream)
+            torch.cuda.synchronize()
+            return a.elapsed_time(z) / reps
+
+        def gather(pools_, wgs=0):
+            return lambda: ops.kv_gather_tokens(pools_, tmap, ww.k_fresh, ww.v_fresh, cos, sin,
+                                                hb.k_asm, hb.v_asm, hb.scores, max_workgroups=wgs)
+
+        def eq3_path(pools_, gs):
+            return lambda: ops.eq3_select_tokens_path(ww.q, ww.k_fresh, ww.v_fresh, pools_, tmap,
+                                                      status, inputs.ITEM_POOL_MASK, 0.5, kh, ki,
+                                                      cos, sin, bufs=hb, gather_stream=gs)
+
+        reps = max(3, min(10, args.steps // 10))
+        g_dev = timeit(gather(dev_pools), reps * 3)
+        g_host = timeit(gather(host_pools), reps * 3)
+        g_host32 = timeit(gather(host_pools, 32), reps * 3)
+        e_dev = timeit(eq3_path(dev_pools, None), reps)
+        e_seq = timeit(eq3_path(host_pools, None), reps)
+        e_ovl = timeit(eq3_path(host_pools, side), reps)
+        pcie_bytes = 2.0 * B * cfg.hist_len * row   # K and V rows of the history, from host memory
+        host = {"n_protos": 65536, "history_bytes_from_host": pcie_bytes,
+                "gather_device_pool_us": round(g_dev * 1e3, 2),
+                "gather_host_pool_us": round(g_host * 1e3, 2),
+                "gather_host_pool_32_workgroups_us": round(g_host32 * 1e3, 2),
+                "host_read_GBps": round(pcie_bytes / ((g_host - g_dev) * 1e-3) / 1e9, 1)
+                if g_host > g_dev else None,
+                "eq3_device_pool_ms": round(e_dev, 4),
+                "eq3_host_pool_sequential_ms": round(e_seq, 4),
+                "eq3_host_pool_overlapped_ms": round(e_ovl, 4),
+                "overlap_hidden_fraction": round((e_seq - e_ovl) / (e_seq - e_dev), 3)
+                if e_seq > e_dev else None}
+        del tw, ww, hb, host_pools, dev_pools, tmap
+
     # ---- CPU oracle on a bounded sample of the same workload
     cpu = None
     if args.cpu_requests is None or args.cpu_requests > 0:
@@ -394,6 +452,7 @@ def main():
         "full_prefill": full,
         "paged_prefill": paged,
         "eq3_selection": eq3,
+        "token_history_host_pool": host,
         "cpu_baseline": cpu,
         "wall_s_timed": round(wall, 3),
         "source_digest": digest,

@@ -29,6 +29,13 @@
  *                               (dropped for item blocks), separate history
  *                               and item budgets, and the correction (iii)
  *
+ * Token-granular history (single-token prototypes) and host-resident pools:
+ *
+ *   rc_kv_gather_tokens         gather + alignment through a per-position
+ *                               source map instead of segments; pool rows may
+ *                               live in pinned host memory (read over PCIe
+ *                               by the kernel, zero-copy)
+ *
  * Zero-copy variant and the local window:
  *
  *   rc_paged_attention          selective attention that reads K/V through
@@ -117,6 +124,19 @@ typedef struct {
   int32_t pool;
   int32_t block;
 } rc_segment;
+
+/* Source of one position for the token-granular gather: history prototypes
+ * are single tokens (Sec. III-B), so each cached position names its own pool
+ * row. pool < 0: fresh. Otherwise row indexes the pool's rows
+ * (num_blocks * block_len of them, [row, Hkv, D] contiguous) and the key is
+ * rotated by delta (the position it is placed at minus the position it was
+ * stored at; |delta| < max_pos). pad is ignored. */
+typedef struct {
+  int32_t pool;
+  int32_t row;
+  int32_t delta;
+  int32_t pad;
+} rc_token_src;
 
 /* RoPE tables (host). Writes cos/sin of pos * base^(-2j/D) for pos in
  * [0, max_pos), j in [0, D/2), evaluated in fp64 and rounded once to fp32,
@@ -266,6 +286,32 @@ int rc_select_tokens_eq3(const rc_shape* shape, const rc_segment* segs, int32_t 
                          int32_t k_item, const float* mass, const void* k_fresh,
                          const void* v_fresh, void* k_asm, void* v_asm, const float* scores_in,
                          float* scores_out, int32_t* rows, int32_t patch, hipStream_t stream);
+
+/* Token-granular assembly (Sec. III-B history prototypes are single tokens;
+ * Sec. III-C.3 (i) and (ii)). For request b and position i, m = map[b*N + i]:
+ *   m.pool < 0:  K_asm[b,i] = K_fresh[b,i], V_asm[b,i] = V_fresh[b,i]
+ *   otherwise:   K_asm[b,i] = R(m.delta) pool.k[row m.row], V_asm[b,i] = pool.v[row m.row]
+ * with R and its fp32 operation order as in rc_kv_assemble (negative deltas
+ * rotate by cos(|d|), -sin(|d|)); rope tables NULL: no rotation. Pool rows
+ * may be in device memory or in pinned host memory (hipHostMalloc), which
+ * the kernel reads directly over PCIe; run such a gather on its own stream
+ * to overlap the transfer with compute that does not need the pool (the
+ * first layer in full, Sec. III-C.3). scores_out (optional, [B, N] fp32):
+ * the K deviation of Eq. (3) as in rc_kv_assemble. map: device [B, N]
+ * rc_token_src. Entries naming a missing pool or a row out of range leave
+ * the position's output unspecified (not read out of bounds).
+ * max_workgroups: 0 = one workgroup per block of positions (fastest alone);
+ * > 0 = at most about that many workgroups (at least one per request), each
+ * looping over position blocks -- for a gather from host memory beside
+ * compute, so that it occupies few compute units while it waits on PCIe.
+ * Errors: INVALID_ARG for NULL pointers, bad shape or pools, aliasing
+ * outputs, one table without the other, max_workgroups < 0; UNSUPPORTED for
+ * D, dtype, a key row above 8192 bytes with scores_out. */
+int rc_kv_gather_tokens(const rc_shape* shape, const rc_pool* pools, int32_t n_pools,
+                        const rc_token_src* map, const void* k_fresh, const void* v_fresh,
+                        const float* rope_cos, const float* rope_sin, int32_t max_pos,
+                        void* k_asm, void* v_asm, float* scores_out, int32_t max_workgroups,
+                        hipStream_t stream);
 
 /* Zero-copy selective attention (the logical-to-physical block mapping of
  * Sec. III-A applied inside attention; Sec. III-C.2b, III-C.3 (i)-(iii) and

@@ -75,6 +75,8 @@ def lib():
                                        u32, f64, i32, i32, vp, vp, vp, vp, vp, f64, vp, vp, vp,
                                        vp, vp]
         L.rcref_eq3_select.restype = i32
+        L.rcref_gather_tokens.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp,
+                                          vp]
         L.rcref_num_threads.argtypes = []
         L.rcref_num_threads.restype = i32
         _lib = L
@@ -135,6 +137,25 @@ def assemble(k_fresh, v_fresh, pools, segs, cos=None, sin=None):
     sin = None if sin is None else _c(sin, np.float32)
     lib().rcref_assemble(B, N, Hkv, D, dt, pk_arr, pv_arr, _p(nb), _p(bl), n, _p(segs), S,
                          _p(k_fresh), _p(v_fresh), _p(cos), _p(sin), _p(k_asm), _p(v_asm))
+    return k_asm, v_asm
+
+
+def gather_tokens(k_fresh, v_fresh, pools, token_map, cos=None, sin=None):
+    """Token-granular gather: token_map [B, N, 4] int32 = {pool, row, delta, -};
+    pools as for ``assemble`` (rows counted across blocks)."""
+    k_fresh, v_fresh = _c(k_fresh), _c(v_fresh)
+    B, N, Hkv, D = k_fresh.shape
+    token_map = _c(token_map, np.int32)
+    pools = [(_c(pk), _c(pv)) for pk, pv in pools]
+    n = len(pools)
+    pk_arr = (ctypes.c_void_p * max(n, 1))(*[pk.ctypes.data for pk, _ in pools])
+    pv_arr = (ctypes.c_void_p * max(n, 1))(*[pv.ctypes.data for _, pv in pools])
+    k_asm = np.empty_like(k_fresh)
+    v_asm = np.empty_like(v_fresh)
+    cos = None if cos is None else _c(cos, np.float32)
+    sin = None if sin is None else _c(sin, np.float32)
+    lib().rcref_gather_tokens(B, N, Hkv, D, _dt(k_fresh), pk_arr, pv_arr, _p(token_map),
+                              _p(k_fresh), _p(v_fresh), _p(cos), _p(sin), _p(k_asm), _p(v_asm))
     return k_asm, v_asm
 
 

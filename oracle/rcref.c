@@ -192,6 +192,37 @@ void rcref_assemble(int B, int N, int Hkv, int D, int dt,
   }
 }
 
+/* Token-granular assembly (Sec. III-B: history prototypes are single tokens;
+ * Sec. III-C.3 steps i, ii). map[b, i] = {pool, row, delta, unused}: pool < 0
+ * takes the fresh rows; otherwise the K and V rows are row `row` of the pool
+ * (its rows counted across blocks), and the key is rotated by delta when
+ * tables are given. */
+void rcref_gather_tokens(int B, int N, int Hkv, int D, int dt,
+                         const void* const* pool_k, const void* const* pool_v,
+                         const int32_t* map, const void* k_fresh, const void* v_fresh,
+                         const float* cos_tab, const float* sin_tab, void* k_asm, void* v_asm) {
+  size_t row = (size_t)Hkv * D;
+  size_t es = el_size(dt);
+#pragma omp parallel for schedule(static)
+  for (long bi = 0; bi < (long)B * N; ++bi) {
+    const int32_t* m = map + (size_t)bi * 4;
+    size_t dst = (size_t)bi * row;
+    const char *src_k, *src_v;
+    if (m[0] < 0) {
+      src_k = (const char*)k_fresh + dst * es;
+      src_v = (const char*)v_fresh + dst * es;
+    } else {
+      src_k = (const char*)pool_k[m[0]] + (size_t)m[1] * row * es;
+      src_v = (const char*)pool_v[m[0]] + (size_t)m[1] * row * es;
+    }
+    memcpy((char*)k_asm + dst * es, src_k, row * es);
+    memcpy((char*)v_asm + dst * es, src_v, row * es);
+    if (m[0] >= 0 && m[2] != 0 && cos_tab && sin_tab)
+      for (int h = 0; h < Hkv; ++h)
+        rotate_head(k_asm, dt, dst + (size_t)h * D, D, m[2], cos_tab, sin_tab);
+  }
+}
+
 /* Standalone alignment: rotate K[b, i] by delta[b, i]; delta 0 leaves the row
  * untouched (Sec. III-C.3 step ii). */
 void rcref_rerope(int B, int N, int Hkv, int D, int dt, void* k, const int32_t* delta,

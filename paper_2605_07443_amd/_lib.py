@@ -22,6 +22,7 @@ RC_F32, RC_BF16 = 0, 1
 EXPORTS = ("rc_rope_table", "rc_kv_assemble", "rc_rerope", "rc_select_tokens",
            "rc_selective_attention", "rc_selective_attention_lse", "rc_attention_mass",
            "rc_select_tokens_eq3", "rc_paged_attention", "rc_segments_with_window",
+           "rc_kv_gather_tokens",
            "rc_status_string", "rc_last_error")
 
 
@@ -68,9 +69,12 @@ def load() -> ctypes.CDLL:
     L.rc_paged_attention.argtypes = [P(RcShape), vp, vp, i32, P(RcPool), i32, vp, i32, vp, vp, vp,
                                      vp, i32, f32, vp, vp]
     L.rc_segments_with_window.argtypes = [vp, i32, i32, i32, i32, vp, i32, P(i32)]
+    L.rc_kv_gather_tokens.argtypes = [P(RcShape), P(RcPool), i32, vp, vp, vp, vp, vp, i32, vp, vp,
+                                      vp, i32, vp]
     for name in ("rc_rope_table", "rc_kv_assemble", "rc_rerope", "rc_select_tokens",
                  "rc_selective_attention", "rc_selective_attention_lse", "rc_attention_mass",
-                 "rc_select_tokens_eq3", "rc_paged_attention", "rc_segments_with_window"):
+                 "rc_select_tokens_eq3", "rc_paged_attention", "rc_segments_with_window",
+                 "rc_kv_gather_tokens"):
         getattr(L, name).restype = ctypes.c_int
     L.rc_status_string.argtypes = [ctypes.c_int]
     L.rc_status_string.restype = ctypes.c_char_p

@@ -32,16 +32,19 @@ constexpr int kRowBytesPerWg = kKItems * 32;  // key-row bytes of a workgroup (8
 // produced (0 at fresh positions, whose assembled row is the fresh row).
 // WRITE = false (with ASSEMBLE and SCORE): score only -- the aligned key rows
 // are formed in registers and compared, nothing is stored and V is not read.
+// MAP (with ASSEMBLE): sources come from a per-position map {pool, row,
+// delta, -} instead of the segment table (single-token prototypes).
 // Every load of a workgroup's 16-byte units is issued before the first use.
-template <int ES, bool ASSEMBLE, bool SCORE, bool WRITE = true>
+template <int ES, bool ASSEMBLE, bool SCORE, bool WRITE = true, bool MAP = false>
 __global__ __launch_bounds__(kThreads) void kv_rows_kernel(
     PoolArgs pools, const int4* __restrict__ segs, int S, int N, int tok_per_wg, int row_units,
     int head_units, const char* __restrict__ k_fresh, const char* __restrict__ v_fresh,
-    const int32_t* __restrict__ delta_arr, const float* __restrict__ cos_t,
+    const int32_t* __restrict__ delta_arr, const int4* __restrict__ map,
+    const float* __restrict__ cos_t,
     const float* __restrict__ sin_t, int max_pos, int half, char* __restrict__ k_out,
     char* __restrict__ v_out, float* __restrict__ scores) {
   constexpr int E = 16 / ES;  // elements per 16-byte unit
-  __shared__ int4 s_segs[ASSEMBLE ? kMaxSegments : 1];
+  __shared__ int4 s_segs[(ASSEMBLE && !MAP) ? kMaxSegments : 1];
   __shared__ const char* s_srck[kMaxTok];
   __shared__ const char* s_srcv[kMaxTok];
   __shared__ int s_delta[kMaxTok];
@@ -49,22 +52,38 @@ __global__ __launch_bounds__(kThreads) void kv_rows_kernel(
   __shared__ float s_part[SCORE ? kKItems : 1];
 
   const int b = blockIdx.y;
-  const int i0 = blockIdx.x * tok_per_wg;
-  const int tok_cnt = min(tok_per_wg, N - i0);
   const size_t row_bytes = static_cast<size_t>(row_units) * 16;
   const int tid = threadIdx.x;
 
-  if constexpr (ASSEMBLE) {
+  if constexpr (ASSEMBLE && !MAP) {
     for (int s = tid; s < S; s += kThreads) s_segs[s] = segs[static_cast<size_t>(b) * S + s];
     __syncthreads();
   }
+  // token blocks of this request; a bounded grid loops over them
+  const int n_blk = (N + tok_per_wg - 1) / tok_per_wg;
+  for (int blk = blockIdx.x; blk < n_blk; blk += gridDim.x) {
+  const int i0 = blk * tok_per_wg;
+  const int tok_cnt = min(tok_per_wg, N - i0);
   for (int t = tid; t < tok_cnt; t += kThreads) {
     const int i = i0 + t;
     const size_t row_off = (static_cast<size_t>(b) * N + i) * row_bytes;
     const char* sk = nullptr;
     const char* sv = nullptr;
     int d = 0, cached = 0;
-    if constexpr (ASSEMBLE) {
+    if constexpr (ASSEMBLE && MAP) {
+      const int4 m = map[static_cast<size_t>(b) * N + i];  // {pool, row, delta, -}
+      if (m.x < 0) {
+        sk = k_fresh + row_off;
+        sv = v_fresh + row_off;
+      } else if (m.x < pools.n && m.y >= 0 &&
+                 m.y < static_cast<int64_t>(pools.num_blocks[m.x]) * pools.block_len[m.x]) {
+        const size_t src = static_cast<size_t>(m.y) * row_bytes;
+        sk = pools.k[m.x] + src;
+        sv = pools.v[m.x] + src;
+        cached = 1;
+        if (cos_t != nullptr && m.z < max_pos && -m.z < max_pos) d = m.z;
+      }
+    } else if constexpr (ASSEMBLE) {
       const int s = find_segment(s_segs, S, i);
       if (s >= 0) {
         const int4 g = s_segs[s];
@@ -200,6 +219,8 @@ __global__ __launch_bounds__(kThreads) void kv_rows_kernel(
       if (lane == 0) scores[static_cast<size_t>(b) * N + i0 + t] = x;
     }
   }
+  __syncthreads();  // the next block reuses the workgroup's LDS
+  }
 }
 
 int tokens_per_wg(int row_bytes) {
@@ -207,11 +228,11 @@ int tokens_per_wg(int row_bytes) {
   return t < 1 ? 1 : (t > kMaxTok ? kMaxTok : t);
 }
 
-template <bool ASSEMBLE>
+template <bool ASSEMBLE, bool MAP = false>
 int launch_rows(const rc_shape* s, const PoolArgs& pools, const int4* segs, int S,
                 const void* k_fresh, const void* v_fresh, const int32_t* delta, const float* cos_t,
                 const float* sin_t, int max_pos, void* k_out, void* v_out, float* scores,
-                hipStream_t stream) {
+                hipStream_t stream, const int4* map = nullptr, int max_wgs = 0) {
   const int es = elem_size(s->dtype);
   const int row_bytes = s->Hkv * s->D * es;
   const int row_units = row_bytes / 16;
@@ -220,16 +241,28 @@ int launch_rows(const rc_shape* s, const PoolArgs& pools, const int4* segs, int 
   if (scores && tok * (row_units / 2) > kKItems)
     return fail(RC_ERR_UNSUPPORTED, "scoring needs a key row of at most %d bytes", kRowBytesPerWg);
   dim3 grid((s->N + tok - 1) / tok, s->B);
+  if (max_wgs > 0) {  // bounded grid: each workgroup loops over token blocks
+    const int gx = max(1, max_wgs / s->B);
+    grid.x = min(grid.x, static_cast<unsigned>(gx));
+  }
   if (grid.y > 65535) return fail(RC_ERR_UNSUPPORTED, "B=%d exceeds 65535", s->B);
   auto args = [&](auto kern) {
     hipLaunchKernelGGL(kern, grid, dim3(kThreads), 0, stream, pools, segs, S, s->N, tok, row_units,
                        head_units, static_cast<const char*>(k_fresh),
-                       static_cast<const char*>(v_fresh), delta, cos_t, sin_t, max_pos, s->D / 2,
+                       static_cast<const char*>(v_fresh), delta, map, cos_t, sin_t, max_pos, s->D / 2,
                        static_cast<char*>(k_out), static_cast<char*>(v_out), scores);
   };
   if (!ASSEMBLE) {
     if (s->dtype == RC_BF16) args(kv_rows_kernel<2, false, false>);
     else args(kv_rows_kernel<4, false, false>);
+  } else if (MAP) {
+    if (scores) {
+      if (s->dtype == RC_BF16) args(kv_rows_kernel<2, true, true, true, true>);
+      else args(kv_rows_kernel<4, true, true, true, true>);
+    } else {
+      if (s->dtype == RC_BF16) args(kv_rows_kernel<2, true, false, true, true>);
+      else args(kv_rows_kernel<4, true, false, true, true>);
+    }
   } else if (scores && !k_out) {
     if (s->dtype == RC_BF16) args(kv_rows_kernel<2, true, true, false>);
     else args(kv_rows_kernel<4, true, true, false>);
@@ -240,7 +273,7 @@ int launch_rows(const rc_shape* s, const PoolArgs& pools, const int4* segs, int 
     if (s->dtype == RC_BF16) args(kv_rows_kernel<2, true, false>);
     else args(kv_rows_kernel<4, true, false>);
   }
-  return check_launch(ASSEMBLE ? "rc_kv_assemble" : "rc_rerope");
+  return check_launch(MAP ? "rc_kv_gather_tokens" : ASSEMBLE ? "rc_kv_assemble" : "rc_rerope");
 }
 
 }  // namespace
@@ -299,4 +332,39 @@ extern "C" int rc_rerope(const rc_shape* shape, void* k, const int32_t* delta,
   PoolArgs pa{};
   return launch_rows<false>(shape, pa, nullptr, 0, nullptr, nullptr, delta, rope_cos, rope_sin,
                             max_pos, k, nullptr, nullptr, stream);
+}
+
+extern "C" int rc_kv_gather_tokens(const rc_shape* shape, const rc_pool* pools, int32_t n_pools,
+                                   const rc_token_src* map, const void* k_fresh,
+                                   const void* v_fresh, const float* rope_cos,
+                                   const float* rope_sin, int32_t max_pos, void* k_asm,
+                                   void* v_asm, float* scores_out, int32_t max_workgroups,
+                                   hipStream_t stream) {
+  using namespace rc;
+  clear_error();
+  if (int st = check_shape(shape, false)) return st;
+  if (n_pools < 1 || n_pools > kMaxPools)
+    return fail(n_pools > kMaxPools ? RC_ERR_UNSUPPORTED : RC_ERR_INVALID_ARG,
+                "n_pools=%d (1..%d)", n_pools, kMaxPools);
+  if (!pools || !map || !k_fresh || !v_fresh || !k_asm || !v_asm)
+    return fail(RC_ERR_INVALID_ARG, "pools, map, k_fresh, v_fresh, k_asm and v_asm must be non-NULL");
+  if ((rope_cos == nullptr) != (rope_sin == nullptr))
+    return fail(RC_ERR_INVALID_ARG, "rope_cos and rope_sin must both be given or both be NULL");
+  if (rope_cos && max_pos < 1) return fail(RC_ERR_INVALID_ARG, "max_pos=%d must be >= 1", max_pos);
+  if (k_asm == k_fresh || v_asm == v_fresh || k_asm == v_asm)
+    return fail(RC_ERR_INVALID_ARG, "outputs alias inputs");
+  if (max_workgroups < 0) return fail(RC_ERR_INVALID_ARG, "max_workgroups=%d must be >= 0", max_workgroups);
+  PoolArgs pa{};
+  pa.n = n_pools;
+  for (int p = 0; p < n_pools; ++p) {
+    if (!pools[p].k || !pools[p].v || pools[p].num_blocks < 1 || pools[p].block_len < 1)
+      return fail(RC_ERR_INVALID_ARG, "pool %d: NULL tensor or empty shape", p);
+    pa.k[p] = static_cast<const char*>(pools[p].k);
+    pa.v[p] = static_cast<const char*>(pools[p].v);
+    pa.num_blocks[p] = pools[p].num_blocks;
+    pa.block_len[p] = pools[p].block_len;
+  }
+  return launch_rows<true, true>(shape, pa, nullptr, 0, k_fresh, v_fresh, nullptr, rope_cos,
+                                 rope_sin, rope_cos ? max_pos : 0, k_asm, v_asm, scores_out, stream,
+                                 reinterpret_cast<const int4*>(map), max_workgroups);
 }

@@ -381,3 +381,81 @@ def referenced_subpools(w: Workload):
 
 def scale_for(D: int) -> float:
     return 1.0 / math.sqrt(D)
+
+
+@dataclass
+class TokenWorkload:
+    """A batch whose history is token-granular: every history position reuses
+    one single-token prototype row (Sec. III-B builds history prototypes per
+    token), items stay blocks. pools[0] holds the prototypes ([n_protos, 1,
+    Hkv, D]), pools[1] the item blocks."""
+    w: Workload
+    token_map: torch.Tensor     # [B, N, 4] int32 (host): {pool, row, delta, 0}
+    status_segs: torch.Tensor   # [B, S, 4] int32 (host): fresh / cached runs for selection
+    proto_ids: torch.Tensor     # [B, hist_len] int64 (host)
+
+
+def make_prototypes(cfg: Config, seed: int, device="cpu", n_protos: int = 4096,
+                    sigma: float | None = None) -> TokenWorkload:
+    """Workload `cfg` with a prototype history: each history position draws a
+    prototype id uniformly; the prototype row is stored at position 0
+    (pool K = raw + eps, pool V = v + eta) and the position's fresh K/V are
+    the model's rows of the clean prototype at that position."""
+    sigma = cfg.sigma if sigma is None else float(sigma)
+    w = make(cfg, seed, device=device, sigma=sigma)
+    dt = cfg.torch_dtype
+    B, N, Hkv, D = cfg.B, cfg.N, cfg.Hkv, cfg.D
+    g = _gen(device, seed, 7)
+    shp = (n_protos, 1, Hkv, D)
+    raw = torch.randn(shp, generator=g, device=device, dtype=torch.float32)
+    val = torch.randn(shp, generator=g, device=device, dtype=torch.float32)
+    eps = torch.randn(shp, generator=g, device=device, dtype=torch.float32)
+    eta = torch.randn(shp, generator=g, device=device, dtype=torch.float32)
+    proto_k = (raw.to(torch.float64) + sigma * eps.to(torch.float64)).to(dt)  # position 0: no rotation
+    proto_v = (val.to(torch.float64) + sigma * eta.to(torch.float64)).to(dt)
+    gi = _gen("cpu", seed, 8)
+    ids = torch.randint(0, n_protos, (B, cfg.hist_len), generator=gi)
+    h0, h1 = cfg.F, cfg.F + cfg.hist_len
+    pos = torch.arange(h0, h1, device=device)
+    for b in range(B):
+        idx = ids[b].to(device)
+        r = raw[idx, 0].to(torch.float64)                      # [hist_len, Hkv, D]
+        w.k_fresh[b, h0:h1] = _rope_model(r, pos, cfg.rope_base).to(dt)
+        w.v_fresh[b, h0:h1] = val[idx, 0].to(dt)
+    tmap = torch.zeros((B, N, 4), dtype=torch.int32)
+    tmap[..., 0] = -1
+    segs = w.segs
+    for b in range(B):
+        for s in range(segs.shape[1]):
+            dst, ln, p, blk = (int(x) for x in segs[b, s])
+            if p == 0:
+                tmap[b, dst:dst + ln, 0] = 0
+                tmap[b, dst:dst + ln, 1] = ids[b, :ln].to(torch.int32)
+                tmap[b, dst:dst + ln, 2] = torch.arange(dst, dst + ln, dtype=torch.int32)
+            elif p > 0:
+                tmap[b, dst:dst + ln, 0] = p
+                tmap[b, dst:dst + ln, 1] = blk * cfg.item_len + torch.arange(ln, dtype=torch.int32)
+                tmap[b, dst:dst + ln, 2] = dst
+    status = segs.clone()
+    status[..., 3] = torch.where(status[..., 2] == 0, torch.zeros_like(status[..., 3]), status[..., 3])
+    w.pools = [(proto_k, proto_v), w.pools[1]]
+    w.segs = status
+    return TokenWorkload(w=w, token_map=tmap, status_segs=status, proto_ids=ids)
+
+
+def token_map_from_segments(segs, block_lens) -> torch.Tensor:
+    """The per-position map equivalent to a segment table: row = block *
+    block_len + offset, delta = dst_start."""
+    segs = torch.as_tensor(segs)
+    B, S = segs.shape[:2]
+    N = int(segs[0, :, 1].sum())
+    tmap = torch.zeros((B, N, 4), dtype=torch.int32)
+    tmap[..., 0] = -1
+    for b in range(B):
+        for s in range(S):
+            dst, ln, p, blk = (int(x) for x in segs[b, s])
+            if p >= 0:
+                tmap[b, dst:dst + ln, 0] = p
+                tmap[b, dst:dst + ln, 1] = blk * int(block_lens[p]) + torch.arange(ln, dtype=torch.int32)
+                tmap[b, dst:dst + ln, 2] = dst
+    return tmap

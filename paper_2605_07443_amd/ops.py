@@ -36,6 +36,15 @@ def _dev(t: torch.Tensor, name: str) -> int:
     return t.data_ptr()
 
 
+def _pool_ptr(t: torch.Tensor, name: str) -> int:
+    """Device tensors, or pinned host tensors (read by the kernels over PCIe)."""
+    if isinstance(t, torch.Tensor) and not t.is_cuda and t.is_pinned():
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+        return t.data_ptr()
+    return _dev(t, name)
+
+
 def _stream(stream=None) -> ctypes.c_void_p:
     s = torch.cuda.current_stream() if stream is None else stream
     return ctypes.c_void_p(s.cuda_stream)
@@ -64,9 +73,11 @@ class Segments:
         return self.N - self.n_fresh
 
 
-def prepare_segments(segs, N: int, pools, device) -> Segments:
+def prepare_segments(segs, N: int, pools, device, check_blocks: bool = True) -> Segments:
     """Check on the host that every request's segments tile [0, N) in order,
-    name existing pools and blocks and share one fresh count, then upload."""
+    name existing pools and blocks and share one fresh count, then upload.
+    check_blocks=False: a status table (fresh / cached-from-pool runs) that
+    only the selection reads, e.g. for a token-granular gather."""
     h = np.ascontiguousarray(np.asarray(segs.cpu() if isinstance(segs, torch.Tensor) else segs,
                                         dtype=np.int32))
     if h.ndim != 3 or h.shape[2] != 4 or h.shape[1] < 1:
@@ -81,7 +92,7 @@ def prepare_segments(segs, N: int, pools, device) -> Segments:
                 if p >= len(pools):
                     raise ValueError(f"request {b}: pool {p} does not exist")
                 pk = pools[p][0]
-                if not (0 <= blk < pk.shape[0]) or ln > pk.shape[1]:
+                if check_blocks and (not (0 <= blk < pk.shape[0]) or ln > pk.shape[1]):
                     raise ValueError(f"request {b}: block {blk}/len {ln} outside pool {p}")
             else:
                 fresh += ln
@@ -117,7 +128,7 @@ def _pool_array(pools, dtype, Hkv, D):
             raise TypeError("pool dtype differs from the fresh tensors")
         if pk.shape != pv.shape or pk.dim() != 4 or pk.shape[2] != Hkv or pk.shape[3] != D:
             raise ValueError("pool K/V must be [num_blocks, block_len, Hkv, D]")
-        arr[i] = RcPool(_dev(pk, "pool k"), _dev(pv, "pool v"), pk.shape[0], pk.shape[1])
+        arr[i] = RcPool(_pool_ptr(pk, "pool k"), _pool_ptr(pv, "pool v"), pk.shape[0], pk.shape[1])
     return arr
 
 
@@ -147,6 +158,34 @@ def kv_assemble(pools, segs: Segments, k_fresh, v_fresh, cos=None, sin=None, k_o
         None if score_only else _dev(v_out, "v_out"),
         None if scores_out is None else _dev(scores_out, "scores_out"), _stream(stream)))
     return (None, None) if score_only else (k_out, v_out)
+
+
+def kv_gather_tokens(pools, token_map, k_fresh, v_fresh, cos=None, sin=None, k_out=None,
+                     v_out=None, scores_out=None, stream=None, max_workgroups=0):
+    """rc_kv_gather_tokens: per-position map gather + alignment (+ deviation
+    scores). token_map: device int32 [B, N, 4]. Pools may be pinned host
+    tensors. Returns (k_asm, v_asm)."""
+    B, N, Hkv, D = k_fresh.shape
+    if tuple(token_map.shape) != (B, N, 4) or token_map.dtype != torch.int32:
+        raise ValueError("token_map must be int32 [B, N, 4]")
+    k_out = torch.empty_like(k_fresh) if k_out is None else k_out
+    v_out = torch.empty_like(v_fresh) if v_out is None else v_out
+    parr = _pool_array(pools, k_fresh.dtype, Hkv, D)
+    max_pos = 0 if cos is None else int(cos.shape[0])
+    check(_lib.load().rc_kv_gather_tokens(
+        ctypes.byref(_shape(B, N, 1, Hkv, D, _dtype_code(k_fresh))), parr, len(pools),
+        _dev(token_map, "token_map"), _dev(k_fresh, "k_fresh"), _dev(v_fresh, "v_fresh"),
+        None if cos is None else _dev(cos, "cos"), None if sin is None else _dev(sin, "sin"),
+        max_pos, _dev(k_out, "k_out"), _dev(v_out, "v_out"),
+        None if scores_out is None else _dev(scores_out, "scores_out"), int(max_workgroups),
+        _stream(stream)))
+    return k_out, v_out
+
+
+def pin_pool(pool):
+    """Pinned host copy of a (pool_k, pool_v) pair: the pool then stays in host
+    memory and the gather reads it over PCIe."""
+    return tuple(t.detach().cpu().contiguous().pin_memory() for t in pool)
 
 
 def rerope(k, delta, cos, sin, stream=None):
@@ -407,6 +446,42 @@ def paged_prefill(q, k_fresh, v_fresh, pools, segs: Segments, k: int, cos, sin, 
     if R > 0:
         paged_attention(q, k_fresh, v_fresh, pools, segs, bufs.rows, cos, sin, scale, bufs.out,
                         stream)
+    return bufs
+
+
+def eq3_select_tokens_path(q, k_fresh, v_fresh, pools, token_map, status: Segments, item_mask: int,
+                           lam: float, k_hist: int, k_item: int, cos, sin, scale=None,
+                           bufs: Eq3Buffers | None = None, gather_stream=None,
+                           gather_workgroups: int = 32):
+    """Eq. (3) selection with token-granular sources (pool rows possibly in
+    pinned host memory). With gather_stream, the gather runs there, overlapping
+    the first layer in full (attention with log-sum-exp, attention mass) on the
+    current stream, which needs no pool row (Sec. III-C.3 hides the transfer of
+    cached KV under the first layer); the score then waits for the gather.
+    Without it everything runs in order on the current stream. The
+    overlapped gather runs on about gather_workgroups workgroups, so that it
+    leaves the compute units to the first layer while it waits on PCIe."""
+    B, N, Hq, D = q.shape
+    Hkv = k_fresh.shape[2]
+    R = status.n_fresh + int(k_hist) + int(k_item)
+    if bufs is None:
+        bufs = Eq3Buffers.alloc(B, N, Hq, Hkv, D, R, q.dtype, q.device)
+    main = torch.cuda.current_stream()
+    if gather_stream is None:
+        kv_gather_tokens(pools, token_map, k_fresh, v_fresh, cos, sin, bufs.k_asm, bufs.v_asm)
+    else:
+        gather_stream.wait_stream(main)   # inputs written on the current stream
+        kv_gather_tokens(pools, token_map, k_fresh, v_fresh, cos, sin, bufs.k_asm, bufs.v_asm,
+                         stream=gather_stream, max_workgroups=gather_workgroups)
+        done = torch.cuda.Event()
+        done.record(gather_stream)
+    selective_attention_lse(q, k_fresh, v_fresh, None, scale, bufs.out_full, bufs.lse)
+    attention_mass(q, k_fresh, bufs.lse, scale, bufs.mass)
+    if gather_stream is not None:
+        main.wait_event(done)
+    select_tokens_eq3(status, item_mask, lam, k_hist, k_item, k_fresh, v_fresh, bufs.k_asm,
+                      bufs.v_asm, mass=bufs.mass, scores_out=bufs.scores, rows_out=bufs.rows,
+                      patch=True)
     return bufs
 
 

@@ -500,3 +500,56 @@ def test_window_recomputes_the_window_rows_with_fresh_kv():
         sel = rows >= cfg.N - W
         d = np.abs(O.as_f32(r0["out"][b][sel]) - O.as_f32(full[b][rows[sel]]))
         assert d.max() <= 3e-2
+
+
+# ---------------------------------------------------------------------------
+# Token-granular gather (history prototypes are single tokens, Sec. III-B)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", ["tiny-bf16", "miss-bf16", "tiny-f32-gqa"])
+def test_token_gather_equals_segment_gather(name):
+    """The per-position map derived from a segment table reproduces the
+    (separately pinned) segment gather bit for bit, rotation included."""
+    cfg = inputs.TEST_CONFIGS[name]
+    w = inputs.make(cfg, 12)
+    cos, sin = O.rope_table(cfg.N, cfg.D, cfg.rope_base)
+    pools = [(H(a), H(b)) for a, b in w.pools]
+    tmap = inputs.token_map_from_segments(w.segs, [cfg.hist_len, cfg.item_len]).numpy()
+    ka, va = O.assemble(H(w.k_fresh), H(w.v_fresh), pools, w.segs.numpy(), cos, sin)
+    kt, vt = O.gather_tokens(H(w.k_fresh), H(w.v_fresh), pools, tmap, cos, sin)
+    np.testing.assert_array_equal(kt, ka)
+    np.testing.assert_array_equal(vt, va)
+
+
+def test_token_gather_names_rows_and_rotates_by_delta():
+    cfg = inputs.TEST_CONFIGS["tiny-bf16"]
+    tw = inputs.make_prototypes(cfg, 4, n_protos=50, sigma=0.0)
+    w = tw.w
+    pools = [(H(a), H(b)) for a, b in w.pools]
+    tmap = tw.token_map.numpy()
+    # no tables: the bytes of the named rows
+    kt, vt = O.gather_tokens(H(w.k_fresh), H(w.v_fresh), pools, tmap)
+    for b in range(cfg.B):
+        for i in range(cfg.N):
+            p, r = tmap[b, i, :2]
+            if p < 0:
+                assert np.array_equal(kt[b, i], H(w.k_fresh)[b, i])
+            else:
+                assert np.array_equal(kt[b, i], pools[p][0].reshape(-1, cfg.Hkv, cfg.D)[r])
+                assert np.array_equal(vt[b, i], pools[p][1].reshape(-1, cfg.Hkv, cfg.D)[r])
+    # zero noise: rotating each prototype by its position gives the model's key
+    cos, sin = O.rope_table(cfg.N, cfg.D, cfg.rope_base)
+    kr, vr = O.gather_tokens(H(w.k_fresh), H(w.v_fresh), pools, tmap, cos, sin)
+    # (two bf16 roundings on the cached side, one on the fresh side: <= 2 ulps)
+    np.testing.assert_allclose(O.as_f32(kr), O.as_f32(H(w.k_fresh)), rtol=2 ** -7, atol=1e-2)
+    np.testing.assert_array_equal(vr, H(w.v_fresh))
+    # a row placed at delta and moved back by -delta returns to itself (to rounding)
+    back = tmap.copy()
+    back[..., 2] = -back[..., 2]
+    ctab, stab = O.rope_table(cfg.N, cfg.D, cfg.rope_base)
+    kb, _ = O.gather_tokens(kr, vr, [(kr.reshape(-1, 1, cfg.Hkv, cfg.D), vr.reshape(-1, 1, cfg.Hkv, cfg.D))],
+                            np.stack([np.where(back[..., 0] >= 0, 0, -1),
+                                      np.arange(cfg.B * cfg.N).reshape(cfg.B, cfg.N),
+                                      back[..., 2], back[..., 3]], -1).astype(np.int32), ctab, stab)
+    hist = slice(cfg.F, cfg.F + cfg.hist_len)
+    np.testing.assert_allclose(O.as_f32(kb[:, hist]), O.as_f32(kt[:, hist]), rtol=2 ** -7, atol=1e-2)

@@ -52,6 +52,8 @@ def parse_args():
                     help="skip timing the zero-copy (paged attention) variant")
     ap.add_argument("--no-host-pool", action="store_true",
                     help="skip timing the token-granular gather from a pinned host pool")
+    ap.add_argument("--stack-layers", type=int, default=4,
+                    help="layers of the multi-layer leg (0 skips it)")
     ap.add_argument("--no-eq3", action="store_true",
                     help="skip timing the selection by the full Eq. (3) score")
     ap.add_argument("--no-full-prefill", action="store_true",
@@ -400,6 +402,48 @@ def main():
                 if e_seq > e_dev else None}
         del tw, ww, hb, host_pools, dev_pools, tmap
 
+    # ---- several layers (Llama-3-8B layer dimensions, random weights): the
+    # first layer for every row picks the rows, later layers recompute only
+    # them; against the full recompute of every row of every layer
+    stack = None
+    if args.stack_layers > 0 and cfg.dtype == "bf16":
+        Hd, I, nl = 4096, 14336, args.stack_layers
+        sx, slayers, spools, ssegs = inputs.make_stack(cfg, base + 11, nl, Hd, I, device=dev)
+        W = 16
+        sseg = ops.prepare_segments(ops.segments_with_window(ssegs.numpy(), N, W), N, spools[0], dev)
+        sk = (sseg.n_reused * pct + 99) // 100
+        scos, ssin = cos, sin
+
+        def run_sel():
+            return ops.stack_prefill(sx, slayers, spools, sseg, sk, scos, ssin)
+
+        def run_full():
+            return ops.stack_full(sx, slayers, Hq, Hkv, D, scos, ssin)
+
+        def timeit2(fn, reps):
+            fn()
+            torch.cuda.synchronize()
+            a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for _ in range(reps):
+                fn()
+            z.record(stream)
+            torch.cuda.synchronize()
+            return a.elapsed_time(z) / reps
+
+        reps = max(2, min(5, args.steps // 20))
+        t_sel = timeit2(run_sel, reps)
+        t_full = timeit2(run_full, reps)
+        R2 = sseg.n_fresh + sk
+        per_row = 2.0 * Hd * ((Hq + 2 * Hkv) * D + Hq * D + 3 * I)      # projection FLOPs of one row
+        sel_flops = B * N * 2.0 * Hd * (Hq + 2 * Hkv) * D + (B * R2) * (per_row - 2.0 * Hd * (Hq + 2 * Hkv) * D) \
+            + (nl - 1) * B * R2 * per_row
+        stack = {"layers": nl, "hidden": Hd, "intermediate": I, "window": W,
+                 "rows_per_request": R2, "selective_ms": round(t_sel, 3), "full_ms": round(t_full, 3),
+                 "speedup": round(t_full / t_sel, 2),
+                 "selective_projection_tflops": round(sel_flops / (t_sel * 1e-3) / 1e12, 1)}
+        del sx, slayers, spools
+
     # ---- CPU oracle on a bounded sample of the same workload
     cpu = None
     if args.cpu_requests is None or args.cpu_requests > 0:
@@ -453,6 +497,7 @@ def main():
         "paged_prefill": paged,
         "eq3_selection": eq3,
         "token_history_host_pool": host,
+        "layer_stack": stack,
         "cpu_baseline": cpu,
         "wall_s_timed": round(wall, 3),
         "source_digest": digest,

@@ -29,6 +29,18 @@
  *                               (dropped for item blocks), separate history
  *                               and item budgets, and the correction (iii)
  *
+ * Several layers (the first computed in full, later ones recomputing only the
+ * selected rows, Sec. III-C.2b), with random-weight decoder layers:
+ *
+ *   rc_gemm_bf16                Y = X W^T (+ residual) projections
+ *   rc_rmsnorm                  RMSNorm of rows
+ *   rc_qkv_rope                 split a QKV projection, rotate q and k to
+ *                               their positions, write q/k/v at those
+ *                               positions (the heavy-hitter update of a
+ *                               cached layer)
+ *   rc_silu_mul                 SwiGLU activation
+ *   rc_gather_rows              rows of a [B, N, width] tensor by position
+ *
  * Token-granular history (single-token prototypes) and host-resident pools:
  *
  *   rc_kv_gather_tokens         gather + alignment through a per-position
@@ -348,6 +360,50 @@ int rc_paged_attention(const rc_shape* shape, const void* q, const int32_t* rows
  * window shorter than the pieces it needs, S_cap < S_out. */
 int rc_segments_with_window(const rc_segment* segs_in, int32_t B, int32_t S, int32_t N,
                             int32_t W, rc_segment* segs_out, int32_t S_cap, int32_t* S_out);
+
+/* Projection of a decoder layer on the matrix cores:
+ *   y[m, j] = sum_i x[m, i] w[j, i] (+ residual[m, j]),  m < M, j < n, i < k
+ * x: [M, k], w: [n, k], residual (optional) and y: [M, n]; all bf16 row-major
+ * device tensors; fp32 accumulation, one rounding to bf16 (after adding the
+ * residual in fp32). Deterministic.
+ * Errors: INVALID_ARG for NULL pointers, M < 0, n < 1, k not a positive
+ * multiple of 8, residual == y. */
+int rc_gemm_bf16(int64_t M, int32_t n, int32_t k, const void* x, const void* w,
+                 const void* residual, void* y, hipStream_t stream);
+
+/* RMSNorm of M rows of width H (bf16 device tensors x, y [M, H], gamma [H]):
+ *   y = x / sqrt(mean(x^2) + eps) * gamma   (fp32 statistics, RNE to bf16).
+ * Errors: INVALID_ARG for NULL pointers, H not a positive multiple of 8,
+ * eps negative or not finite; UNSUPPORTED for H > 8192. */
+int rc_rmsnorm(int32_t M, int32_t H, const void* x, const void* gamma, float eps, void* y,
+               hipStream_t stream);
+
+/* Split projected rows into q, k, v and place them at their positions
+ * (Sec. III-C.2b: a later layer recomputes the selected rows; their fresh
+ * K/V replace the cached rows, Sec. III-C.3 (iii)). Row m = b*R + r of qkv
+ * ([B*R, (Hq + 2 Hkv) D] bf16: q heads, then k heads, then v heads) belongs
+ * to position p = rows[b*R + r] (p = r when rows is NULL, then R = N); q and
+ * k heads are rotated by p with the tables (rotate-half pairs, the fp32
+ * operation order of rc_kv_assemble; no tables: no rotation) and written to
+ * q_out [B, N, Hq, D], k_out / v_out [B, N, Hkv, D] at position p. Positions
+ * outside [0, N) are skipped. bf16 only.
+ * Errors: INVALID_ARG for NULL pointers, bad shape, rows NULL with R != N,
+ * one table without the other, max_pos < N; UNSUPPORTED for fp32, D. */
+int rc_qkv_rope(const rc_shape* shape, const void* qkv, const int32_t* rows, int32_t R,
+                const float* rope_cos, const float* rope_sin, int32_t max_pos, void* q_out,
+                void* k_out, void* v_out, hipStream_t stream);
+
+/* SwiGLU activation: out[m, i] = silu(gu[m, i]) * gu[m, I + i] for m < M,
+ * i < I (gate_up: [M, 2I], out: [M, I], bf16; fp32 math). Errors:
+ * INVALID_ARG for NULL pointers, M < 0, I not a positive multiple of 8. */
+int rc_silu_mul(int64_t M, int32_t I, const void* gate_up, void* out, hipStream_t stream);
+
+/* dst[b, r] = src[b, rows[b*R + r]] for rows of row_bytes bytes (a multiple
+ * of 16): src [B, Nsrc, row], dst [B, R, row]. Positions outside [0, Nsrc)
+ * leave their destination row untouched. Errors: INVALID_ARG for NULL
+ * pointers or bad sizes. */
+int rc_gather_rows(int32_t B, int32_t Nsrc, int32_t R, int32_t row_bytes, const void* src,
+                   const int32_t* rows, void* dst, hipStream_t stream);
 
 /* Static description of a status code. */
 const char* rc_status_string(int status);

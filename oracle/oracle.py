@@ -15,7 +15,9 @@ Paper passages followed (arXiv 2605.07443):
     the first layer computed in full, K and V divergence, lambda, no divergence
     for item blocks) with separate history and item budgets (Sec. IV-A);
   * Eq. (1): scaled dot-product attention, causal, grouped-query;
-  * Sec. IV-A: Full-Recompute baseline (every row recomputed).
+  * Sec. IV-A: Full-Recompute baseline (every row recomputed);
+  * Sec. III-C.2b, several layers: the first computed in full, later layers
+    recomputing only the selected rows over their aligned caches.
 """
 from __future__ import annotations
 
@@ -379,6 +381,115 @@ def segments_with_window(segs, N: int, W: int) -> np.ndarray:
             runs[-1:] = [[dst, ln - 1, -1, 0], [dst + ln - 1, 1, -1, 0]]
         out[b] = np.array(runs, np.int32)
     return out
+
+
+# ---------------------------------------------------------------------------
+# Several layers: the first computed in full, later ones only for the
+# selected rows (Sec. III-C.2b), with pre-norm decoder layers
+# ---------------------------------------------------------------------------
+
+def f64(a):
+    """Storage array (fp32, or bf16 bits) as fp64 values."""
+    a = np.asarray(a)
+    return as_f32(a).astype(np.float64) if a.dtype in (np.uint16, np.float32) else a.astype(np.float64)
+
+
+def rmsnorm64(x, gamma, eps):
+    x = np.asarray(x, np.float64)
+    return x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps) * np.asarray(gamma, np.float64)
+
+
+def silu_mul64(gu):
+    gu = np.asarray(gu, np.float64)
+    I = gu.shape[-1] // 2
+    g, u = gu[..., :I], gu[..., I:]
+    return g / (1.0 + np.exp(-g)) * u
+
+
+def rope_at(x, pos, base):
+    """Rotate-half rotary encoding of x [..., T, H, D] at absolute positions
+    pos [..., T], angles pos * base^(-2j/D), in fp64."""
+    x = np.asarray(x, np.float64)
+    D = x.shape[-1]
+    half = D // 2
+    inv = base ** (-2.0 * np.arange(half) / D)
+    ang = np.asarray(pos, np.float64)[..., None, None] * inv
+    c, sn = np.cos(ang), np.sin(ang)
+    a, b = x[..., :half], x[..., half:]
+    return np.concatenate([a * c - b * sn, a * sn + b * c], axis=-1)
+
+
+def _attend(q, k, v, rows):
+    """Causal GQA attention (the pinned oracle, fp32 storage of fp64 values)."""
+    return f64(attention(q.astype(np.float32), k.astype(np.float32), v.astype(np.float32),
+                         rows=None if rows is None else np.ascontiguousarray(rows, np.int32)))
+
+
+def _layer_w(L):
+    return {k: f64(v) for k, v in L.items()}
+
+
+def decoder_stack_full(x, layers, Hq, Hkv, D, rope_base, eps, return_kv=False):
+    """Every row through every layer: h = x + O(attn(norm(x))), x' = h +
+    down(silu(gate) * up)(norm(h)). layers: dicts of storage arrays w_qkv,
+    w_o, w_gu, w_down, g_attn, g_mlp. Returns [B, N, H] fp64 (and each
+    layer's pre-rotation keys and values)."""
+    X = f64(x)
+    B, N, _ = X.shape
+    pos = np.broadcast_to(np.arange(N), (B, N))
+    kv = []
+    for L in layers:
+        W = _layer_w(L)
+        qkv = rmsnorm64(X, W["g_attn"], eps) @ W["w_qkv"].T
+        q = qkv[..., :Hq * D].reshape(B, N, Hq, D)
+        kr = qkv[..., Hq * D:(Hq + Hkv) * D].reshape(B, N, Hkv, D)
+        v = qkv[..., (Hq + Hkv) * D:].reshape(B, N, Hkv, D)
+        kv.append((kr, v))
+        att = _attend(rope_at(q, pos, rope_base), rope_at(kr, pos, rope_base), v, None)
+        h = X + att.reshape(B, N, Hq * D) @ W["w_o"].T
+        X = h + silu_mul64(rmsnorm64(h, W["g_mlp"], eps) @ W["w_gu"].T) @ W["w_down"].T
+    return (X, kv) if return_kv else X
+
+
+def decoder_stack_selective(x, layers, pools_by_layer, segs, rows, cos, sin, Hq, rope_base, eps,
+                            dt=1):
+    """The stack for the listed rows [B, R] (the selection is made by the
+    caller): layer 1 runs every row's projections and attends the listed rows
+    over its fresh K/V; layers 2..L project only the listed rows, put their
+    rotated keys and values into the layer's aligned cache (pinned assembly of
+    its pools, storage dtype dt) and attend over it. Returns the listed rows'
+    states [B, R, H] fp64 and layer 1's rotated keys [B, N, Hkv, D] fp64."""
+    X = f64(x)
+    B, N, Hd = X.shape
+    rows = np.asarray(rows)
+    R = rows.shape[1]
+    pool0 = pools_by_layer[0][0][0]
+    Hkv, D = pool0.shape[2], pool0.shape[3]
+    pos = np.broadcast_to(np.arange(N), (B, N))
+    bidx = np.arange(B)[:, None]
+    W = _layer_w(layers[0])
+    qkv = rmsnorm64(X, W["g_attn"], eps) @ W["w_qkv"].T
+    q = rope_at(qkv[..., :Hq * D].reshape(B, N, Hq, D), pos, rope_base)
+    k1 = rope_at(qkv[..., Hq * D:(Hq + Hkv) * D].reshape(B, N, Hkv, D), pos, rope_base)
+    v1 = qkv[..., (Hq + Hkv) * D:].reshape(B, N, Hkv, D)
+    att = _attend(q, k1, v1, rows)
+    h = X[bidx, rows] + att.reshape(B, R, Hq * D) @ W["w_o"].T
+    xs = h + silu_mul64(rmsnorm64(h, W["g_mlp"], eps) @ W["w_gu"].T) @ W["w_down"].T
+    store = (lambda a: f32_to_bf16(a.astype(np.float32))) if dt == 1 else (lambda a: a.astype(np.float32))
+    zeros = store(np.zeros((B, N, Hkv, D)))
+    for L, pools in zip(layers[1:], pools_by_layer[1:]):
+        W = _layer_w(L)
+        ka, va = assemble(zeros, zeros, pools, segs, cos, sin)
+        ka, va = f64(ka), f64(va)
+        qkv = rmsnorm64(xs, W["g_attn"], eps) @ W["w_qkv"].T
+        qf = np.zeros((B, N, Hq, D))
+        qf[bidx, rows] = rope_at(qkv[..., :Hq * D].reshape(B, R, Hq, D), rows, rope_base)
+        ka[bidx, rows] = rope_at(qkv[..., Hq * D:(Hq + Hkv) * D].reshape(B, R, Hkv, D), rows, rope_base)
+        va[bidx, rows] = qkv[..., (Hq + Hkv) * D:].reshape(B, R, Hkv, D)
+        att = _attend(qf, ka, va, rows)
+        h = xs + att.reshape(B, R, Hq * D) @ W["w_o"].T
+        xs = h + silu_mul64(rmsnorm64(h, W["g_mlp"], eps) @ W["w_gu"].T) @ W["w_down"].T
+    return xs, k1
 
 
 # ---------------------------------------------------------------------------

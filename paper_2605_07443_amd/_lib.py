@@ -22,7 +22,8 @@ RC_F32, RC_BF16 = 0, 1
 EXPORTS = ("rc_rope_table", "rc_kv_assemble", "rc_rerope", "rc_select_tokens",
            "rc_selective_attention", "rc_selective_attention_lse", "rc_attention_mass",
            "rc_select_tokens_eq3", "rc_paged_attention", "rc_segments_with_window",
-           "rc_kv_gather_tokens",
+           "rc_kv_gather_tokens", "rc_gemm_bf16", "rc_rmsnorm", "rc_qkv_rope", "rc_silu_mul",
+           "rc_gather_rows",
            "rc_status_string", "rc_last_error")
 
 
@@ -71,10 +72,17 @@ def load() -> ctypes.CDLL:
     L.rc_segments_with_window.argtypes = [vp, i32, i32, i32, i32, vp, i32, P(i32)]
     L.rc_kv_gather_tokens.argtypes = [P(RcShape), P(RcPool), i32, vp, vp, vp, vp, vp, i32, vp, vp,
                                       vp, i32, vp]
+    i64 = ctypes.c_int64
+    L.rc_gemm_bf16.argtypes = [i64, i32, i32, vp, vp, vp, vp, vp]
+    L.rc_rmsnorm.argtypes = [i32, i32, vp, vp, f32, vp, vp]
+    L.rc_qkv_rope.argtypes = [P(RcShape), vp, vp, i32, vp, vp, i32, vp, vp, vp, vp]
+    L.rc_silu_mul.argtypes = [i64, i32, vp, vp, vp]
+    L.rc_gather_rows.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp]
     for name in ("rc_rope_table", "rc_kv_assemble", "rc_rerope", "rc_select_tokens",
                  "rc_selective_attention", "rc_selective_attention_lse", "rc_attention_mass",
                  "rc_select_tokens_eq3", "rc_paged_attention", "rc_segments_with_window",
-                 "rc_kv_gather_tokens"):
+                 "rc_kv_gather_tokens", "rc_gemm_bf16", "rc_rmsnorm", "rc_qkv_rope", "rc_silu_mul",
+                 "rc_gather_rows"):
         getattr(L, name).restype = ctypes.c_int
     L.rc_status_string.argtypes = [ctypes.c_int]
     L.rc_status_string.restype = ctypes.c_char_p

@@ -11,7 +11,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG, "_build")
 LIB_PATH = os.path.join(PKG, "librcllm.so")
-SOURCES = ["capi.cpp", "assemble.hip", "select.hip", "attention.hip", "mass.hip"]
+SOURCES = ["capi.cpp", "assemble.hip", "select.hip", "attention.hip", "mass.hip", "layer.hip",
+           "gemm.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

@@ -459,3 +459,49 @@ def token_map_from_segments(segs, block_lens) -> torch.Tensor:
                 tmap[b, dst:dst + ln, 1] = blk * int(block_lens[p]) + torch.arange(ln, dtype=torch.int32)
                 tmap[b, dst:dst + ln, 2] = dst
     return tmap
+
+
+@dataclass
+class LayerWeights:
+    """One decoder layer (pre-norm attention + SwiGLU MLP), bf16."""
+    w_qkv: torch.Tensor   # [(Hq + 2 Hkv) D, H]: q heads, then k heads, then v heads
+    w_o: torch.Tensor     # [H, Hq D]
+    w_gu: torch.Tensor    # [2 I, H]: gate rows, then up rows
+    w_down: torch.Tensor  # [H, I]
+    g_attn: torch.Tensor  # [H]
+    g_mlp: torch.Tensor   # [H]
+
+
+def make_layers(n_layers: int, H: int, Hq: int, Hkv: int, D: int, inter: int, seed: int,
+                device="cpu"):
+    """Random decoder-layer weights, bf16: projections ~ N(0, 1/fan_in) so the
+    residual stream keeps unit scale; norm gains ~ 1 + N(0, 0.1^2)."""
+    layers = []
+    for l in range(n_layers):
+        g = _gen(device, seed, 9, l)
+
+        def w(rows, cols):
+            return (torch.randn((rows, cols), generator=g, device=device, dtype=torch.float32)
+                    / math.sqrt(cols)).to(torch.bfloat16)
+
+        gains = 1.0 + 0.1 * torch.randn((2, H), generator=g, device=device, dtype=torch.float32)
+        layers.append(LayerWeights(w_qkv=w((Hq + 2 * Hkv) * D, H), w_o=w(H, Hq * D),
+                                   w_gu=w(2 * inter, H), w_down=w(H, inter),
+                                   g_attn=gains[0].to(torch.bfloat16), g_mlp=gains[1].to(torch.bfloat16)))
+    return layers
+
+
+def make_stack(cfg: Config, seed: int, n_layers: int, H: int, inter: int, device="cpu"):
+    """A batch of `cfg` for a stack of decoder layers: input states x [B, N, H]
+    ~ N(0, 1), one pool set per layer (independent contents, the same
+    segment table), random layer weights. Returns (x, layers, pools_by_layer,
+    segs [B, S, 4])."""
+    w0 = make(cfg, seed, device=device)
+    pools = [w0.pools]
+    for l in range(1, n_layers):
+        pools.append(make(cfg, seed, device=device, pool_seed=seed * 131 + l).pools)
+    gx = _gen(device, seed, 10)
+    x = torch.randn((cfg.B, cfg.N, H), generator=gx, device=device, dtype=torch.float32).to(cfg.torch_dtype)
+    layers = make_layers(n_layers, H, cfg.Hq, cfg.Hkv, cfg.D, inter, seed, device)
+    segs = w0.segs
+    return x, layers, pools, segs

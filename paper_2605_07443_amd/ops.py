@@ -16,6 +16,7 @@ import torch
 
 from . import _lib
 from ._lib import RcPool, RcShape, check
+from .inputs import LayerWeights
 
 
 def _dtype_code(t: torch.Tensor) -> int:
@@ -488,3 +489,123 @@ def eq3_select_tokens_path(q, k_fresh, v_fresh, pools, token_map, status: Segmen
 def full_prefill(q, k_fresh, v_fresh, scale=None, out=None, stream=None):
     """Full-Recompute baseline: causal attention of every row over fresh K/V."""
     return selective_attention(q, k_fresh, v_fresh, None, scale, out, stream)
+
+
+# ------------------------------------------------------- several layers
+
+def gemm(x, w, residual=None, out=None, stream=None):
+    """rc_gemm_bf16: out[M, n] = x[M, k] @ w[n, k]^T (+ residual)."""
+    M, k = x.shape
+    n = w.shape[0]
+    if w.shape[1] != k:
+        raise ValueError(f"x [M, {k}] and w [{n}, {w.shape[1]}] do not match")
+    out = torch.empty((M, n), dtype=x.dtype, device=x.device) if out is None else out
+    check(_lib.load().rc_gemm_bf16(
+        int(M), int(n), int(k), _dev(x, "x"), _dev(w, "w"),
+        None if residual is None else _dev(residual, "residual"), _dev(out, "out"), _stream(stream)))
+    return out
+
+
+def rmsnorm(x, gamma, eps=1e-5, out=None, stream=None):
+    M, Hd = x.shape
+    out = torch.empty_like(x) if out is None else out
+    check(_lib.load().rc_rmsnorm(int(M), int(Hd), _dev(x, "x"), _dev(gamma, "gamma"),
+                                 ctypes.c_float(eps), _dev(out, "out"), _stream(stream)))
+    return out
+
+
+def qkv_rope(qkv, B, N, Hq, Hkv, D, rows, cos, sin, q_out, k_out, v_out, stream=None):
+    R = N if rows is None else int(rows.shape[1])
+    check(_lib.load().rc_qkv_rope(
+        ctypes.byref(_shape(B, N, Hq, Hkv, D, _lib.RC_BF16)), _dev(qkv, "qkv"),
+        None if rows is None else _dev(rows, "rows"), R,
+        None if cos is None else _dev(cos, "cos"), None if sin is None else _dev(sin, "sin"),
+        0 if cos is None else int(cos.shape[0]), _dev(q_out, "q_out"), _dev(k_out, "k_out"),
+        _dev(v_out, "v_out"), _stream(stream)))
+
+
+def silu_mul(gate_up, out=None, stream=None):
+    M, I2 = gate_up.shape
+    out = torch.empty((M, I2 // 2), dtype=gate_up.dtype, device=gate_up.device) if out is None else out
+    check(_lib.load().rc_silu_mul(int(M), int(I2 // 2), _dev(gate_up, "gate_up"), _dev(out, "out"),
+                                  _stream(stream)))
+    return out
+
+
+def gather_rows(src, rows, out=None, stream=None):
+    """dst[b, r] = src[b, rows[b, r]] for src [B, Nsrc, ...]."""
+    B, Nsrc = src.shape[:2]
+    R = int(rows.shape[1])
+    row_bytes = src[0, 0].numel() * src.element_size()
+    out = torch.empty((B, R) + tuple(src.shape[2:]), dtype=src.dtype, device=src.device) if out is None else out
+    check(_lib.load().rc_gather_rows(int(B), int(Nsrc), R, int(row_bytes), _dev(src, "src"),
+                                     _dev(rows, "rows"), _dev(out, "out"), _stream(stream)))
+    return out
+
+
+def _mlp_and_residual(h, L: "LayerWeights", eps):
+    n2 = rmsnorm(h, L.g_mlp, eps)
+    act = silu_mul(gemm(n2, L.w_gu))
+    return gemm(act, L.w_down, residual=h)
+
+
+def stack_prefill(x, layers, pools_by_layer, segs: Segments, k: int, cos, sin, eps=1e-5):
+    """Selective prefill through a stack of decoder layers (Sec. III-C.2b).
+    Layer 1 is computed for every row: its fresh K are scored against the
+    layer's aligned cache (score-only pass), the top-k picks the rows, and the
+    rows' attention runs over the layer's fresh K/V. Layers 2..L recompute only
+    those rows: each layer's cache is assembled (gather + alignment), the rows'
+    projected K/V overwrite their positions in it, and the rows attend over
+    it. x: [B, N, H] bf16 input states. Returns (hidden [B, R, H] of the
+    rows after the last layer, rows, layer-1 scores)."""
+    B, N, Hd = x.shape
+    L0 = layers[0]
+    Hkv = pools_by_layer[0][0][0].shape[2]
+    D = pools_by_layer[0][0][0].shape[3]
+    Hq = L0.w_o.shape[1] // D
+    R = segs.n_fresh + int(k)
+    dev, dt = x.device, x.dtype
+    # ---- layer 1, every row
+    n = rmsnorm(x.view(B * N, Hd), L0.g_attn, eps)
+    qkv = gemm(n, L0.w_qkv)
+    q = torch.empty((B, N, Hq, D), dtype=dt, device=dev)
+    k1 = torch.empty((B, N, Hkv, D), dtype=dt, device=dev)
+    v1 = torch.empty_like(k1)
+    qkv_rope(qkv, B, N, Hq, Hkv, D, None, cos, sin, q, k1, v1)
+    del qkv, n
+    scores = torch.empty((B, N), dtype=torch.float32, device=dev)
+    kv_assemble(pools_by_layer[0], segs, k1, v1, cos, sin, scores_out=scores, score_only=True)
+    rows, _ = select_tokens(segs, k, k1, v1, None, None, scores_in=scores, patch=False)
+    attn = selective_attention(q, k1, v1, rows)
+    x_rows = gather_rows(x, rows).view(B * R, Hd)
+    h = gemm(attn.view(B * R, Hq * D), L0.w_o, residual=x_rows)
+    xs = _mlp_and_residual(h, L0, eps)
+    # ---- layers 2..L, the selected rows only
+    zeros = torch.zeros((B, N, Hkv, D), dtype=dt, device=dev)  # fresh positions are all rows
+    for L, pools in zip(layers[1:], pools_by_layer[1:]):
+        k_asm, v_asm = kv_assemble(pools, segs, zeros, zeros, cos, sin)
+        n = rmsnorm(xs, L.g_attn, eps)
+        qkv = gemm(n, L.w_qkv)
+        qkv_rope(qkv, B, N, Hq, Hkv, D, rows, cos, sin, q, k_asm, v_asm)
+        attn = selective_attention(q, k_asm, v_asm, rows)
+        h = gemm(attn.view(B * R, Hq * D), L.w_o, residual=xs)
+        xs = _mlp_and_residual(h, L, eps)
+    return xs.view(B, R, Hd), rows, scores
+
+
+def stack_full(x, layers, Hq, Hkv, D, cos, sin, eps=1e-5):
+    """Full recompute through the stack: every row of every layer over fresh
+    K/V. Returns hidden [B, N, H] after the last layer."""
+    B, N, Hd = x.shape
+    dev, dt = x.device, x.dtype
+    q = torch.empty((B, N, Hq, D), dtype=dt, device=dev)
+    kk = torch.empty((B, N, Hkv, D), dtype=dt, device=dev)
+    vv = torch.empty_like(kk)
+    xs = x.reshape(B * N, Hd)
+    for L in layers:
+        n = rmsnorm(xs, L.g_attn, eps)
+        qkv_rope(gemm(n, L.w_qkv), B, N, Hq, Hkv, D, None, cos, sin, q, kk, vv)
+        attn = selective_attention(q, kk, vv)
+        h = gemm(attn.view(B * N, Hq * D), L.w_o, residual=xs)
+        xs = _mlp_and_residual(h, L, eps)
+    return xs.view(B, N, Hd)

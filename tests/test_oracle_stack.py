@@ -1,0 +1,132 @@
+"""Pins for the oracle's decoder stack (arXiv 2605.07443, Sec. III-C.2b: the
+first layer computed in full, later layers recomputing only the selected
+rows over cached K/V): closed forms, agreement with separately pinned oracle
+functions, and the invariants the method must satisfy (every row selected ==
+full recompute; a cache holding exactly the full computation's K/V makes the
+selected rows exact)."""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2605_07443_amd import inputs
+
+EPS = 1e-5
+
+
+def _weights(n_layers, H, Hq, Hkv, D, I, seed, zero_out=False, dt="f32"):
+    rng = np.random.default_rng(seed)
+    layers = []
+    for _ in range(n_layers):
+        def w(r, c):
+            a = (rng.standard_normal((r, c)) / math.sqrt(c)).astype(np.float32)
+            return O.f32_to_bf16(a) if dt == "bf16" else a
+        L = dict(w_qkv=w((Hq + 2 * Hkv) * D, H), w_o=w(H, Hq * D), w_gu=w(2 * I, H),
+                 w_down=w(H, I), g_attn=(1 + 0.1 * rng.standard_normal(H)).astype(np.float32),
+                 g_mlp=(1 + 0.1 * rng.standard_normal(H)).astype(np.float32))
+        if zero_out:
+            L["w_o"] = np.zeros_like(L["w_o"])
+            L["w_down"] = np.zeros_like(L["w_down"])
+        layers.append(L)
+    return layers
+
+
+def test_rmsnorm_and_silu_closed_forms():
+    rng = np.random.default_rng(1)
+    x = rng.standard_normal((5, 64)) * 3.0
+    y = O.rmsnorm64(x, np.ones(64), 0.0)
+    np.testing.assert_allclose(np.sqrt(np.mean(y * y, -1)), 1.0, rtol=1e-12)
+    np.testing.assert_allclose(O.rmsnorm64(7.5 * x, np.ones(64), 0.0), y, rtol=1e-12)
+    g = np.array([[0.0, 1.0, -1.0, 40.0, -40.0, 2.0, 2.0, 2.0, 2.0, 2.0]])
+    gu = np.concatenate([g, np.ones_like(g)], -1)
+    want = np.array([0.0, 1 / (1 + math.exp(-1)), -1 / (1 + math.e), 40.0, 0.0, 2 / (1 + math.exp(-2)),
+                     2 / (1 + math.exp(-2)), 2 / (1 + math.exp(-2)), 2 / (1 + math.exp(-2)),
+                     2 / (1 + math.exp(-2))])
+    np.testing.assert_allclose(O.silu_mul64(gu)[0], want, rtol=1e-12, atol=1e-15)
+
+
+def test_rope_at_matches_the_pinned_rotation():
+    """fp64 rotation at absolute positions vs the pinned table-driven
+    rotation (fp32 tables, fp32 arithmetic): equal to fp32 rounding."""
+    B, N, H, D = 2, 33, 3, 64
+    x = np.random.default_rng(2).standard_normal((B, N, H, D)).astype(np.float32)
+    cos, sin = O.rope_table(N, D, 10000.0)
+    delta = np.broadcast_to(np.arange(N, dtype=np.int32), (B, N)).copy()
+    want = O.rerope(x, delta, cos, sin)
+    got = O.rope_at(x, np.broadcast_to(np.arange(N), (B, N)), 10000.0)
+    np.testing.assert_allclose(got, want, rtol=0, atol=2e-6)
+
+
+def _small_case(seed=3, n_layers=3):
+    cfg = inputs.TEST_CONFIGS["tiny-f32-gqa"]
+    w = inputs.make(cfg, seed)
+    H, I = 96, 128
+    x = np.random.default_rng(seed).standard_normal((cfg.B, cfg.N, H)).astype(np.float32)
+    return cfg, w, x, H, I
+
+
+def test_zero_output_projections_make_the_stack_the_identity():
+    cfg, w, x, H, I = _small_case()
+    layers = _weights(3, H, cfg.Hq, cfg.Hkv, cfg.D, I, 4, zero_out=True)
+    full = O.decoder_stack_full(x, layers, cfg.Hq, cfg.Hkv, cfg.D, cfg.rope_base, EPS)
+    np.testing.assert_array_equal(full, x.astype(np.float64))
+    cos, sin = O.rope_table(cfg.N, cfg.D, cfg.rope_base)
+    pools = [[(a.numpy(), b.numpy()) for a, b in w.pools]] * 3
+    rows = O.topk(w.segs.numpy(), cfg.N, cfg.k, np.random.default_rng(5).random((cfg.B, cfg.N)).astype(np.float32))
+    sel, _ = O.decoder_stack_selective(x, layers, pools, w.segs.numpy(), rows, cos, sin, cfg.Hq,
+                                       cfg.rope_base, EPS, dt=0)
+    np.testing.assert_array_equal(sel, np.stack([x[b, rows[b]] for b in range(cfg.B)]).astype(np.float64))
+
+
+def test_every_row_selected_equals_full_recompute():
+    cfg, w, x, H, I = _small_case()
+    layers = _weights(3, H, cfg.Hq, cfg.Hkv, cfg.D, I, 6)
+    full = O.decoder_stack_full(x, layers, cfg.Hq, cfg.Hkv, cfg.D, cfg.rope_base, EPS)
+    cos, sin = O.rope_table(cfg.N, cfg.D, cfg.rope_base)
+    pools = [[(a.numpy(), b.numpy()) for a, b in w.pools]] * 3
+    rows = np.broadcast_to(np.arange(cfg.N, dtype=np.int32), (cfg.B, cfg.N)).copy()
+    sel, _ = O.decoder_stack_selective(x, layers, pools, w.segs.numpy(), rows, cos, sin, cfg.Hq,
+                                       cfg.rope_base, EPS, dt=0)
+    np.testing.assert_allclose(sel, full, rtol=0, atol=2e-5)
+
+
+def test_exact_cache_makes_the_selected_rows_exact():
+    """Pools holding each layer's keys (rotated to block-local positions) and
+    values from the full computation: after alignment the cache equals the
+    full computation's K/V, so every selected row equals its full-recompute
+    row, whichever rows are selected."""
+    cfg, w, x, H, I = _small_case(seed=7)
+    layers = _weights(3, H, cfg.Hq, cfg.Hkv, cfg.D, I, 8)
+    full, kv = O.decoder_stack_full(x, layers, cfg.Hq, cfg.Hkv, cfg.D, cfg.rope_base, EPS,
+                                    return_kv=True)
+    segs = w.segs.numpy().copy()
+    B, S = segs.shape[:2]
+    Lmax = int(segs[..., 1].max())
+    cos, sin = O.rope_table(cfg.N, cfg.D, cfg.rope_base)
+    pools_by_layer = []
+    new = segs.copy()
+    for kr, v in kv:
+        pk = np.zeros((B * S, Lmax, cfg.Hkv, cfg.D), np.float32)
+        pv = np.zeros_like(pk)
+        for b in range(B):
+            for s in range(S):
+                dst, ln, p, _ = segs[b, s]
+                if p < 0:
+                    continue
+                pk[b * S + s, :ln] = O.rope_at(kr[b, dst:dst + ln], np.arange(ln), cfg.rope_base)
+                pv[b * S + s, :ln] = v[b, dst:dst + ln]
+                new[b, s, 2], new[b, s, 3] = 0, b * S + s
+        pools_by_layer.append([(pk, pv)])
+    rng = np.random.default_rng(9)
+    for _ in range(2):
+        rows = O.topk(new, cfg.N, cfg.k, rng.random((B, cfg.N)).astype(np.float32))
+        sel, _ = O.decoder_stack_selective(x, layers, pools_by_layer, new, rows, cos, sin, cfg.Hq,
+                                           cfg.rope_base, EPS, dt=0)
+        want = np.stack([full[b, rows[b]] for b in range(B)])
+        np.testing.assert_allclose(sel, want, rtol=0, atol=2e-4)
+    # a noisy cache (the workload's own pools) does move the selected rows
+    pools = [[(a.numpy(), b.numpy()) for a, b in w.pools]] * 3
+    sel_n, _ = O.decoder_stack_selective(x, layers, pools, segs, rows, cos, sin, cfg.Hq,
+                                         cfg.rope_base, EPS, dt=0)
+    assert np.abs(sel_n - want).max() > 1e-2

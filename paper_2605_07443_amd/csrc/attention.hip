@@ -336,9 +336,12 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
       float m = -INFINITY;
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
-        m = fmaxf(m, fmaxf(fmaxf(s[kb][nb][0], s[kb][nb][1]), fmaxf(s[kb][nb][2], s[kb][nb][3])));
-      m = fmaxf(m, __shfl_xor(m, 16, 64));
-      mx[nb] = fmaxf(m, __shfl_xor(m, 32, 64));
+        m = __builtin_elementwise_maximum(
+            __builtin_elementwise_maximum(m, s[kb][nb][0]),
+            __builtin_elementwise_maximum(__builtin_elementwise_maximum(s[kb][nb][1], s[kb][nb][2]),
+                                          s[kb][nb][3]));
+      m = __builtin_elementwise_maximum(m, __shfl_xor(m, 16, 64));
+      mx[nb] = __builtin_elementwise_maximum(m, __shfl_xor(m, 32, 64));
     }
     // a query sees key 0 in the first tile, so the reference max is finite after it
     if (__ballot(mx[0] * scale_log2e - m_run[0] * scale_log2e > kLazy ||

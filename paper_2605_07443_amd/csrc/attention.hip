@@ -59,6 +59,24 @@ struct AttnSmem {
   uint16_t v[2][kKT][D + 16];  // V tiles, key-major (read transposed)
 };
 
+// D = 128, not paged: tiles land in LDS straight from global memory
+// (global_load_lds_dwordx4: each wave instruction writes 1 KB contiguously, 4
+// rows of 256 bytes), so rows cannot be padded; the 16-byte chunks of a row
+// are XOR-swizzled instead. K row r keeps data chunk c at chunk c ^ (r & 15):
+// the fragment reads of 16 consecutive rows then hit 16 distinct chunks. V
+// row r keeps data chunk c at c ^ (2 (r & 3)): the 4 rows of each transposed
+// read pass use 4 distinct chunk pairs.
+// The two buffers are separate objects so that the compiler can tell the
+// loads into one buffer from the reads of the other and does not wait for
+// the former before the latter.
+struct AttnBufDirect {
+  uint16_t k[kKT * 128];
+  uint16_t v[kKT * 128];
+};
+struct AttnNone {
+  int unused;
+};
+
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 typedef float f32x2 __attribute__((ext_vector_type(2)));
@@ -105,7 +123,9 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
   constexpr int UPR = D / 8;          // 16-byte units per K/V head row
   constexpr int KU = kKT * UPR / kAttnThreads;   // K (and V) units per thread
   constexpr int KSTEP = kAttnThreads / UPR;      // keys between a thread's units
-  __shared__ AttnSmem<D> sm;
+  constexpr bool DIRECT = (D == 128) && !PAGED;
+  __shared__ std::conditional_t<DIRECT, AttnNone, AttnSmem<D>> sm;
+  __shared__ std::conditional_t<DIRECT, AttnBufDirect, AttnNone> sb0, sb1;
   __shared__ int s_ext[4];
   __shared__ int4 s_psegs[PAGED ? kPagedMaxSegments : 1];
   __shared__ uint32_t s_sel[PAGED ? kMaxSelectN / 32 : 1];  // recomputed rows of the request
@@ -192,9 +212,33 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
   const uint16_t* kp = k + off0;
   const uint16_t* vp = v + off0;
   const size_t tile_step = static_cast<size_t>(kKT) * stride;
-  u32x4 kreg[KU], vreg[KU];
+  u32x4 kreg[DIRECT ? 1 : KU], vreg[DIRECT ? 1 : KU];
   int pdelta[PAGED ? PK : 1];  // paged: rotation of each staged key (0: none)
+  // DIRECT: wave w fills rows 16w .. 16w+15 of both tiles with 4 + 4 loads;
+  // lane l writes chunk l % 16 of row 16w + 4j + l / 16 and so fetches the
+  // data chunk that the swizzle stores there. Keys past N repeat key N - 1
+  // (finite values; the causal mask removes them).
+  auto issue_tile = [&](int t, auto buf_tag) {
+    if constexpr (DIRECT) {
+      auto& dst = decltype(buf_tag)::value ? sb1 : sb0;
+      const int ch = lane & 15;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int row = wave * 16 + j * 4 + (lane >> 4);
+        const int key = min(t * kKT + row, N - 1);
+        const uint16_t* kr = k + (static_cast<size_t>(b) * N + key) * stride + static_cast<size_t>(g) * D;
+        const uint16_t* vr = v + (static_cast<size_t>(b) * N + key) * stride + static_cast<size_t>(g) * D;
+        __builtin_amdgcn_global_load_lds(
+            (const __attribute__((address_space(1))) void*)(kr + ((ch ^ (row & 15)) * 8)),
+            (__attribute__((address_space(3))) void*)(&dst.k[(wave * 16 + j * 4) * 128]), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(
+            (const __attribute__((address_space(1))) void*)(vr + ((ch ^ (2 * (row & 3))) * 8)),
+            (__attribute__((address_space(3))) void*)(&dst.v[(wave * 16 + j * 4) * 128]), 16, 0, 0);
+      }
+    }
+  };
   auto load_tile = [&](int t) {
+    if constexpr (!DIRECT) {
     if constexpr (PAGED) {
 #pragma unroll
       for (int i = 0; i < PK; ++i) {
@@ -243,8 +287,10 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
         vreg[i] = in ? *reinterpret_cast<const u32x4*>(vt + i * KSTEP * stride) : u32x4{0, 0, 0, 0};
       }
     }
-  };
+      }
+};
   auto store_tile = [&](int buf) {
+    if constexpr (!DIRECT) {
     if constexpr (PAGED) {
 #pragma unroll
       for (int i = 0; i < PK; ++i) {
@@ -273,7 +319,8 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
       *reinterpret_cast<u32x4*>(&sm.k[buf][key0 + i * KSTEP][col0]) = kreg[i];
       *reinterpret_cast<u32x4*>(&sm.v[buf][key0 + i * KSTEP][col0]) = vreg[i];
     }
-  };
+      }
+};
 
   f32x4 o[DB][2];
 #pragma unroll
@@ -290,17 +337,47 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
   const int tr_row = q4 * 4 + (c16 >> 2);
   const int tr_col = 4 * (c16 & 3);
 
-  load_tile(0);
-  store_tile(0);
-  __syncthreads();
-  if (n_kv > 1) load_tile(1);
+  // LDS addresses of a K fragment (row, 16-byte data chunk u) and of a
+  // transposed V read (row, element col)
+  auto kfrag = [&](auto buf_tag, int row, int u) -> const uint16_t* {
+    constexpr int BUF = decltype(buf_tag)::value;
+    if constexpr (DIRECT) return &(BUF ? sb1 : sb0).k[row * 128 + ((u ^ (row & 15)) * 8)];
+    else return &sm.k[BUF][row][u * 8];
+  };
+  auto vtr = [&](auto buf_tag, int row, int col) -> const uint16_t* {
+    constexpr int BUF = decltype(buf_tag)::value;
+    if constexpr (DIRECT)
+      return &(BUF ? sb1 : sb0).v[row * 128 + (((col >> 3) ^ (2 * (row & 3))) * 8) + (col & 7)];
+    else return &sm.v[BUF][row][col];
+  };
+  using Buf0 = std::integral_constant<int, 0>;
+  using Buf1 = std::integral_constant<int, 1>;
+
+  if constexpr (DIRECT) {
+    issue_tile(0, Buf0{});
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+  } else {
+    load_tile(0);
+    store_tile(0);
+    __syncthreads();
+    if (n_kv > 1) load_tile(1);
+  }
+
+  // first tile whose last key passes this wave's earliest row
+  const int t_mask = min(n_kv, wave_pmin / kKT);
 
   // One KV tile: S^T = K Q^T, (masked) online softmax, O^T += V^T P^T, then
-  // stage the next tile. MASK selects the causal mask (only tiles reaching past
-  // some row of this wave need it, so the main loop runs without it).
-  auto do_tile = [&](int t, auto mask_tag) {
-    constexpr bool MASK = decltype(mask_tag)::value;
-    const int cur = t & 1;
+  // stage the next tile. The causal mask is applied only on tiles reaching past
+  // some row of this wave (a uniform branch).
+  auto do_tile = [&](int t, auto buf_tag) {
+    const bool MASK = t >= t_mask;                  // uniform: tiles past this wave's first row
+    constexpr int cur = decltype(buf_tag)::value;   // == t & 1
+    using Next = std::integral_constant<int, cur ^ 1>;
+    // DIRECT: the next tile flows into the other buffer during this one
+    if constexpr (DIRECT) {
+      if (t + 1 < n_kv) issue_tile(t + 1, Next{});
+    }
 
     // ---- S^T for 64 keys x 32 queries (8 independent accumulators)
     f32x4 s[4][2];
@@ -311,14 +388,13 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
     for (int dc = 0; dc < DC; ++dc)
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) {
-        const bf16x8 a = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(&sm.k[cur][kb * 16 + c16][dc * 32 + q4 * 8]));
+        const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(kfrag(buf_tag, kb * 16 + c16, dc * 4 + q4)));
         s[kb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[0][dc], s[kb][0], 0, 0, 0);
         s[kb][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[1][dc], s[kb][1], 0, 0, 0);
       }
     __builtin_amdgcn_s_setprio(0);
 
-    if constexpr (MASK) {
+    if (MASK) {
       const int j0 = t * kKT;
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb)
@@ -389,8 +465,8 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
     for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const u32x2 lo = lds_read_tr4(&sm.v[cur][kc * 32 + tr_row][db * 16 + tr_col]);
-        const u32x2 hi = lds_read_tr4(&sm.v[cur][kc * 32 + 16 + tr_row][db * 16 + tr_col]);
+        const u32x2 lo = lds_read_tr4(vtr(buf_tag, kc * 32 + tr_row, db * 16 + tr_col));
+        const u32x2 hi = lds_read_tr4(vtr(buf_tag, kc * 32 + 16 + tr_row, db * 16 + tr_col));
         const bf16x8 a = __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
         o[db][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][0], o[db][0], 0, 0, 0);
         o[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][1], o[db][1], 0, 0, 0);
@@ -403,18 +479,21 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
     __builtin_amdgcn_s_setprio(0);
 
     // ---- stage the next tile into the other buffer, prefetch the one after
-    if (t + 1 < n_kv) {
+    if constexpr (DIRECT) {
+      __builtin_amdgcn_s_waitcnt(0);   // this wave's loads of tile t + 1 have landed
+    } else if (t + 1 < n_kv) {
       store_tile(cur ^ 1);
       if (t + 2 < n_kv) load_tile(t + 2);
     }
     __syncthreads();
   };
 
-  // first tile whose last key passes this wave's earliest row
-  const int t_mask = min(n_kv, wave_pmin / kKT);
   int t = 0;
-  for (; t < t_mask; ++t) do_tile(t, std::false_type{});
-  for (; t < n_kv; ++t) do_tile(t, std::true_type{});
+  for (; t + 1 < n_kv; t += 2) {
+    do_tile(t, Buf0{});
+    do_tile(t + 1, Buf1{});
+  }
+  if (t < n_kv) do_tile(t, Buf0{});
 
   // ---- log-sum-exp: the 4 lanes of a query column hold disjoint keys
   if constexpr (LSE) {

@@ -11,6 +11,8 @@
 // with the next tile's global loads in flight during the MFMAs. Tiles are
 // ordered n-fastest within groups of 8 row tiles, so the workgroups running
 // together share both operands in L2.
+#include <type_traits>
+
 #include "rc_common.h"
 
 namespace rc {
@@ -135,6 +137,133 @@ void gemm_bf16_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict
     }
 }
 
+// Large tiles for k % 64 == 0: a 256 x 256 tile per workgroup of 8 waves,
+// each 128 x 64 (8 x 4 accumulator blocks), two waves per SIMD. X and W tiles
+// of 64 k go straight from global memory into LDS (global_load_lds_dwordx4,
+// 1 KB = 8 rows of 128 B per wave instruction), so the 16-byte chunks of a
+// row are XOR-swizzled instead of padded: row r keeps data chunk c at chunk
+// c ^ ((r >> 1) & 7), which puts the fragment reads of 16 consecutive rows on
+// 16 distinct (bank half, chunk) pairs. The two LDS buffers are separate
+// objects and every k tile knows its buffer at compile time, so loading one
+// never waits on reading the other. Rows past M or n repeat the last row
+// (finite values whose products are never stored).
+constexpr int kBThreads = 512;
+constexpr int kBM = 256, kBN = 256;
+struct GemmBuf {
+  uint16_t a[kBM * kGK];
+  uint16_t b[kBN * kGK];
+};
+
+__global__ __launch_bounds__(kBThreads) __attribute__((amdgpu_waves_per_eu(2)))
+void gemm_bf16_big_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ w,
+                          const uint16_t* __restrict__ res, uint16_t* __restrict__ y, int64_t M,
+                          int n, int k, int tiles_m, int tiles_n) {
+  __shared__ GemmBuf s0, s1;
+  const int64_t bid = blockIdx.x;
+  const int64_t per_group = static_cast<int64_t>(kGGroup) * tiles_n;
+  const int64_t grp = bid / per_group;
+  const int64_t in = bid - grp * per_group;
+  const int64_t first_m = grp * kGGroup;
+  const int64_t gm = min(static_cast<int64_t>(kGGroup), tiles_m - first_m);
+  const int64_t tm = first_m + in % gm;
+  const int tn = static_cast<int>(in / gm);
+  const int64_t m0 = tm * kBM;
+  const int n0 = tn * kBN;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int c16 = lane & 15;
+  const int q4 = lane >> 4;
+  const int wm = (wave >> 2) * 128;
+  const int wn = (wave & 3) * 64;
+  const int n_kt = k / kGK;
+
+  // wave w fills rows 32w .. 32w+31 of both tiles, 8 rows per instruction
+  auto issue = [&](int kt, auto buf_tag) {
+    GemmBuf& dst = decltype(buf_tag)::value ? s1 : s0;
+    const int ch = lane & 7;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int row = wave * 32 + j * 8 + (lane >> 3);
+      const int dch = ch ^ ((row >> 1) & 7);
+      const int64_t gr = min(m0 + row, M - 1);
+      const int gc = min(n0 + row, n - 1);
+      const int kk = kt * kGK + dch * 8;
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(x + gr * k + kk),
+                                       (__attribute__((address_space(3))) void*)(&dst.a[(wave * 32 + j * 8) * kGK]),
+                                       16, 0, 0);
+      __builtin_amdgcn_global_load_lds(
+          (const __attribute__((address_space(1))) void*)(w + static_cast<int64_t>(gc) * k + kk),
+          (__attribute__((address_space(3))) void*)(&dst.b[(wave * 32 + j * 8) * kGK]), 16, 0, 0);
+    }
+  };
+
+  f32x4 acc[8][4];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto compute = [&](auto buf_tag) {
+    const GemmBuf& src = decltype(buf_tag)::value ? s1 : s0;
+#pragma unroll
+    for (int ks = 0; ks < kGK / 32; ++ks) {
+      const int u = ks * 4 + q4;
+      bf16x8 fb[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int rb = wn + j * 16 + c16;
+        fb[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(
+                                               &src.b[rb * kGK + ((u ^ ((rb >> 1) & 7)) * 8)]));
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int ra = wm + i * 16 + c16;
+        const bf16x8 fa = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(
+                                                       &src.a[ra * kGK + ((u ^ ((ra >> 1) & 7)) * 8)]));
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa, fb[j], acc[i][j], 0, 0, 0);
+      }
+    }
+  };
+  using B0 = std::integral_constant<int, 0>;
+  using B1 = std::integral_constant<int, 1>;
+
+  issue(0, B0{});
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  int kt = 0;
+  for (; kt + 1 < n_kt; kt += 2) {
+    issue(kt + 1, B1{});
+    compute(B0{});
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (kt + 2 < n_kt) issue(kt + 2, B0{});
+    compute(B1{});
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+  }
+  if (kt < n_kt) compute(B0{});
+
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int gc = n0 + wn + j * 16 + c16;
+      if (gc >= n) continue;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t gr = m0 + wm + i * 16 + q4 * 4 + r;
+        if (gr >= M) continue;
+        float v = acc[i][j][r];
+        if (res) v += bf16_to_f32(res[gr * n + gc]);
+        y[gr * n + gc] = f32_to_bf16(v);
+      }
+    }
+}
+
 }  // namespace
 }  // namespace rc
 
@@ -148,6 +277,16 @@ extern "C" int rc_gemm_bf16(int64_t M, int32_t n, int32_t k, const void* x, cons
                 static_cast<long long>(M), n, k);
   if (residual == y) return fail(RC_ERR_INVALID_ARG, "residual must not alias y");
   if (M == 0) return RC_OK;
+  if (k % kGK == 0 && M >= kBM && n >= kBN) {
+    const int64_t tm = (M + kBM - 1) / kBM;
+    const int tn = (n + kBN - 1) / kBN;
+    if (tm * tn > 0x7fffffff) return fail(RC_ERR_UNSUPPORTED, "grid too large");
+    hipLaunchKernelGGL(gemm_bf16_big_kernel, dim3(static_cast<unsigned>(tm * tn)), dim3(kBThreads), 0,
+                       stream, static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w),
+                       static_cast<const uint16_t*>(residual), static_cast<uint16_t*>(y), M, n, k,
+                       static_cast<int>(tm), tn);
+    return check_launch("rc_gemm_bf16");
+  }
   const int64_t tiles_m = (M + kGM - 1) / kGM;
   const int tiles_n = (n + kGN - 1) / kGN;
   const int64_t blocks = tiles_m * tiles_n;

@@ -34,7 +34,8 @@ def _lib_loaded():
 
 
 @pytest.mark.parametrize("M,n,k,res", [(1, 8, 8, False), (127, 100, 72, True), (129, 129, 200, False),
-                                       (300, 640, 256, True), (256, 256, 4096, True)])
+                                       (300, 640, 256, True), (256, 256, 4096, True),
+                                       (257, 260, 64, True), (513, 777, 192, False), (700, 300, 640, True)])
 def test_gemm_small_against_fp64(M, n, k, res):
     """Own MFMA GEMM against an fp64 host product of the same bf16 operands:
     one bf16 rounding of the fp32 result (2^-8 relative) plus fp32 sums."""

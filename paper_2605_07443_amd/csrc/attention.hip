@@ -64,8 +64,10 @@ struct AttnSmem {
 // rows of 256 bytes), so rows cannot be padded; the 16-byte chunks of a row
 // are XOR-swizzled instead. K row r keeps data chunk c at chunk c ^ (r & 15):
 // the fragment reads of 16 consecutive rows then hit 16 distinct chunks. V
-// row r keeps data chunk c at c ^ (2 (r & 3)): the 4 rows of each transposed
-// read pass use 4 distinct chunk pairs.
+// is stored as 16 x 16 blocks (16 keys x 16 dims, key-major, 512 bytes): block
+// (key / 16, dim / 16) at byte 4096 (key / 16) + 512 (dim / 16). A transposed
+// read then takes one whole block, lane l the 8 bytes at 8 l, so every V^T
+// operand is one base address plus a constant offset and no read conflicts.
 // The two buffers are separate objects so that the compiler can tell the
 // loads into one buffer from the reads of the other and does not wait for
 // the former before the latter.
@@ -91,6 +93,37 @@ __device__ __forceinline__ u32x2 lds_read_tr4(const uint16_t* p) {
   const v4i16 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
       (lds_v4i16*)((__attribute__((address_space(3))) char*)(p)));
   return __builtin_bit_cast(u32x2, r);
+}
+
+// The same transposed read as inline assembly. The compiler cannot tell which
+// LDS object the intrinsic above reads, so it waits for every outstanding
+// global->LDS load before it: on a tile whose successor is already in flight
+// that wait would stall the V^T P^T products until the next tile has landed.
+// The assembly form is not tracked by the compiler; its result is valid only
+// after lds_wait_tied has covered it.
+template <int OFF>
+__device__ __forceinline__ u32x2 lds_read_tr4_async(uint32_t lds_addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset field");
+  u32x2 r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(lds_addr), "n"(OFF));
+  return r;
+}
+
+template <int I, int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<I + 1, N>(f);
+  }
+}
+
+// Waits until at most N LDS operations of this wave are outstanding. LDS
+// operations complete in issue order, so this covers every read issued more
+// than N operations ago. x and y are tied to the wait so that their uses
+// cannot be scheduled above it.
+template <int N>
+__device__ __forceinline__ void lds_wait_tied(u32x2& x, u32x2& y) {
+  asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(x), "+v"(y) : "n"(N));
 }
 
 // two fp32 -> packed bf16 (round to nearest even), one v_cvt_pk_bf16_f32
@@ -218,22 +251,56 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
   // lane l writes chunk l % 16 of row 16w + 4j + l / 16 and so fetches the
   // data chunk that the swizzle stores there. Keys past N repeat key N - 1
   // (finite values; the causal mask removes them).
+  // DIRECT, whole tiles: per-lane byte offsets of the sources within a tile
+  // (K rows and V blocks as below), so that a tile costs one scalar base and
+  // eight loads; LDS destinations derive from the wave index kept in an SGPR
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  uint32_t koff[DIRECT ? 4 : 1], voff = 0;
+  if constexpr (DIRECT) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int row = wave * 16 + j * 4 + (lane >> 4);
+      koff[j] = static_cast<uint32_t>((row * stride + g * D + (((lane & 15) ^ (row & 15)) * 8)) * 2);
+    }
+    voff = static_cast<uint32_t>(((wave * 16 + ((lane >> 1) & 15)) * stride + g * D +
+                                  (2 * (lane >> 5) + (lane & 1)) * 8) * 2);
+  }
   auto issue_tile = [&](int t, auto buf_tag) {
     if constexpr (DIRECT) {
       auto& dst = decltype(buf_tag)::value ? sb1 : sb0;
+      if ((t + 1) * kKT <= N) {
+        const size_t tile0 = (static_cast<size_t>(b) * N + static_cast<size_t>(t) * kKT) * stride;
+        const char* kt = reinterpret_cast<const char*>(k + tile0);
+        const char* vt = reinterpret_cast<const char*>(v + tile0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(kt + koff[j]),
+                                           (__attribute__((address_space(3))) void*)(&dst.k[(wave_u * 16 + j * 4) * 128]),
+                                           16, 0, 0);
+          __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(vt + (voff + j * 64)),
+                                           (__attribute__((address_space(3))) void*)(&dst.v[(wave_u * 4 + j) * 512]),
+                                           16, 0, 0);
+        }
+        return;
+      }
+      // the last, partial tile: keys past N repeat key N - 1
       const int ch = lane & 15;
+      // V: instruction j of wave w writes blocks (w, 2j) and (w, 2j + 1):
+      // lane l carries key 16w + (l / 2) % 16, 16-byte chunk 4j + 2 (l / 32) + l % 2
+      const int vkey = min(t * kKT + wave * 16 + ((lane >> 1) & 15), N - 1);
+      const uint16_t* vr = v + (static_cast<size_t>(b) * N + vkey) * stride + static_cast<size_t>(g) * D +
+                           (2 * (lane >> 5) + (lane & 1)) * 8;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int row = wave * 16 + j * 4 + (lane >> 4);
         const int key = min(t * kKT + row, N - 1);
         const uint16_t* kr = k + (static_cast<size_t>(b) * N + key) * stride + static_cast<size_t>(g) * D;
-        const uint16_t* vr = v + (static_cast<size_t>(b) * N + key) * stride + static_cast<size_t>(g) * D;
         __builtin_amdgcn_global_load_lds(
             (const __attribute__((address_space(1))) void*)(kr + ((ch ^ (row & 15)) * 8)),
             (__attribute__((address_space(3))) void*)(&dst.k[(wave * 16 + j * 4) * 128]), 16, 0, 0);
         __builtin_amdgcn_global_load_lds(
-            (const __attribute__((address_space(1))) void*)(vr + ((ch ^ (2 * (row & 3))) * 8)),
-            (__attribute__((address_space(3))) void*)(&dst.v[(wave * 16 + j * 4) * 128]), 16, 0, 0);
+            (const __attribute__((address_space(1))) void*)(vr + j * 32),
+            (__attribute__((address_space(3))) void*)(&dst.v[(wave * 4 + j) * 512]), 16, 0, 0);
       }
     }
   };
@@ -346,10 +413,15 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
   };
   auto vtr = [&](auto buf_tag, int row, int col) -> const uint16_t* {
     constexpr int BUF = decltype(buf_tag)::value;
-    if constexpr (DIRECT)
-      return &(BUF ? sb1 : sb0).v[row * 128 + (((col >> 3) ^ (2 * (row & 3))) * 8) + (col & 7)];
+    if constexpr (DIRECT) return nullptr;   // DIRECT reads V through vbase below
     else return &sm.v[BUF][row][col];
   };
+  // DIRECT: LDS byte address of this lane's 8 bytes in the first V block
+  uint32_t vbase[2] = {0u, 0u};
+  if constexpr (DIRECT) {
+    vbase[0] = (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) uint16_t*)(&sb0.v[0])) + 8 * lane;
+    vbase[1] = (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) uint16_t*)(&sb1.v[0])) + 8 * lane;
+  }
   using Buf0 = std::integral_constant<int, 0>;
   using Buf1 = std::integral_constant<int, 1>;
 
@@ -461,16 +533,44 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
     // keys kc*32 + q4*4 + {0..3} and kc*32 + 16 + q4*4 + {0..3}: the key
     // order of the P^T operand above.
     __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-    for (int kc = 0; kc < 2; ++kc)
-#pragma unroll
-      for (int db = 0; db < DB; ++db) {
-        const u32x2 lo = lds_read_tr4(vtr(buf_tag, kc * 32 + tr_row, db * 16 + tr_col));
-        const u32x2 hi = lds_read_tr4(vtr(buf_tag, kc * 32 + 16 + tr_row, db * 16 + tr_col));
-        const bf16x8 a = __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
+    if constexpr (DIRECT) {
+      // 16 groups (kc, db) of two reads; three groups in flight ahead of the
+      // one being multiplied
+      // keys kc*32 + q4*4 + {0..3} (lo) and kc*32 + 16 + q4*4 + {0..3} (hi)
+      // of dims db*16 .. db*16 + 15 are blocks (2 kc, db) and (2 kc + 1, db)
+      constexpr int NG = 2 * DB;
+      constexpr int AHEAD = 3;
+      const uint32_t vb = vbase[cur];
+      u32x2 lo[NG], hi[NG];
+      auto rd = [&](auto G) {
+        constexpr int gi = decltype(G)::value;
+        constexpr int kc = gi / DB, db = gi % DB;
+        lo[gi] = lds_read_tr4_async<(2 * kc) * 4096 + db * 512>(vb);
+        hi[gi] = lds_read_tr4_async<(2 * kc + 1) * 4096 + db * 512>(vb);
+      };
+      static_for<0, AHEAD + 1>(rd);
+      static_for<0, NG>([&](auto G) {
+        constexpr int gi = decltype(G)::value;
+        constexpr int later = (NG - 1 - gi) < AHEAD ? (NG - 1 - gi) : AHEAD;   // groups issued after
+        lds_wait_tied<2 * later>(lo[gi], hi[gi]);
+        constexpr int kc = gi / DB, db = gi % DB;
+        const bf16x8 a = __builtin_bit_cast(bf16x8, u32x4{lo[gi][0], lo[gi][1], hi[gi][0], hi[gi][1]});
         o[db][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][0], o[db][0], 0, 0, 0);
         o[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][1], o[db][1], 0, 0, 0);
-      }
+        if constexpr (gi + AHEAD + 1 < NG) rd(std::integral_constant<int, gi + AHEAD + 1>{});
+      });
+    } else {
+#pragma unroll
+      for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          const u32x2 lo = lds_read_tr4(vtr(buf_tag, kc * 32 + tr_row, db * 16 + tr_col));
+          const u32x2 hi = lds_read_tr4(vtr(buf_tag, kc * 32 + 16 + tr_row, db * 16 + tr_col));
+          const bf16x8 a = __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
+          o[db][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][0], o[db][0], 0, 0, 0);
+          o[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][1], o[db][1], 0, 0, 0);
+        }
+    }
 #pragma unroll
     for (int kc = 0; kc < 2; ++kc) {
       l_acc[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[kc][0], l_acc[0], 0, 0, 0);

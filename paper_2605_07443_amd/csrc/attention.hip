@@ -6,7 +6,9 @@
 // bf16 path (matrix cores, gfx950 v_mfma_f32_16x16x32_bf16):
 //   * A workgroup owns M = 128 query vectors of one (request, KV head): BR
 //     consecutive selected rows x the G = Hq/Hkv query heads that share the KV
-//     head, so one K/V stream feeds all of them.
+//     head, so one K/V stream feeds all of them. When BR does not divide the
+//     row count, the short tile is the first (lowest positions, fewest keys)
+//     rather than the last (the longest).
 //   * Each of the 4 waves owns 32 query vectors and computes S^T = K Q^T for a
 //     64-key tile (keys on the MFMA rows, queries on its columns) with Q held
 //     in registers and K read from LDS. In the output layout a lane then holds
@@ -145,7 +147,7 @@ constexpr float kLazy = 8.f;
 template <int D, bool SELECTIVE, bool LSE, bool PAGED>
 __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict__ rows, int R,
-                      int N, int Hq, int Hkv, int G, int BR, const uint16_t* __restrict__ k,
+                      int N, int Hq, int Hkv, int G, int BR, int shift, const uint16_t* __restrict__ k,
                       const uint16_t* __restrict__ v, float scale_log2e,
                       uint16_t* __restrict__ out, float* __restrict__ lse, int n_tiles,
                       int n_groups, int gpx, int chunk, PoolArgs pools,
@@ -193,8 +195,8 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
     const int m = wave * 32 + nb * 16 + c16;
     const int hh = m / BR;
     const int rl = m - hh * BR;
-    const int r = tile * BR + rl;
-    valid[nb] = hh < G && r < R;
+    const int r = tile * BR + rl - shift;
+    valid[nb] = hh < G && r >= 0 && r < R;
     int p = 0;
     if (valid[nb]) {
       p = SELECTIVE ? rows[static_cast<size_t>(b) * R + r] : r;
@@ -741,7 +743,7 @@ int attention_impl(const rc_shape* shape, const void* q, const int32_t* rows, in
     const Paged& pg = paged ? *paged : none;
     auto launch = [&](auto kern) {
       hipLaunchKernelGGL(kern, grid, dim3(kAttnThreads), 0, stream,
-                         static_cast<const uint16_t*>(q), rows, R, N, Hq, Hkv, G, BR,
+                         static_cast<const uint16_t*>(q), rows, R, N, Hq, Hkv, G, BR, n_tiles * BR - R,
                          static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
                          scale_log2e, static_cast<uint16_t*>(out), lse, n_tiles, n_groups, gpx,
                          chunk, pg.pools, pg.segs, pg.S, pg.cos_t, pg.sin_t, pg.max_pos);

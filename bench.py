@@ -384,7 +384,7 @@ def main():
         reps = max(3, min(10, args.steps // 10))
         g_dev = timeit(gather(dev_pools), reps * 3)
         g_host = timeit(gather(host_pools), reps * 3)
-        g_host32 = timeit(gather(host_pools, 32), reps * 3)
+        g_host_b = timeit(gather(host_pools, ops.OVERLAP_GATHER_WORKGROUPS), reps * 3)
         e_dev = timeit(eq3_path(dev_pools, None), reps)
         e_seq = timeit(eq3_path(host_pools, None), reps)
         e_ovl = timeit(eq3_path(host_pools, side), reps)
@@ -392,7 +392,8 @@ def main():
         host = {"n_protos": 65536, "history_bytes_from_host": pcie_bytes,
                 "gather_device_pool_us": round(g_dev * 1e3, 2),
                 "gather_host_pool_us": round(g_host * 1e3, 2),
-                "gather_host_pool_32_workgroups_us": round(g_host32 * 1e3, 2),
+                "gather_host_pool_bounded_us": round(g_host_b * 1e3, 2),
+                "gather_bounded_workgroups": ops.OVERLAP_GATHER_WORKGROUPS,
                 "host_read_GBps": round(pcie_bytes / ((g_host - g_dev) * 1e-3) / 1e9, 1)
                 if g_host > g_dev else None,
                 "eq3_device_pool_ms": round(e_dev, 4),

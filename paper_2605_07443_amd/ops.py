@@ -450,10 +450,16 @@ def paged_prefill(q, k_fresh, v_fresh, pools, segs: Segments, k: int, cos, sin, 
     return bufs
 
 
+# Workgroups of a gather that overlaps the first layer: few enough to leave the
+# compute units to the first layer while the gather waits on PCIe (measured
+# best of 24..128 on the 3,008- and 2,080-position workloads).
+OVERLAP_GATHER_WORKGROUPS = 64
+
+
 def eq3_select_tokens_path(q, k_fresh, v_fresh, pools, token_map, status: Segments, item_mask: int,
                            lam: float, k_hist: int, k_item: int, cos, sin, scale=None,
                            bufs: Eq3Buffers | None = None, gather_stream=None,
-                           gather_workgroups: int = 32):
+                           gather_workgroups: int = OVERLAP_GATHER_WORKGROUPS):
     """Eq. (3) selection with token-granular sources (pool rows possibly in
     pinned host memory). With gather_stream, the gather runs there, overlapping
     the first layer in full (attention with log-sum-exp, attention mass) on the

@@ -251,6 +251,31 @@ def main():
                 "selective_speedup": round(fms / ms_per_step, 3)}
         del fout
 
+    # ---- standalone re-alignment (rc_rerope) of the reused rows of one batch,
+    # in place on a copy of its assembled K: delta = dst_start on pool rows
+    rerope = None
+    w0, _, bufs0 = batches[0]
+    delta = torch.zeros((B, N), dtype=torch.int32)
+    for b in range(B):
+        for dst, ln, pool, _blk in w0.segs[b].tolist():
+            if pool >= 0:
+                delta[b, dst:dst + ln] = dst
+    n_reused = int((delta != 0).sum())
+    delta = delta.to(dev)
+    kk = bufs0.k_asm.clone()
+    reps = max(5, min(50, args.steps // 2))
+    ops.rerope(kk, delta, cos, sin)
+    torch.cuda.synchronize()
+    r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    r0.record(stream)
+    for _ in range(reps):
+        ops.rerope(kk, delta, cos, sin)
+    r1.record(stream)
+    torch.cuda.synchronize()
+    r_ms = r0.elapsed_time(r1) / reps
+    rerope = dict(us=round(r_ms * 1e3, 2), reused_rows=n_reused, **hbm(2.0 * n_reused * row, r_ms))
+    del kk, delta
+
     # ---- zero-copy variant: score-only alignment pass, top-k, paged attention
     paged = None
     if not args.no_paged and cfg.dtype == "bf16" and R > 0:
@@ -516,6 +541,7 @@ def main():
         "roofline": roofline,
         "kernels": kernels,
         "full_prefill": full,
+        "rerope_standalone": rerope,
         "paged_prefill": paged,
         "eq3_selection": eq3,
         "token_history_host_pool": host,

@@ -128,6 +128,16 @@ __device__ __forceinline__ void lds_wait_tied(u32x2& x, u32x2& y) {
   asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(x), "+v"(y) : "n"(N));
 }
 
+// Maximum over the four 16-lane rows of a wave for each lane position
+// (lanes l, l^16, l^32, l^48), with the gfx950 row-swap permutes on the vector
+// ALU instead of LDS-routed shuffles.
+__device__ __forceinline__ float max_over_rows(float m) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+  m = __builtin_elementwise_maximum(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+  return __builtin_elementwise_maximum(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
 // two fp32 -> packed bf16 (round to nearest even), one v_cvt_pk_bf16_f32
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
@@ -490,8 +500,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
             __builtin_elementwise_maximum(m, s[kb][nb][0]),
             __builtin_elementwise_maximum(__builtin_elementwise_maximum(s[kb][nb][1], s[kb][nb][2]),
                                           s[kb][nb][3]));
-      m = __builtin_elementwise_maximum(m, __shfl_xor(m, 16, 64));
-      mx[nb] = __builtin_elementwise_maximum(m, __shfl_xor(m, 32, 64));
+      mx[nb] = max_over_rows(m);
     }
     // a query sees key 0 in the first tile, so the reference max is finite after it
     if (__ballot(mx[0] * scale_log2e - m_run[0] * scale_log2e > kLazy ||

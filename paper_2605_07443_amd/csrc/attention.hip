@@ -63,16 +63,18 @@ struct AttnSmem {
 
 // D = 128, not paged: tiles land in LDS straight from global memory
 // (global_load_lds_dwordx4: each wave instruction writes 1 KB contiguously, 4
-// rows of 256 bytes), so rows cannot be padded; the 16-byte chunks of a row
-// are XOR-swizzled instead. K row r keeps data chunk c at chunk c ^ (r & 15):
-// the fragment reads of 16 consecutive rows then hit 16 distinct chunks. V
-// is stored as 16 x 16 blocks (16 keys x 16 dims, key-major, 512 bytes): block
-// (key / 16, dim / 16) at byte 4096 (key / 16) + 512 (dim / 16). A transposed
-// read then takes one whole block, lane l the 8 bytes at 8 l, so every V^T
-// operand is one base address plus a constant offset and no read conflicts.
-// The two buffers are separate objects so that the compiler can tell the
-// loads into one buffer from the reads of the other and does not wait for
-// the former before the latter.
+// whole rows of 256 bytes, the best-coalesced fetch), so rows cannot be
+// padded; the 16-byte chunks of a row are XOR-swizzled instead. K row r keeps
+// data chunk c at chunk c ^ (r % 16): a fragment read of 16 consecutive rows
+// hits 16 distinct chunks. V row r keeps data chunk c at chunk c ^ 2 (r % 8):
+// the transposed reads of one half-wave (8 consecutive rows, two adjacent
+// chunks) hit 16 distinct chunks. Every K and V read of the tile loop is
+// issued as assembly from a few precomputed per-lane addresses plus constant
+// offsets (tile row block, buffer), and the tile loads as assembly too: the
+// compiler sees none of them, so it inserts no waits between the loads in
+// flight and the reads of the other buffer (after LDS lowering both buffers
+// are offsets of one object, and it would drain every load before each
+// read); the kernel orders them itself with explicit waits and barriers.
 struct AttnBufDirect {
   uint16_t k[kKT * 128];
   uint16_t v[kKT * 128];
@@ -97,17 +99,33 @@ __device__ __forceinline__ u32x2 lds_read_tr4(const uint16_t* p) {
   return __builtin_bit_cast(u32x2, r);
 }
 
-// The same transposed read as inline assembly. The compiler cannot tell which
-// LDS object the intrinsic above reads, so it waits for every outstanding
-// global->LDS load before it: on a tile whose successor is already in flight
-// that wait would stall the V^T P^T products until the next tile has landed.
-// The assembly form is not tracked by the compiler; its result is valid only
-// after lds_wait_tied has covered it.
+// The same transposed read as inline assembly, at lds_addr + OFF bytes. The
+// compiler does not track it: its result is valid only after lds_wait_tied
+// has covered it.
 template <int OFF>
 __device__ __forceinline__ u32x2 lds_read_tr4_async(uint32_t lds_addr) {
   static_assert(OFF >= 0 && OFF < 65536, "ds offset field");
   u32x2 r;
   asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(lds_addr), "n"(OFF));
+  return r;
+}
+
+// One global->LDS load (16 bytes per lane, 1 KB per wave) from a wave-uniform
+// base plus a 32-bit per-lane byte offset into the LDS bytes at lds_addr
+// (wave-uniform). Issued as assembly: the compiler does not track it, so the
+// caller waits for it with an explicit vmcnt wait before the data is read.
+__device__ __forceinline__ void dma16(uint32_t lds_addr, const void* gbase, uint32_t goff) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds_addr), "v"(goff), "s"(gbase)
+               : "memory", "m0");
+}
+
+// A 16-byte LDS read at lds_addr + OFF bytes as assembly; valid after
+// lds_wait_tied has covered it.
+template <int OFF>
+__device__ __forceinline__ u32x4 lds_read_b128_async(uint32_t lds_addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset field");
+  u32x4 r;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(lds_addr), "n"(OFF));
   return r;
 }
 
@@ -126,6 +144,10 @@ __device__ __forceinline__ void static_for(F&& f) {
 template <int N>
 __device__ __forceinline__ void lds_wait_tied(u32x2& x, u32x2& y) {
   asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(x), "+v"(y) : "n"(N));
+}
+template <int N>
+__device__ __forceinline__ void lds_wait_tied(u32x4& x) {
+  asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(x) : "n"(N));
 }
 
 // Maximum over the four 16-lane rows of a wave for each lane position
@@ -170,7 +192,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
   constexpr int KSTEP = kAttnThreads / UPR;      // keys between a thread's units
   constexpr bool DIRECT = (D == 128) && !PAGED;
   __shared__ std::conditional_t<DIRECT, AttnNone, AttnSmem<D>> sm;
-  __shared__ std::conditional_t<DIRECT, AttnBufDirect, AttnNone> sb0, sb1;
+  __shared__ std::conditional_t<DIRECT, AttnBufDirect, AttnNone> sbuf[2];
   __shared__ int s_ext[4];
   __shared__ int4 s_psegs[PAGED ? kPagedMaxSegments : 1];
   __shared__ uint32_t s_sel[PAGED ? kMaxSelectN / 32 : 1];  // recomputed rows of the request
@@ -263,56 +285,49 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
   // lane l writes chunk l % 16 of row 16w + 4j + l / 16 and so fetches the
   // data chunk that the swizzle stores there. Keys past N repeat key N - 1
   // (finite values; the causal mask removes them).
-  // DIRECT, whole tiles: per-lane byte offsets of the sources within a tile
-  // (K rows and V blocks as below), so that a tile costs one scalar base and
-  // eight loads; LDS destinations derive from the wave index kept in an SGPR
+  // DIRECT, whole tiles: per-lane 32-bit byte offsets of the sources within a
+  // tile, so that a tile costs one scalar base and eight loads; LDS
+  // destinations derive from the wave index kept in an SGPR
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-  uint32_t koff[DIRECT ? 4 : 1], voff = 0;
+  uint32_t koff[DIRECT ? 4 : 1], voff[DIRECT ? 4 : 1];
   if constexpr (DIRECT) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int row = wave * 16 + j * 4 + (lane >> 4);
       koff[j] = static_cast<uint32_t>((row * stride + g * D + (((lane & 15) ^ (row & 15)) * 8)) * 2);
+      voff[j] = static_cast<uint32_t>((row * stride + g * D + (((lane & 15) ^ (2 * (row & 7))) * 8)) * 2);
     }
-    voff = static_cast<uint32_t>(((wave * 16 + ((lane >> 1) & 15)) * stride + g * D +
-                                  (2 * (lane >> 5) + (lane & 1)) * 8) * 2);
   }
   auto issue_tile = [&](int t, auto buf_tag) {
     if constexpr (DIRECT) {
-      auto& dst = decltype(buf_tag)::value ? sb1 : sb0;
+      auto& dst = sbuf[decltype(buf_tag)::value];
       if ((t + 1) * kKT <= N) {
         const size_t tile0 = (static_cast<size_t>(b) * N + static_cast<size_t>(t) * kKT) * stride;
         const char* kt = reinterpret_cast<const char*>(k + tile0);
         const char* vt = reinterpret_cast<const char*>(v + tile0);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(kt + koff[j]),
-                                           (__attribute__((address_space(3))) void*)(&dst.k[(wave_u * 16 + j * 4) * 128]),
-                                           16, 0, 0);
-          __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(vt + (voff + j * 64)),
-                                           (__attribute__((address_space(3))) void*)(&dst.v[(wave_u * 4 + j) * 512]),
-                                           16, 0, 0);
+          dma16((uint32_t)(uintptr_t)((__attribute__((address_space(3))) uint16_t*)(&dst.k[(wave_u * 16 + j * 4) * 128])),
+                kt, koff[j]);
+          dma16((uint32_t)(uintptr_t)((__attribute__((address_space(3))) uint16_t*)(&dst.v[(wave_u * 16 + j * 4) * 128])),
+                vt, voff[j]);
         }
         return;
       }
       // the last, partial tile: keys past N repeat key N - 1
       const int ch = lane & 15;
-      // V: instruction j of wave w writes blocks (w, 2j) and (w, 2j + 1):
-      // lane l carries key 16w + (l / 2) % 16, 16-byte chunk 4j + 2 (l / 32) + l % 2
-      const int vkey = min(t * kKT + wave * 16 + ((lane >> 1) & 15), N - 1);
-      const uint16_t* vr = v + (static_cast<size_t>(b) * N + vkey) * stride + static_cast<size_t>(g) * D +
-                           (2 * (lane >> 5) + (lane & 1)) * 8;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int row = wave * 16 + j * 4 + (lane >> 4);
         const int key = min(t * kKT + row, N - 1);
         const uint16_t* kr = k + (static_cast<size_t>(b) * N + key) * stride + static_cast<size_t>(g) * D;
+        const uint16_t* vr = v + (static_cast<size_t>(b) * N + key) * stride + static_cast<size_t>(g) * D;
         __builtin_amdgcn_global_load_lds(
             (const __attribute__((address_space(1))) void*)(kr + ((ch ^ (row & 15)) * 8)),
             (__attribute__((address_space(3))) void*)(&dst.k[(wave * 16 + j * 4) * 128]), 16, 0, 0);
         __builtin_amdgcn_global_load_lds(
-            (const __attribute__((address_space(1))) void*)(vr + j * 32),
-            (__attribute__((address_space(3))) void*)(&dst.v[(wave * 4 + j) * 512]), 16, 0, 0);
+            (const __attribute__((address_space(1))) void*)(vr + ((ch ^ (2 * (row & 7))) * 8)),
+            (__attribute__((address_space(3))) void*)(&dst.v[(wave * 16 + j * 4) * 128]), 16, 0, 0);
       }
     }
   };
@@ -420,20 +435,30 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
   // transposed V read (row, element col)
   auto kfrag = [&](auto buf_tag, int row, int u) -> const uint16_t* {
     constexpr int BUF = decltype(buf_tag)::value;
-    if constexpr (DIRECT) return &(BUF ? sb1 : sb0).k[row * 128 + ((u ^ (row & 15)) * 8)];
+    if constexpr (DIRECT) return nullptr;   // DIRECT reads K through kaddr below
     else return &sm.k[BUF][row][u * 8];
   };
   auto vtr = [&](auto buf_tag, int row, int col) -> const uint16_t* {
     constexpr int BUF = decltype(buf_tag)::value;
-    if constexpr (DIRECT) return nullptr;   // DIRECT reads V through vbase below
+    if constexpr (DIRECT) return nullptr;   // DIRECT reads V through vaddr below
     else return &sm.v[BUF][row][col];
   };
   // DIRECT: LDS byte address of this lane's 8 bytes in the first V block
-  uint32_t vbase[2] = {0u, 0u};
+  // DIRECT: LDS byte address of this lane's transposed V read of 16-dim block
+  // db in rows 4 q4 + c16/4 (+ a multiple of 16 rows, a constant offset)
+  uint32_t vaddr[DIRECT ? DB : 1], kaddr[DIRECT ? DC : 1];
   if constexpr (DIRECT) {
-    vbase[0] = (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) uint16_t*)(&sb0.v[0])) + 8 * lane;
-    vbase[1] = (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) uint16_t*)(&sb1.v[0])) + 8 * lane;
+    const uint32_t v0 = (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) uint16_t*)(&sbuf[0].v[0]));
+    const uint32_t k0 = (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) uint16_t*)(&sbuf[0].k[0]));
+    const int x = 4 * (q4 & 1) + (c16 >> 2);   // row % 8 of this lane's rows
+    const uint32_t lane_part = (4 * q4 + (c16 >> 2)) * 256 + (c16 & 1) * 8;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) vaddr[db] = v0 + lane_part + (2 * (db ^ x) + ((c16 >> 1) & 1)) * 16;
+    // K fragment (kb, dc): row kb*16 + c16, data chunk dc*4 + q4 at chunk (dc*4 + q4) ^ c16
+#pragma unroll
+    for (int dc = 0; dc < DC; ++dc) kaddr[dc] = k0 + c16 * 256 + (((dc * 4 + q4) ^ c16) * 16);
   }
+  constexpr uint32_t kBufBytes = sizeof(AttnBufDirect);
   using Buf0 = std::integral_constant<int, 0>;
   using Buf1 = std::integral_constant<int, 1>;
 
@@ -468,14 +493,37 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) s[kb][0] = s[kb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
     __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-    for (int dc = 0; dc < DC; ++dc)
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(kfrag(buf_tag, kb * 16 + c16, dc * 4 + q4)));
+    if constexpr (DIRECT) {
+      // fragments (dc, kb) in dc-major order, three reads ahead
+      constexpr int KG = DC * 4;
+      constexpr int KAHEAD = 3;
+      u32x4 kf[KG];
+      auto rdk = [&](auto G) {
+        constexpr int gi = decltype(G)::value;
+        constexpr int dc = gi / 4, kb = gi % 4;
+        kf[gi] = lds_read_b128_async<cur * kBufBytes + kb * 4096>(kaddr[dc]);
+      };
+      static_for<0, KAHEAD + 1>(rdk);
+      static_for<0, KG>([&](auto G) {
+        constexpr int gi = decltype(G)::value;
+        constexpr int later = (KG - 1 - gi) < KAHEAD ? (KG - 1 - gi) : KAHEAD;
+        lds_wait_tied<later>(kf[gi]);
+        constexpr int dc = gi / 4, kb = gi % 4;
+        const bf16x8 a = __builtin_bit_cast(bf16x8, kf[gi]);
         s[kb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[0][dc], s[kb][0], 0, 0, 0);
         s[kb][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[1][dc], s[kb][1], 0, 0, 0);
-      }
+        if constexpr (gi + KAHEAD + 1 < KG) rdk(std::integral_constant<int, gi + KAHEAD + 1>{});
+      });
+    } else {
+#pragma unroll
+      for (int dc = 0; dc < DC; ++dc)
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) {
+          const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(kfrag(buf_tag, kb * 16 + c16, dc * 4 + q4)));
+          s[kb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[0][dc], s[kb][0], 0, 0, 0);
+          s[kb][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[1][dc], s[kb][1], 0, 0, 0);
+        }
+    }
     __builtin_amdgcn_s_setprio(0);
 
     if (MASK) {
@@ -547,17 +595,16 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
     if constexpr (DIRECT) {
       // 16 groups (kc, db) of two reads; three groups in flight ahead of the
       // one being multiplied
-      // keys kc*32 + q4*4 + {0..3} (lo) and kc*32 + 16 + q4*4 + {0..3} (hi)
-      // of dims db*16 .. db*16 + 15 are blocks (2 kc, db) and (2 kc + 1, db)
+      // keys kc*32 + q4*4 + {0..3} (lo) and kc*32 + 16 + q4*4 + {0..3} (hi):
+      // rows 32 kc (+16) further than the lane's base rows
       constexpr int NG = 2 * DB;
       constexpr int AHEAD = 3;
-      const uint32_t vb = vbase[cur];
       u32x2 lo[NG], hi[NG];
       auto rd = [&](auto G) {
         constexpr int gi = decltype(G)::value;
         constexpr int kc = gi / DB, db = gi % DB;
-        lo[gi] = lds_read_tr4_async<(2 * kc) * 4096 + db * 512>(vb);
-        hi[gi] = lds_read_tr4_async<(2 * kc + 1) * 4096 + db * 512>(vb);
+        lo[gi] = lds_read_tr4_async<cur * kBufBytes + kc * 8192>(vaddr[db]);
+        hi[gi] = lds_read_tr4_async<cur * kBufBytes + kc * 8192 + 4096>(vaddr[db]);
       };
       static_for<0, AHEAD + 1>(rd);
       static_for<0, NG>([&](auto G) {

@@ -105,6 +105,27 @@ def test_attention_unsorted_rows_and_groups(Hq, Hkv, D):
     assert_attn_close(H(full), reff, "bf16", "full prefill")
 
 
+@pytest.mark.parametrize("N", [1, 17, 63, 64, 65, 127, 128, 129])
+@pytest.mark.parametrize("D", [64, 128])
+def test_attention_tile_boundary_lengths(N, D):
+    """Prompts shorter than, equal to and just past one 64-key tile and two:
+    the partial last tile, a single tile and a single key."""
+    B, Hq, Hkv = 2, 8, 2
+    g = torch.Generator(device="cpu").manual_seed(N * 10 + D)
+    q = torch.randn((B, N, Hq, D), generator=g).to(torch.bfloat16)
+    k = torch.randn((B, N, Hkv, D), generator=g).to(torch.bfloat16)
+    v = torch.randn((B, N, Hkv, D), generator=g).to(torch.bfloat16)
+    R = min(N, 5)
+    rows = torch.sort(torch.randint(0, N, (B, R), generator=g, dtype=torch.int32), dim=1).values
+    rows[:, -1] = N - 1
+    say(f"[attention boundary] N={N} D={D}")
+    out = ops.selective_attention(q.to(DEV), k.to(DEV), v.to(DEV), rows.to(DEV))
+    full = ops.full_prefill(q.to(DEV), k.to(DEV), v.to(DEV))
+    torch.cuda.synchronize()
+    assert_attn_close(H(out), O.attention(H(q), H(k), H(v), rows=rows.numpy()), "bf16", "selective")
+    assert_attn_close(H(full), O.attention(H(q), H(k), H(v)), "bf16", "full prefill")
+
+
 def test_attention_fp32_full_and_selected():
     B, N, Hq, Hkv, D = 2, 190, 8, 2, 128
     g = torch.Generator(device="cpu").manual_seed(3)

@@ -277,23 +277,33 @@ extern "C" int rc_gemm_bf16(int64_t M, int32_t n, int32_t k, const void* x, cons
                 static_cast<long long>(M), n, k);
   if (residual == y) return fail(RC_ERR_INVALID_ARG, "residual must not alias y");
   if (M == 0) return RC_OK;
+  const uint16_t* xs = static_cast<const uint16_t*>(x);
+  const uint16_t* rs = static_cast<const uint16_t*>(residual);
+  uint16_t* ys = static_cast<uint16_t*>(y);
   if (k % kGK == 0 && M >= kBM && n >= kBN) {
-    const int64_t tm = (M + kBM - 1) / kBM;
+    // whole 256-row tiles on the big kernel; a tail of fewer than 256 rows
+    // goes to the 128 x 128 kernel below (a partial big tile would cost as
+    // much as a full one and, with few tiles per CU, a whole extra round)
+    const int64_t M_main = (M / kBM) * kBM;
+    const int64_t tm = M_main / kBM;
     const int tn = (n + kBN - 1) / kBN;
     if (tm * tn > 0x7fffffff) return fail(RC_ERR_UNSUPPORTED, "grid too large");
     hipLaunchKernelGGL(gemm_bf16_big_kernel, dim3(static_cast<unsigned>(tm * tn)), dim3(kBThreads), 0,
-                       stream, static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w),
-                       static_cast<const uint16_t*>(residual), static_cast<uint16_t*>(y), M, n, k,
+                       stream, xs, static_cast<const uint16_t*>(w), rs, ys, M_main, n, k,
                        static_cast<int>(tm), tn);
-    return check_launch("rc_gemm_bf16");
+    if (int st = check_launch("rc_gemm_bf16")) return st;
+    if (M_main == M) return RC_OK;
+    xs += M_main * k;
+    if (rs) rs += M_main * n;
+    ys += M_main * n;
+    M -= M_main;
   }
   const int64_t tiles_m = (M + kGM - 1) / kGM;
   const int tiles_n = (n + kGN - 1) / kGN;
   const int64_t blocks = tiles_m * tiles_n;
   if (blocks > 0x7fffffff) return fail(RC_ERR_UNSUPPORTED, "grid too large");
   hipLaunchKernelGGL(gemm_bf16_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kGThreads), 0,
-                     stream, static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w),
-                     static_cast<const uint16_t*>(residual), static_cast<uint16_t*>(y), M, n, k,
+                     stream, xs, static_cast<const uint16_t*>(w), rs, ys, M, n, k,
                      static_cast<int>(tiles_m), tiles_n);
   return check_launch("rc_gemm_bf16");
 }

@@ -114,9 +114,15 @@ __device__ __forceinline__ u32x2 lds_read_tr4_async(uint32_t lds_addr) {
 // base plus a 32-bit per-lane byte offset into the LDS bytes at lds_addr
 // (wave-uniform). Issued as assembly: the compiler does not track it, so the
 // caller waits for it with an explicit vmcnt wait before the data is read.
+// M0 (the LDS destination) is restored afterwards: the compiler does not
+// expect an assembly statement to change it.
 __device__ __forceinline__ void dma16(uint32_t lds_addr, const void* gbase, uint32_t goff) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds_addr), "v"(goff), "s"(gbase)
-               : "memory", "m0");
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %2, %3\n\ts_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds_addr), "v"(goff), "s"(gbase)
+      : "memory");
 }
 
 // A 16-byte LDS read at lds_addr + OFF bytes as assembly; valid after

@@ -9,7 +9,9 @@
 //     head, so one K/V stream feeds all of them. When BR does not divide the
 //     row count, the short tile is the first (lowest positions, fewest keys)
 //     rather than the last (the longest).
-//   * Each of the 4 waves owns 32 query vectors and computes S^T = K Q^T for a
+//   * Each of the 4 waves owns 32 query vectors (consecutive rows, all G heads
+//     of each: its rows span the fewest positions, so its causal band is
+//     narrow and it skips the tiles past its last row) and computes S^T = K Q^T for a
 //     64-key tile (keys on the MFMA rows, queries on its columns) with Q held
 //     in registers and K read from LDS. In the output layout a lane then holds
 //     4 consecutive keys of one query column, which is also the B-operand
@@ -231,8 +233,8 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
 #pragma unroll
   for (int nb = 0; nb < 2; ++nb) {
     const int m = wave * 32 + nb * 16 + c16;
-    const int hh = m / BR;
-    const int rl = m - hh * BR;
+    const int rl = m / G;          // vector m: row m / G, head m % G
+    const int hh = m - rl * G;
     const int r = tile * BR + rl - shift;
     valid[nb] = hh < G && r >= 0 && r < R;
     int p = 0;
@@ -481,6 +483,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
 
   // first tile whose last key passes this wave's earliest row
   const int t_mask = min(n_kv, wave_pmin / kKT);
+  const int wave_last = pmax / kKT;   // tiles past it are masked for every row of this wave
 
   // One KV tile: S^T = K Q^T, (masked) online softmax, O^T += V^T P^T, then
   // stage the next tile. The causal mask is applied only on tiles reaching past
@@ -494,6 +497,8 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
       if (t + 1 < n_kv) issue_tile(t + 1, Next{});
     }
 
+    // a wave skips the tiles past all of its rows (their weights are zero)
+    if (t <= wave_last) {
     // ---- S^T for 64 keys x 32 queries (8 independent accumulators)
     f32x4 s[4][2];
 #pragma unroll
@@ -641,6 +646,8 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
       l_acc[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[kc][1], l_acc[1], 0, 0, 0);
     }
     __builtin_amdgcn_s_setprio(0);
+
+    }  // t <= wave_last
 
     // ---- stage the next tile into the other buffer, prefetch the one after
     if constexpr (DIRECT) {

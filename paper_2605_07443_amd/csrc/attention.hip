@@ -11,8 +11,8 @@
 //     rather than the last (the longest).
 //   * Each of the 4 waves owns 32 query vectors (consecutive rows, all G heads
 //     of each: its rows span the fewest positions, so its causal band is
-//     narrow and it skips the tiles past its last row) and computes S^T = K Q^T for a
-//     64-key tile (keys on the MFMA rows, queries on its columns) with Q held
+//     narrow and it skips the tiles past its last row) and computes
+//     S^T = K Q^T for a 64-key tile (keys on the MFMA rows, queries on its columns) with Q held
 //     in registers and K read from LDS. In the output layout a lane then holds
 //     4 consecutive keys of one query column, which is also the B-operand
 //     layout of the second product O^T = V^T P^T, so P never leaves registers;
@@ -22,7 +22,9 @@
 //     the running denominators are column sums of the bf16 P^T taken on the
 //     matrix cores (ones x P^T), consistent with the P used for O. K/V tiles
 //     are double-buffered in LDS (one barrier per tile) with the next tile's
-//     global loads in flight during compute.
+//     global loads in flight during compute. For D = 128 (not paged) the
+//     tiles go from HBM straight into LDS and every K/V read of the tile loop
+//     is issued as assembly (layouts and ordering at AttnBufDirect).
 //   * Workgroup ids are remapped so that all row tiles of one (request, KV
 //     head) run on the same XCD (ids are dealt round-robin over the 8 XCDs),
 //     sharing its L2 for the K/V stream. Each XCD starts its longest (latest)

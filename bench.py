@@ -64,11 +64,19 @@ def parse_args():
     return ap.parse_args()
 
 
+def code_text(text: str) -> str:
+    """A source file without comments and whitespace: edits to comments or
+    layout do not change the digest of the code they describe."""
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    return re.sub(r"\s+", "", text)
+
+
 def source_digest(*names) -> str:
     h = hashlib.sha256()
     for n in names:
-        with open(os.path.join(ROOT, "paper_2605_07443_amd", "csrc", n), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, "paper_2605_07443_amd", "csrc", n), encoding="utf-8") as f:
+            h.update(code_text(f.read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -5,10 +5,11 @@
 //   deviation_kernel  one wave per position: L1 distance between the fresh
 //                     and the assembled key row (HBM-bound, 16-byte loads,
 //                     wave reduction)
-//   topk_kernel       one 1024-thread workgroup per request: range-adaptive
-//                     radix select of the k-th largest score key in LDS
-//                     (11-bit digits), then a block scan that emits the fresh
-//                     and selected positions in ascending order
+//   topk_kernel       one workgroup per request, keys held in registers:
+//                     range-adaptive radix select of the k-th largest score
+//                     key (11-bit digits, LDS histograms), then the fresh and
+//                     selected positions written in ascending order from
+//                     per-wave counts
 //   patch_kernel      copies the fresh K/V rows of the selected cached
 //                     positions over the assembled rows
 #include "rc_common.h"
@@ -58,11 +59,12 @@ __global__ __launch_bounds__(64 * kDevWaves) void deviation_kernel(
 
 // ---------------------------------------------------------------------- top-k
 
-constexpr int kTopkThreads = 1024;
-constexpr int kTopkWaves = kTopkThreads / 64;
-constexpr int kBins = 2048;  // 11-bit digits
+constexpr int kTopkMaxPer = 16;  // positions per thread at most
+constexpr int kBins = 2048;                           // 11-bit digits
 constexpr int kDigitBits = 11;
-constexpr int kBinsPerThread = kBins / kTopkThreads;
+constexpr int kCoarse = 64;                           // coarse bins of 32 digits
+static_assert(kBins == 32 * kCoarse, "top-k bin layout");
+static_assert(kMaxSelectN <= 1024 * kTopkMaxPer, "top-k positions per thread");
 
 // Total order on fp32: larger key = larger value; +NaN above +inf.
 __device__ __forceinline__ uint32_t score_key(float f) {
@@ -70,34 +72,39 @@ __device__ __forceinline__ uint32_t score_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// Inclusive block scan of one int per thread (1024 threads); also returns
-// the block total. `warp_tot` is LDS scratch of kTopkWaves ints.
-__device__ __forceinline__ int block_inclusive_scan(int x, int* warp_tot, int& total) {
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const int y = __shfl_up(x, off, 64);
-    if (lane >= off) x += y;
-  }
-  if (lane == 63) warp_tot[wave] = x;
-  __syncthreads();
-  int before = 0;
-  total = 0;
-#pragma unroll
-  for (int w = 0; w < kTopkWaves; ++w) {
-    const int v = warp_tot[w];
-    before += (w < wave) ? v : 0;
-    total += v;
-  }
-  __syncthreads();
-  return x + before;
+// Inclusive scan over the lanes of a wave in lane order: shifts within each
+// row of 16 lanes (DPP row_shr), then the row totals carried across rows.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
+  x += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x111, 0xf, 0xf, false));
+  x += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x112, 0xf, 0xf, false));
+  x += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x114, 0xf, 0xf, false));
+  x += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x118, 0xf, 0xf, false));
+  const uint32_t r0 = __builtin_amdgcn_readlane(x, 15);
+  const uint32_t r1 = __builtin_amdgcn_readlane(x, 31);
+  const uint32_t r2 = __builtin_amdgcn_readlane(x, 47);
+  const int row = (threadIdx.x & 63) >> 4;
+  return x + (row >= 1 ? r0 : 0u) + (row >= 2 ? r1 : 0u) + (row >= 3 ? r2 : 0u);
 }
 
-__device__ __forceinline__ int block_sum(int x, int* warp_tot) {
-  int total;
-  block_inclusive_scan(x, warp_tot, total);
-  return total;
+// Minimum / maximum over the wave, in every lane: quad and row rotations
+// (DPP), then the gfx950 row swaps across the four rows.
+template <bool MAX>
+__device__ __forceinline__ uint32_t wave_extreme(uint32_t x) {
+  auto pick = [](uint32_t a, uint32_t b) { return MAX ? max(a, b) : min(a, b); };
+  x = pick(x, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0xb1, 0xf, 0xf, false)));
+  x = pick(x, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x4e, 0xf, 0xf, false)));
+  x = pick(x, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x124, 0xf, 0xf, false)));
+  x = pick(x, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x128, 0xf, 0xf, false)));
+  const auto a = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  x = pick(a[0], a[1]);
+  const auto c = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+  return pick(c[0], c[1]);
+}
+
+// Set lanes of `mask` below this lane.
+__device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
+  return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
+                                    __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
 }
 
 // One workgroup per request. Candidates are positions outside fresh
@@ -107,176 +114,259 @@ __device__ __forceinline__ int block_sum(int x, int* warp_tot) {
 // score_key(score[i]), order (key desc, i asc). Fresh positions are always
 // taken; the taken positions are written in ascending order. NC: number of
 // classes with a budget (1: class 0 only, k1 is 0).
-template <int NC>
-__global__ __launch_bounds__(kTopkThreads) void topk_kernel(
+//
+// Thread t of TPB holds positions j * TPB + t (j < NJ, TPB NJ >= N) in
+// registers, so that (j, wave, lane) runs in position order; every loop over
+// j is unrolled and its memory reads are issued together. The whole request
+// runs on one compute unit, where vector-ALU issue is the limit: NJ follows
+// N closely so that few slots are padding. (256 threads, one wave per SIMD,
+// were slower: latencies are then exposed.) The k-th largest key of a class is
+// found by a range-adaptive radix select: each pass histograms the keys in
+// [lo, hi] on 11-bit digits (plus a 64-bin coarse histogram), one wave finds
+// the boundary digit by two lane scans, and [lo, hi] narrows to it. The
+// histograms rotate over three LDS buffers, so that a pass costs two
+// barriers. The output is written from per-(j, wave) counts with one
+// barrier: each lane's slot is the count of taken positions before it.
+template <int NC, int NJ, int TPB>
+__global__ __launch_bounds__(TPB) void topk_kernel(
     const float* __restrict__ scores, const int4* __restrict__ segs, int S, int N,
     uint32_t item_mask, int k0, int k1, int R, int32_t* __restrict__ rows) {
-  __shared__ uint32_t s_key[kMaxSelectN];
-  __shared__ uint8_t s_cls[kMaxSelectN];  // 0 fresh, 1 + class for candidates; bit 7 = taken
   __shared__ int4 s_segs[kMaxSegments];
-  __shared__ int s_hist[kBins];
-  __shared__ int s_wt[kTopkWaves];
-  __shared__ uint32_t s_bounds[NC][4];
+  __shared__ uint32_t s_hist[3][kBins];
+  __shared__ uint32_t s_coarse[3][kCoarse];
+  constexpr int W = TPB / 64;                           // waves
+  static_assert(W % 4 == 0 && NJ * W <= 256 && NJ <= kTopkMaxPer, "top-k shape");
+  __shared__ uint32_t s_cnt[2][NJ * W];                  // per (j, wave): taken | ties << 16; ties of class 1
+  __shared__ uint32_t s_bounds[2][3];                   // per class: min key, max key, candidates
+  __shared__ uint32_t s_sel[2];                         // boundary digit, keys above it
 
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
-  for (int s = tid; s < S; s += kTopkThreads) s_segs[s] = segs[static_cast<size_t>(b) * S + s];
-  if (tid < NC) {
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+  // scores first: their latency overlaps the segment table's
+  float sc[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+    sc[j] = scores[static_cast<size_t>(b) * N + min(j * TPB + tid, N - 1)];
+  {
+    constexpr int SP = kMaxSegments / TPB;
+    int4 sv[SP];
+#pragma unroll
+    for (int q = 0; q < SP; ++q) sv[q] = segs[static_cast<size_t>(b) * S + min(q * TPB + tid, S - 1)];
+#pragma unroll
+    for (int q = 0; q < SP; ++q)
+      if (q * TPB + tid < S) s_segs[q * TPB + tid] = sv[q];
+  }
+#pragma unroll
+  for (int q = 0; q < kBins / TPB; ++q) {
+    s_hist[0][q * TPB + tid] = 0u;
+    s_hist[1][q * TPB + tid] = 0u;
+  }
+  if (tid < kCoarse) {
+    s_coarse[0][tid] = 0u;
+    s_coarse[1][tid] = 0u;
+  }
+  if (tid < 2) {
     s_bounds[tid][0] = 0xffffffffu;
     s_bounds[tid][1] = 0u;
+    s_bounds[tid][2] = 0u;
   }
   __syncthreads();
 
-  uint32_t kmin[2] = {0xffffffffu, 0xffffffffu}, kmax[2] = {0u, 0u};
-  int ncand[2] = {0, 0};
-  for (int i = tid; i < N; i += kTopkThreads) {
-    const int s = find_segment(s_segs, S, i);
-    const int pool = s >= 0 ? s_segs[s].z : -1;
-    const int cls = pool < 0 ? 0 : 1 + static_cast<int>(pool < 32 && ((item_mask >> pool) & 1u));
-    const uint32_t key = score_key(scores[static_cast<size_t>(b) * N + i]);
-    s_key[i] = key;
-    s_cls[i] = static_cast<uint8_t>(cls);
+  // class of each position, 2 bits per j: 0 fresh, 1 + c for a candidate of
+  // class c, 3 beyond N. The segment of a position is found by a binary
+  // search with a uniform step count, the searches of all j side by side.
+  int top = 1;  // smallest power of two >= S
+  while (top < S) top <<= 1;
+  int seg[NJ];
 #pragma unroll
-    for (int c = 0; c < NC; ++c)
-      if (cls == c + 1) {
-        kmin[c] = min(kmin[c], key);
-        kmax[c] = max(kmax[c], key);
-        ++ncand[c];
+  for (int j = 0; j < NJ; ++j) seg[j] = 0;
+  for (int step = top >> 1; step > 0; step >>= 1) {
+    int x[NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) x[j] = s_segs[min(seg[j] + step, S - 1)].x;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      if (seg[j] + step < S && x[j] <= j * TPB + tid) seg[j] += step;
+  }
+  int4 sg[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) sg[j] = s_segs[seg[j]];
+  uint32_t key[NJ];
+  uint32_t cls = 0u;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int i = j * TPB + tid;
+    key[j] = i < N ? score_key(sc[j]) : 0u;
+    const bool inside = sg[j].x <= i && i < sg[j].x + sg[j].y;
+    const int pool = inside ? sg[j].z : -1;
+    const uint32_t c = i >= N     ? 3u
+                       : pool < 0 ? 0u
+                                  : 1u + static_cast<uint32_t>(pool < 32 && ((item_mask >> pool) & 1u));
+    cls |= c << (2 * j);
+  }
+
+  // per class: smallest and largest key, number of candidates
+  {
+    uint32_t kmin[2] = {0xffffffffu, 0xffffffffu}, kmax[2] = {0u, 0u};
+    uint32_t ncand[2] = {0u, 0u};
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        const bool is = ((cls >> (2 * j)) & 3u) == static_cast<uint32_t>(c + 1);
+        if (is) {
+          kmin[c] = min(kmin[c], key[j]);
+          kmax[c] = max(kmax[c], key[j]);
+        }
+        ncand[c] += __popcll(__ballot(is));
       }
-  }
-  // block reductions of min/max/count per class
-#pragma unroll
-  for (int c = 0; c < NC; ++c) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-      kmin[c] = min(kmin[c], static_cast<uint32_t>(__shfl_xor(static_cast<int>(kmin[c]), off, 64)));
-      kmax[c] = max(kmax[c], static_cast<uint32_t>(__shfl_xor(static_cast<int>(kmax[c]), off, 64)));
     }
-    if ((tid & 63) == 0) {
-      atomicMin(&s_bounds[c][0], kmin[c]);
-      atomicMax(&s_bounds[c][1], kmax[c]);
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      kmin[c] = wave_extreme<false>(kmin[c]);
+      kmax[c] = wave_extreme<true>(kmax[c]);
+      if (lane == 0) {
+        atomicMin(&s_bounds[c][0], kmin[c]);
+        atomicMax(&s_bounds[c][1], kmax[c]);
+        atomicAdd(&s_bounds[c][2], ncand[c]);
+      }
     }
   }
+  __syncthreads();
+
   const int kc_arg[2] = {k0, k1};
   int kk[2] = {0, 0};
   uint32_t T[2] = {0u, 0u};
   int need[2] = {0, 0};
+  int pass = 0;
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
     if (kc_arg[c] <= 0) continue;  // uniform: kernel arguments
-    const int nc = block_sum(ncand[c], s_wt);  // contains barriers
-    kk[c] = min(kc_arg[c], nc);
+    kk[c] = min(kc_arg[c], static_cast<int>(s_bounds[c][2]));
     if (kk[c] == 0) continue;
-    // ---- threshold key T_c: the kk-th largest key of class c
     uint32_t lo = s_bounds[c][0], hi = s_bounds[c][1];
-    int nd = kk[c];  // how many of the class's keys in [lo, hi] we still take
-    const uint8_t want = static_cast<uint8_t>(c + 1);
+    int nd = kk[c];  // how many of the class's keys in [lo, hi] are still to take (>= 1)
+    const uint32_t want = static_cast<uint32_t>(c + 1);
     while (lo != hi) {
       const uint32_t range = hi - lo;
       const int bits = 32 - __clz(range);
       const int shift = bits > kDigitBits ? bits - kDigitBits : 0;
-      for (int j = tid; j < kBins; j += kTopkThreads) s_hist[j] = 0;
-      __syncthreads();
-      for (int i = tid; i < N; i += kTopkThreads) {
-        const uint32_t key = s_key[i];
-        if (s_cls[i] == want && key >= lo && key <= hi) atomicAdd(&s_hist[(key - lo) >> shift], 1);
-      }
-      __syncthreads();
-      // suffix sums from the top bin: thread t owns kBinsPerThread adjacent
-      // bins, threads ordered from the highest bins down
-      const int top = kBins - 1 - kBinsPerThread * tid;
-      int cnt[kBinsPerThread];
-      int mine = 0;
+      uint32_t* hist = s_hist[pass % 3];
+      uint32_t* coarse = s_coarse[pass % 3];
 #pragma unroll
-      for (int j = 0; j < kBinsPerThread; ++j) {
-        cnt[j] = s_hist[top - j];
-        mine += cnt[j];
-      }
-      int total;
-      int run = block_inclusive_scan(mine, s_wt, total) - mine;  // count in bins above `top`
-      // the bin where the running count first reaches `nd`
-      if (run < nd && run + mine >= nd) {
-#pragma unroll
-        for (int j = 0; j < kBinsPerThread; ++j) {
-          if (run < nd && run + cnt[j] >= nd) {
-            s_bounds[c][2] = static_cast<uint32_t>(top - j);
-            s_bounds[c][3] = static_cast<uint32_t>(run);
-          }
-          run += cnt[j];
+      for (int j = 0; j < NJ; ++j) {
+        if (((cls >> (2 * j)) & 3u) == want && key[j] >= lo && key[j] <= hi) {
+          const uint32_t d = (key[j] - lo) >> shift;
+          atomicAdd(&hist[d], 1u);
+          atomicAdd(&coarse[d >> 5], 1u);
         }
       }
       __syncthreads();
-      const uint32_t bin = s_bounds[c][2];
-      nd -= static_cast<int>(s_bounds[c][3]);
-      const uint32_t nlo = lo + (bin << shift);
-      const uint32_t width_m1 = (shift >= 32) ? 0xffffffffu : ((1u << shift) - 1u);
-      const uint32_t nhi = (hi - nlo > width_m1) ? nlo + width_m1 : hi;
-      lo = nlo;
-      hi = nhi;
+      // the buffers of pass + 2 were last read in pass - 1, before the
+      // barrier above, and are next written after the barrier below
+#pragma unroll
+      for (int q = 0; q < kBins / TPB; ++q) s_hist[(pass + 2) % 3][q * TPB + tid] = 0u;
+      if (tid < kCoarse) s_coarse[(pass + 2) % 3][tid] = 0u;
+      if (wave == 0) {
+        // lane l: coarse bin 63 - l, so the lane scan counts from the top
+        const uint32_t mc = coarse[kCoarse - 1 - lane];
+        const uint32_t ic = wave_incl_scan(mc);
+        const int lc = __builtin_ctzll(__ballot(ic >= static_cast<uint32_t>(nd) || lane == 63));
+        const uint32_t above_c = __builtin_amdgcn_readlane(ic - mc, lc);
+        const int cb = kCoarse - 1 - lc;
+        // lanes 0..31: the digits of coarse bin cb, from its top
+        const uint32_t mf = lane < 32 ? hist[cb * 32 + 31 - lane] : 0u;
+        const uint32_t inf = wave_incl_scan(mf);
+        const uint32_t rest = static_cast<uint32_t>(nd) - above_c;
+        const int lf = __builtin_ctzll(__ballot(inf >= rest || lane == 31));
+        const uint32_t above_f = __builtin_amdgcn_readlane(inf - mf, lf);
+        if (lane == 0) {
+          s_sel[0] = static_cast<uint32_t>(cb * 32 + 31 - lf);
+          s_sel[1] = above_c + above_f;
+        }
+      }
       __syncthreads();
+      const uint32_t bin = s_sel[0];
+      nd -= static_cast<int>(s_sel[1]);
+      const uint32_t nlo = lo + (bin << shift);
+      const uint32_t width_m1 = (1u << shift) - 1u;  // shift <= 21
+      hi = (hi - nlo > width_m1) ? nlo + width_m1 : hi;
+      lo = nlo;
+      ++pass;
     }
     T[c] = lo;
     need[c] = nd;  // candidates of class c with key == T_c to take, lowest positions first
   }
 
-  __syncthreads();  // s_key / s_cls complete even when no class ran a selection
-
   // ---- emit rows: fresh positions, keys > T_c, and the first need_c ties
-  const int per = (N + kTopkThreads - 1) / kTopkThreads;
-  const int beg = min(N, tid * per), end = min(N, beg + per);
-  int ties = 0;  // class-0 ties in the low 16 bits, class-1 ties in the high 16
-  for (int i = beg; i < end; ++i) {
-    const int cls = s_cls[i];
-    if (cls == 1 && kk[0] > 0 && s_key[i] == T[0]) ties += 1;
-    if (NC == 2 && cls == 2 && kk[1] > 0 && s_key[i] == T[1]) ties += 1 << 16;
-  }
-  int tot;
-  const int tb = block_inclusive_scan(ties, s_wt, tot) - ties;
-  int tb0 = tb & 0xffff, tb1 = tb >> 16;  // ties of each class before this thread
-  int take = 0;
-  for (int i = beg; i < end; ++i) {
-    const int cls = s_cls[i];
-    bool t;
-    if (cls == 0) {
-      t = true;
-    } else if (NC == 1 && cls == 2) {
-      t = false;  // class 1 has no budget
-    } else {
-      const bool one = NC == 2 && cls == 2;
-      const int kkc = one ? kk[1] : kk[0];
-      const uint32_t Tc = one ? T[1] : T[0];
-      const int ndc = one ? need[1] : need[0];
-      const uint32_t key = s_key[i];
-      if (kkc == 0) {
-        t = false;
-      } else if (key > Tc) {
-        t = true;
-      } else if (key == Tc) {
-        if (one) {
-          t = tb1 < ndc;
-          ++tb1;
-        } else {
-          t = tb0 < ndc;
-          ++tb0;
-        }
-      } else {
-        t = false;
-      }
+  // per j: taken outright (gt), tie at the threshold of class 0 / 1 (e0, e1)
+  uint32_t fgt = 0u, fe0 = 0u, fe1 = 0u;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const uint32_t c = (cls >> (2 * j)) & 3u;
+    const bool gt = c == 0u || (c == 1u && kk[0] > 0 && key[j] > T[0]) ||
+                    (NC == 2 && c == 2u && kk[1] > 0 && key[j] > T[1]);
+    const bool e0 = c == 1u && kk[0] > 0 && key[j] == T[0];
+    const bool e1 = NC == 2 && c == 2u && kk[1] > 0 && key[j] == T[1];
+    fgt |= static_cast<uint32_t>(gt) << j;
+    fe0 |= static_cast<uint32_t>(e0) << j;
+    fe1 |= static_cast<uint32_t>(e1) << j;
+    const uint32_t ng = __popcll(__ballot(gt));
+    const uint32_t n0 = __popcll(__ballot(e0));
+    const uint32_t n1 = __popcll(__ballot(e1));
+    if (lane == 0) {
+      s_cnt[0][j * W + wave] = ng | (n0 << 16);
+      s_cnt[1][j * W + wave] = n1;
     }
-    take += t ? 1 : 0;
-    s_cls[i] = static_cast<uint8_t>(cls | (t ? 0x80 : 0));
   }
   __syncthreads();
-  int out = block_inclusive_scan(take, s_wt, tot) - take;
-  for (int i = beg; i < end; ++i) {
-    if (s_cls[i] & 0x80) {
-      if (out < R) rows[static_cast<size_t>(b) * R + out] = i;
-      ++out;
+  // exclusive prefix of every (j, wave) entry in position order: lane l sums
+  // entries 4l .. 4l + 3 (fields of at most N < 2^16 never carry over)
+  constexpr int E = NJ * W;
+  uint32_t c0[4], c1[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = 4 * lane + q;
+    c0[q] = e < E ? s_cnt[0][e] : 0u;
+    c1[q] = e < E ? s_cnt[1][e] : 0u;
+  }
+  const uint32_t l0 = c0[0] + c0[1] + c0[2] + c0[3];
+  const uint32_t l1 = c1[0] + c1[1] + c1[2] + c1[3];
+  const uint32_t i0 = wave_incl_scan(l0);
+  const uint32_t i1 = wave_incl_scan(l1);
+  const int sub = wave & 3;  // this wave's entries sit at offset sub of their lane
+  uint32_t p0 = i0 - l0, p1 = i1 - l1;
+#pragma unroll
+  for (int q = 0; q < 3; ++q)
+    if (q < sub) {
+      p0 += c0[q];
+      p1 += c1[q];
     }
+  const uint32_t t0 = __builtin_amdgcn_readlane(i0, 63);
+  const uint32_t t1 = __builtin_amdgcn_readlane(i1, 63);
+  const int total = static_cast<int>((t0 & 0xffffu) + min(t0 >> 16, static_cast<uint32_t>(need[0])) +
+                                     min(t1, static_cast<uint32_t>(need[1])));
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int src = j * (W / 4) + (wave >> 2);
+    const uint32_t q0 = __builtin_amdgcn_readlane(p0, src);
+    const uint32_t q1 = __builtin_amdgcn_readlane(p1, src);
+    const uint32_t gt_before = q0 & 0xffffu, t0_before = q0 >> 16, t1_before = q1;
+    const bool gt = (fgt >> j) & 1u, e0 = (fe0 >> j) & 1u, e1 = (fe1 >> j) & 1u;
+    const uint32_t r0 = t0_before + lanes_below(__ballot(e0));  // tie rank in class 0
+    const uint32_t r1 = t1_before + lanes_below(__ballot(e1));
+    const bool take = gt || (e0 && r0 < static_cast<uint32_t>(need[0])) ||
+                      (e1 && r1 < static_cast<uint32_t>(need[1]));
+    const uint32_t out = gt_before + min(t0_before, static_cast<uint32_t>(need[0])) +
+                         min(t1_before, static_cast<uint32_t>(need[1])) + lanes_below(__ballot(take));
+    if (take && out < static_cast<uint32_t>(R))
+      rows[static_cast<size_t>(b) * R + out] = j * TPB + tid;
   }
   // pad a short list (inconsistent n_fresh) with the last position
-  __syncthreads();
-  for (int r = tot + tid; r < R; r += kTopkThreads) rows[static_cast<size_t>(b) * R + r] = N - 1;
+  for (int r = total + tid; r < R; r += TPB) rows[static_cast<size_t>(b) * R + r] = N - 1;
 }
 
 // ------------------------------------------------------------------ Eq. (3)
@@ -466,12 +556,32 @@ int select_impl(const rc_shape* shape, const rc_segment* segs, int32_t S, int32_
       return fail(RC_ERR_HIP, "%s: copy of scores_in failed", what);
   }
   if (R > 0) {
+    // NC = 1 when class 1 takes nothing (its candidates are simply not
+    // taken); NJ = positions per thread (rounded up to an even count past 8)
+    auto launch = [&](auto kern, int tpb) {
+      hipLaunchKernelGGL(kern, dim3(B), dim3(tpb), 0, stream, sc, segs4, S, N, item_mask, k0, k1,
+                         R, rows);
+    };
+    auto by_chunks = [&](auto nc) {
+      constexpr int NC = decltype(nc)::value;
+      switch ((N + 1023) / 1024) {
+        case 1: launch(topk_kernel<NC, 1, 1024>, 1024); break;
+        case 2: launch(topk_kernel<NC, 2, 1024>, 1024); break;
+        case 3: launch(topk_kernel<NC, 3, 1024>, 1024); break;
+        case 4: launch(topk_kernel<NC, 4, 1024>, 1024); break;
+        case 5: launch(topk_kernel<NC, 5, 1024>, 1024); break;
+        case 6: launch(topk_kernel<NC, 6, 1024>, 1024); break;
+        case 7: launch(topk_kernel<NC, 7, 1024>, 1024); break;
+        case 8: launch(topk_kernel<NC, 8, 1024>, 1024); break;
+        case 9: case 10: launch(topk_kernel<NC, 10, 1024>, 1024); break;
+        case 11: case 12: launch(topk_kernel<NC, 12, 1024>, 1024); break;
+        default: launch(topk_kernel<NC, 16, 1024>, 1024); break;
+      }
+    };
     if (k1 > 0)
-      hipLaunchKernelGGL(topk_kernel<2>, dim3(B), dim3(kTopkThreads), 0, stream, sc, segs4, S, N,
-                         item_mask, k0, k1, R, rows);
-    else  // class 1 takes nothing: its candidates are simply not taken
-      hipLaunchKernelGGL(topk_kernel<1>, dim3(B), dim3(kTopkThreads), 0, stream, sc, segs4, S, N,
-                         item_mask, k0, k1, R, rows);
+      by_chunks(std::integral_constant<int, 2>{});
+    else
+      by_chunks(std::integral_constant<int, 1>{});
     if (int st = check_launch(what)) return st;
   }
   if (patch && ksum > 0) {

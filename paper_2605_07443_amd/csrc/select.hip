@@ -10,8 +10,8 @@
 //                     key (11-bit digits, LDS histograms), then the fresh and
 //                     selected positions written in ascending order from
 //                     per-wave counts
-//   patch_kernel      copies the fresh K/V rows of the selected cached
-//                     positions over the assembled rows
+//   patch_kernel      one wave per listed row: copies the fresh K/V row over
+//                     the assembled one when the position is cached
 #include "rc_common.h"
 
 namespace rc {
@@ -431,53 +431,61 @@ __global__ __launch_bounds__(64 * kDevWaves) void eq3_score_kernel(
 
 // ---------------------------------------------------------------------- patch
 
-constexpr int kPatchThreads = 256;
+constexpr int kPatchThreads = 256;  // one wave per selected row
 
+// Wave w of workgroup x copies row x * 4 + w of the list when its position is
+// cached: the lanes test 64 segments at a time against the position (one
+// ballot), so no segment table is staged and no barrier is needed.
 __global__ __launch_bounds__(kPatchThreads) void patch_kernel(
     const int4* __restrict__ segs, int S, int N, const int32_t* __restrict__ rows, int R,
-    int rows_per_wg, int row_units, const char* __restrict__ k_fresh,
-    const char* __restrict__ v_fresh, char* __restrict__ k_asm, char* __restrict__ v_asm) {
-  __shared__ int4 s_segs[kMaxSegments];
-  __shared__ int s_pos[256];
+    int row_units, const char* __restrict__ k_fresh, const char* __restrict__ v_fresh,
+    char* __restrict__ k_asm, char* __restrict__ v_asm) {
   const int b = blockIdx.y;
-  const int r0 = blockIdx.x * rows_per_wg;
-  const int cnt = min(rows_per_wg, R - r0);
-  for (int s = threadIdx.x; s < S; s += kPatchThreads) s_segs[s] = segs[static_cast<size_t>(b) * S + s];
-  __syncthreads();
-  for (int t = threadIdx.x; t < cnt; t += kPatchThreads) {
-    const int i = rows[static_cast<size_t>(b) * R + r0 + t];
-    int pos = -1;
-    if (i >= 0 && i < N) {
-      const int s = find_segment(s_segs, S, i);
-      if (s >= 0 && s_segs[s].z >= 0) pos = i;  // cached position: patch it
+  const int lane = threadIdx.x & 63;
+  const int r = blockIdx.x * (kPatchThreads / 64) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (r >= R) return;
+  const int i = rows[static_cast<size_t>(b) * R + r];
+  if (i < 0 || i >= N) return;
+  bool cached = false;
+  for (int s0 = 0; s0 < S; s0 += 64) {
+    const int sidx = s0 + lane;
+    bool hit = false;
+    int pool = -1;
+    if (sidx < S) {
+      const int4 g = segs[static_cast<size_t>(b) * S + sidx];
+      hit = g.x <= i && i - g.x < g.y;
+      pool = g.z;
     }
-    s_pos[t] = pos;
+    const uint64_t m = __ballot(hit);
+    if (m != 0) {
+      cached = __builtin_amdgcn_readlane(pool, __builtin_ctzll(m)) >= 0;
+      break;
+    }
   }
-  __syncthreads();
-  const int items = cnt * row_units;
-  for (int base = threadIdx.x; base < items; base += kPatchThreads * 4) {
-    u32x4 kv[4], vv[4];
-    int tk[4], un[4];
-    bool ok[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int idx = base + u * kPatchThreads;
-      ok[u] = idx < items;
-      tk[u] = ok[u] ? idx / row_units : 0;
-      un[u] = idx - tk[u] * row_units;
-      ok[u] = ok[u] && s_pos[tk[u]] >= 0;
-      if (ok[u]) {
-        const size_t off = (static_cast<size_t>(b) * N + s_pos[tk[u]]) * row_units;
-        kv[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(k_fresh) + off + un[u]);
-        vv[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(v_fresh) + off + un[u]);
-      }
+  if (!cached) return;  // fresh position (or in no segment)
+  const size_t off = (static_cast<size_t>(b) * N + i) * row_units;
+  const u32x4* kf = reinterpret_cast<const u32x4*>(k_fresh) + off;
+  const u32x4* vf = reinterpret_cast<const u32x4*>(v_fresh) + off;
+  u32x4* ka = reinterpret_cast<u32x4*>(k_asm) + off;
+  u32x4* va = reinterpret_cast<u32x4*>(v_asm) + off;
+  for (int u0 = 0; u0 < row_units; u0 += 128) {
+    const int u1 = u0 + lane, u2 = u0 + 64 + lane;
+    u32x4 k1, v1, k2, v2;
+    if (u1 < row_units) {
+      k1 = __builtin_nontemporal_load(kf + u1);
+      v1 = __builtin_nontemporal_load(vf + u1);
     }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      if (!ok[u]) continue;
-      const size_t off = (static_cast<size_t>(b) * N + s_pos[tk[u]]) * row_units;
-      reinterpret_cast<u32x4*>(k_asm)[off + un[u]] = kv[u];
-      reinterpret_cast<u32x4*>(v_asm)[off + un[u]] = vv[u];
+    if (u2 < row_units) {
+      k2 = __builtin_nontemporal_load(kf + u2);
+      v2 = __builtin_nontemporal_load(vf + u2);
+    }
+    if (u1 < row_units) {
+      ka[u1] = k1;
+      va[u1] = v1;
+    }
+    if (u2 < row_units) {
+      ka[u2] = k2;
+      va[u2] = v2;
     }
   }
 }
@@ -585,10 +593,10 @@ int select_impl(const rc_shape* shape, const rc_segment* segs, int32_t S, int32_
     if (int st = check_launch(what)) return st;
   }
   if (patch && ksum > 0) {
-    const int rows_per_wg = 4;  // many small workgroups: the selected rows are scattered
+    const int rows_per_wg = kPatchThreads / 64;
     dim3 grid((R + rows_per_wg - 1) / rows_per_wg, B);
     hipLaunchKernelGGL(patch_kernel, grid, dim3(kPatchThreads), 0, stream, segs4, S, N, rows, R,
-                       rows_per_wg, row_units, static_cast<const char*>(k_fresh),
+                       row_units, static_cast<const char*>(k_fresh),
                        static_cast<const char*>(v_fresh), static_cast<char*>(k_asm),
                        static_cast<char*>(v_asm));
     if (int st = check_launch(what)) return st;

@@ -40,8 +40,11 @@ PROFILES = os.path.join(ROOT, "profiles")
 def parse_args():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=10)
+    # The shader clock rises over the first tens of milliseconds of sustained
+    # load: 500 untimed steps (about 90 ms on workload 2) reach the sustained
+    # clock before the 1000 timed ones (about 0.2 s).
+    ap.add_argument("--steps", type=int, default=1000)
+    ap.add_argument("--warmup", type=int, default=500)
     ap.add_argument("--config", type=int, default=2, help="workload 1..5 (default 2)")
     ap.add_argument("--pct", type=int, default=None, help="recompute ratio in percent")
     ap.add_argument("--batches", type=int, default=4, help="independent batches rotated")

@@ -5,8 +5,11 @@
 // Both are HBM-bound copies. A workgroup of 256 threads owns TOK consecutive
 // positions of one request (TOK * key row = 8 KiB): it first
 // resolves each position to its source row (binary search of the request's
-// segment table staged in LDS), then streams 16-byte units with non-temporal
-// loads and stores (the fastest copy form measured on MI355X). A key unit pairs
+// segment table staged in LDS), then streams 16-byte units. Source rows and
+// the assembled rows go through the caches with ordinary loads and stores
+// (pool rows of popular items recur across requests and batches, and the
+// attention reads the assembled rows next); the fresh key rows read for the
+// score are non-temporal. A key unit pairs
 // element block [j, j+E) of a head with [j+D/2, j+D/2+E) so the rotation of
 // the pairs (j, j+D/2) happens in registers between the load and the store.
 #include "rc_common.h"
@@ -135,8 +138,8 @@ __global__ __launch_bounds__(kThreads) void kv_rows_kernel(
       if (kok[u]) {
         const u32x4* src = reinterpret_cast<const u32x4*>(s_srck[ktok[u]]);
         if constexpr (ASSEMBLE) {
-          ua[u] = __builtin_nontemporal_load(src + kunit[u]);
-          ub[u] = __builtin_nontemporal_load(src + kunit[u] + half_units);
+          ua[u] = src[kunit[u]];
+          ub[u] = src[kunit[u] + half_units];
         } else {
           ua[u] = src[kunit[u]];
           ub[u] = src[kunit[u] + half_units];
@@ -160,7 +163,7 @@ __global__ __launch_bounds__(kThreads) void kv_rows_kernel(
         vtok[u] = vok[u] ? idx / row_units : 0;
         vunit[u] = idx - vtok[u] * row_units;
         vok[u] = vok[u] && s_srcv[vtok[u]] != nullptr;
-        if (vok[u]) vv[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(s_srcv[vtok[u]]) + vunit[u]);
+        if (vok[u]) vv[u] = reinterpret_cast<const u32x4*>(s_srcv[vtok[u]])[vunit[u]];
       }
     }
 
@@ -184,8 +187,8 @@ __global__ __launch_bounds__(kThreads) void kv_rows_kernel(
         if constexpr (WRITE) {
           u32x4* dst = reinterpret_cast<u32x4*>(k_out + (static_cast<size_t>(b) * N + i0 + ktok[u]) * row_bytes);
           if constexpr (ASSEMBLE) {
-            __builtin_nontemporal_store(ua[u], dst + kunit[u]);
-            __builtin_nontemporal_store(ub[u], dst + kunit[u] + half_units);
+            dst[kunit[u]] = ua[u];
+            dst[kunit[u] + half_units] = ub[u];
           } else {
             dst[kunit[u]] = ua[u];
             dst[kunit[u] + half_units] = ub[u];
@@ -203,7 +206,7 @@ __global__ __launch_bounds__(kThreads) void kv_rows_kernel(
       for (int u = 0; u < kVPer; ++u) {
         if (!vok[u]) continue;
         u32x4* dst = reinterpret_cast<u32x4*>(v_out + (static_cast<size_t>(b) * N + i0 + vtok[u]) * row_bytes);
-        __builtin_nontemporal_store(vv[u], dst + vunit[u]);
+        dst[vunit[u]] = vv[u];
       }
     }
   }

@@ -24,7 +24,10 @@
 //     are double-buffered in LDS (one barrier per tile) with the next tile's
 //     global loads in flight during compute. For D = 128 (not paged) the
 //     tiles go from HBM straight into LDS and every K/V read of the tile loop
-//     is issued as assembly (layouts and ordering at AttnBufDirect).
+//     is issued as assembly (layouts and ordering at AttnBufDirect), and a
+//     tile is computed in halves of 32 keys so that the softmax of one half
+//     runs on the vector ALU beside the matrix products of the other
+//     (direct_tile).
 //   * Workgroup ids are remapped so that all row tiles of one (request, KV
 //     head) run on the same XCD (ids are dealt round-robin over the 8 XCDs),
 //     sharing its L2 for the K/V stream. Each XCD starts its longest (latest)
@@ -487,6 +490,163 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
   const int t_mask = min(n_kv, wave_pmin / kKT);
   const int wave_last = pmax / kKT;   // tiles past it are masked for every row of this wave
 
+  // DIRECT: one KV tile in an order that lets the vector ALU work beside the
+  // matrix cores. Scores of keys 0..31 first; then the scores of keys 32..63
+  // are issued while the probabilities of keys 0..31 are formed against the
+  // current reference max; after the rescale decision (taken on the whole
+  // tile, as before), V^T P^T of keys 0..31 runs while the probabilities of
+  // keys 32..63 are formed. Without a rescale the reference max is unchanged,
+  // so every value is computed exactly as in the plain order; with one, the
+  // probabilities of keys 0..31 are recomputed from the scores, which are
+  // kept until the decision.
+  auto direct_tile = [&](int t, auto buf_tag, auto mask_tag) __attribute__((always_inline)) {
+    constexpr int cur = decltype(buf_tag)::value;
+    constexpr bool MASKED = decltype(mask_tag)::value;
+    f32x4 s[4][2];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) s[kb][0] = s[kb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // K fragments in the order (dc, kb) within each half of the keys:
+    // fragment gi of half h is key block 2h + gi % 2, d chunk gi / 2
+    constexpr int KG = DC * 4;
+    constexpr int KAHEAD = 3;
+    u32x4 kf[KG];
+    auto rdk = [&](auto G) {
+      constexpr int gi = decltype(G)::value;
+      constexpr int h = gi / (KG / 2), r = gi % (KG / 2);
+      constexpr int kb = 2 * h + r % 2, dc = r / 2;
+      kf[gi] = lds_read_b128_async<cur * kBufBytes + kb * 4096>(kaddr[dc]);
+    };
+    auto mm = [&](auto G) {
+      constexpr int gi = decltype(G)::value;
+      constexpr int later = (KG - 1 - gi) < KAHEAD ? (KG - 1 - gi) : KAHEAD;
+      lds_wait_tied<later>(kf[gi]);
+      constexpr int h = gi / (KG / 2), r = gi % (KG / 2);
+      constexpr int kb = 2 * h + r % 2, dc = r / 2;
+      const bf16x8 a = __builtin_bit_cast(bf16x8, kf[gi]);
+      s[kb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[0][dc], s[kb][0], 0, 0, 0);
+      s[kb][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[1][dc], s[kb][1], 0, 0, 0);
+      if constexpr (gi + KAHEAD + 1 < KG) rdk(std::integral_constant<int, gi + KAHEAD + 1>{});
+    };
+    auto mask_half = [&](int h) __attribute__((always_inline)) {
+      if constexpr (MASKED) {
+        const int j0 = t * kKT;
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+          for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if (j0 + (2 * h + kk) * 16 + q4 * 4 + i > pos[nb]) s[2 * h + kk][nb][i] = -INFINITY;
+      }
+    };
+    // per column: maximum of a half, probabilities of a half (packed) and
+    // their fp32 sums by key block
+    auto half_max = [&](int h, int nb) __attribute__((always_inline)) -> float {
+      return __builtin_elementwise_maximum(
+          __builtin_elementwise_maximum(
+              __builtin_elementwise_maximum(s[2 * h][nb][0], s[2 * h][nb][1]),
+              __builtin_elementwise_maximum(s[2 * h][nb][2], s[2 * h][nb][3])),
+          __builtin_elementwise_maximum(
+              __builtin_elementwise_maximum(s[2 * h + 1][nb][0], s[2 * h + 1][nb][1]),
+              __builtin_elementwise_maximum(s[2 * h + 1][nb][2], s[2 * h + 1][nb][3])));
+    };
+    bf16x8 pb[2][2];
+    float ls[4][2];  // LSE: fp32 sum of each key block's probabilities
+    auto probs = [&](int h, int nb, float mc) __attribute__((always_inline)) {
+      float p[2][4];
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          p[kk][i] = __builtin_amdgcn_exp2f(fmaf(s[2 * h + kk][nb][i], scale_log2e, -mc));
+      if constexpr (LSE) {
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) ls[2 * h + kk][nb] = (p[kk][0] + p[kk][1]) + (p[kk][2] + p[kk][3]);
+      }
+      const u32x4 w = {pack_bf16x2(p[0][0], p[0][1]), pack_bf16x2(p[0][2], p[0][3]),
+                       pack_bf16x2(p[1][0], p[1][1]), pack_bf16x2(p[1][2], p[1][3])};
+      pb[h][nb] = __builtin_bit_cast(bf16x8, w);
+    };
+
+    __builtin_amdgcn_s_setprio(1);
+    static_for<0, KAHEAD + 1>(rdk);
+    static_for<0, KG / 2>(mm);
+    // scores of keys 32..63 on the matrix cores; keys 0..31 on the vector ALU
+    static_for<KG / 2, KG>(mm);
+    mask_half(0);
+    float m0[2];
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      m0[nb] = half_max(0, nb);
+      probs(0, nb, m_run[nb] * scale_log2e);
+    }
+    // issue order: the first half's products, then each product of the
+    // second half followed by vector work of the first half
+    __builtin_amdgcn_sched_group_barrier(0x008, KG, 0);
+    static_for<0, KG>([&](auto) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+    });
+    __builtin_amdgcn_s_setprio(0);
+    mask_half(1);
+    float mx[2];
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) mx[nb] = max_over_rows(__builtin_elementwise_maximum(m0[nb], half_max(1, nb)));
+    // a query sees key 0 in the first tile, so the reference max is finite after it
+    if (__ballot(mx[0] * scale_log2e - m_run[0] * scale_log2e > kLazy ||
+                 mx[1] * scale_log2e - m_run[1] * scale_log2e > kLazy) != 0) {
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) {
+        const float m_new = fmaxf(m_run[nb], mx[nb]);
+        const float alpha = __builtin_amdgcn_exp2f((m_run[nb] - m_new) * scale_log2e);
+        l_acc[nb] *= alpha;
+        if constexpr (LSE) l32[nb] *= alpha;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) o[db][nb] *= alpha;
+        m_run[nb] = m_new;
+        probs(0, nb, m_new * scale_log2e);
+      }
+    }
+
+    // ---- O^T += V^T P^T: keys 0..31 while the vector ALU forms keys 32..63
+    __builtin_amdgcn_s_setprio(1);
+    constexpr int NG = 2 * DB;
+    constexpr int AHEAD = 3;
+    u32x2 lo[NG], hi[NG];
+    auto rd = [&](auto G) {
+      constexpr int gi = decltype(G)::value;
+      constexpr int kc = gi / DB, db = gi % DB;
+      lo[gi] = lds_read_tr4_async<cur * kBufBytes + kc * 8192>(vaddr[db]);
+      hi[gi] = lds_read_tr4_async<cur * kBufBytes + kc * 8192 + 4096>(vaddr[db]);
+    };
+    auto pv = [&](auto G) {
+      constexpr int gi = decltype(G)::value;
+      constexpr int later = (NG - 1 - gi) < AHEAD ? (NG - 1 - gi) : AHEAD;
+      lds_wait_tied<2 * later>(lo[gi], hi[gi]);
+      constexpr int kc = gi / DB, db = gi % DB;
+      const bf16x8 a = __builtin_bit_cast(bf16x8, u32x4{lo[gi][0], lo[gi][1], hi[gi][0], hi[gi][1]});
+      o[db][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][0], o[db][0], 0, 0, 0);
+      o[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][1], o[db][1], 0, 0, 0);
+      if constexpr (gi + AHEAD + 1 < NG) rd(std::integral_constant<int, gi + AHEAD + 1>{});
+    };
+    static_for<0, AHEAD + 1>(rd);
+    static_for<0, DB>(pv);
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) probs(1, nb, m_run[nb] * scale_log2e);
+    if constexpr (LSE) {
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+        l32[nb] = (((l32[nb] + ls[0][nb]) + ls[1][nb]) + ls[2][nb]) + ls[3][nb];
+    }
+    static_for<DB, NG>(pv);
+#pragma unroll
+    for (int kc = 0; kc < 2; ++kc) {
+      l_acc[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[kc][0], l_acc[0], 0, 0, 0);
+      l_acc[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[kc][1], l_acc[1], 0, 0, 0);
+    }
+    __builtin_amdgcn_s_setprio(0);
+  };
+
   // One KV tile: S^T = K Q^T, (masked) online softmax, O^T += V^T P^T, then
   // stage the next tile. The causal mask is applied only on tiles reaching past
   // some row of this wave (a uniform branch).
@@ -501,42 +661,23 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
 
     // a wave skips the tiles past all of its rows (their weights are zero)
     if (t <= wave_last) {
+    if constexpr (DIRECT) {
+      if (MASK) direct_tile(t, buf_tag, std::true_type{});
+      else direct_tile(t, buf_tag, std::false_type{});
+    } else {
     // ---- S^T for 64 keys x 32 queries (8 independent accumulators)
     f32x4 s[4][2];
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) s[kb][0] = s[kb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
     __builtin_amdgcn_s_setprio(1);
-    if constexpr (DIRECT) {
-      // fragments (dc, kb) in dc-major order, three reads ahead
-      constexpr int KG = DC * 4;
-      constexpr int KAHEAD = 3;
-      u32x4 kf[KG];
-      auto rdk = [&](auto G) {
-        constexpr int gi = decltype(G)::value;
-        constexpr int dc = gi / 4, kb = gi % 4;
-        kf[gi] = lds_read_b128_async<cur * kBufBytes + kb * 4096>(kaddr[dc]);
-      };
-      static_for<0, KAHEAD + 1>(rdk);
-      static_for<0, KG>([&](auto G) {
-        constexpr int gi = decltype(G)::value;
-        constexpr int later = (KG - 1 - gi) < KAHEAD ? (KG - 1 - gi) : KAHEAD;
-        lds_wait_tied<later>(kf[gi]);
-        constexpr int dc = gi / 4, kb = gi % 4;
-        const bf16x8 a = __builtin_bit_cast(bf16x8, kf[gi]);
+#pragma unroll
+    for (int dc = 0; dc < DC; ++dc)
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(kfrag(buf_tag, kb * 16 + c16, dc * 4 + q4)));
         s[kb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[0][dc], s[kb][0], 0, 0, 0);
         s[kb][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[1][dc], s[kb][1], 0, 0, 0);
-        if constexpr (gi + KAHEAD + 1 < KG) rdk(std::integral_constant<int, gi + KAHEAD + 1>{});
-      });
-    } else {
-#pragma unroll
-      for (int dc = 0; dc < DC; ++dc)
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
-          const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(kfrag(buf_tag, kb * 16 + c16, dc * 4 + q4)));
-          s[kb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[0][dc], s[kb][0], 0, 0, 0);
-          s[kb][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[1][dc], s[kb][1], 0, 0, 0);
-        }
-    }
+      }
     __builtin_amdgcn_s_setprio(0);
 
     if (MASK) {
@@ -605,32 +746,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
     // keys kc*32 + q4*4 + {0..3} and kc*32 + 16 + q4*4 + {0..3}: the key
     // order of the P^T operand above.
     __builtin_amdgcn_s_setprio(1);
-    if constexpr (DIRECT) {
-      // 16 groups (kc, db) of two reads; three groups in flight ahead of the
-      // one being multiplied
-      // keys kc*32 + q4*4 + {0..3} (lo) and kc*32 + 16 + q4*4 + {0..3} (hi):
-      // rows 32 kc (+16) further than the lane's base rows
-      constexpr int NG = 2 * DB;
-      constexpr int AHEAD = 3;
-      u32x2 lo[NG], hi[NG];
-      auto rd = [&](auto G) {
-        constexpr int gi = decltype(G)::value;
-        constexpr int kc = gi / DB, db = gi % DB;
-        lo[gi] = lds_read_tr4_async<cur * kBufBytes + kc * 8192>(vaddr[db]);
-        hi[gi] = lds_read_tr4_async<cur * kBufBytes + kc * 8192 + 4096>(vaddr[db]);
-      };
-      static_for<0, AHEAD + 1>(rd);
-      static_for<0, NG>([&](auto G) {
-        constexpr int gi = decltype(G)::value;
-        constexpr int later = (NG - 1 - gi) < AHEAD ? (NG - 1 - gi) : AHEAD;   // groups issued after
-        lds_wait_tied<2 * later>(lo[gi], hi[gi]);
-        constexpr int kc = gi / DB, db = gi % DB;
-        const bf16x8 a = __builtin_bit_cast(bf16x8, u32x4{lo[gi][0], lo[gi][1], hi[gi][0], hi[gi][1]});
-        o[db][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][0], o[db][0], 0, 0, 0);
-        o[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][1], o[db][1], 0, 0, 0);
-        if constexpr (gi + AHEAD + 1 < NG) rd(std::integral_constant<int, gi + AHEAD + 1>{});
-      });
-    } else {
+    {
 #pragma unroll
       for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
@@ -648,7 +764,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
       l_acc[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[kc][1], l_acc[1], 0, 0, 0);
     }
     __builtin_amdgcn_s_setprio(0);
-
+    }  // not DIRECT
     }  // t <= wave_last
 
     // ---- stage the next tile into the other buffer, prefetch the one after

@@ -283,3 +283,31 @@ def test_full_prefill_full_workloads(cid, stride):
     outh = H(out)
     g_ = np.concatenate([outh[b, idx] for b, idx in enumerate(sel)])
     assert_attn_close(g_, np.concatenate(ref), "bf16", "full prefill")
+
+
+@pytest.mark.parametrize("D", [64, 128])
+def test_attention_max_jumps_inside_tiles(D):
+    """Scores that jump by more than the lazy-rescale margin in the second
+    half of every 64-key tile (keys j with j % 64 >= 32 align with the
+    queries more than all earlier keys): the running max is raised inside a
+    tile, after the first half's probabilities were formed, on every tile.
+    Output and log-sum-exp against the oracle."""
+    B, N, Hq, Hkv = 1, 320, 8, 2
+    g = torch.Generator(device="cpu").manual_seed(77 + D)
+    u = torch.ones(D) / D ** 0.25   # scale * (u . 8u) * log2(e) = 11.5 log2 units per amplitude step
+    amp = torch.tensor([(j // 64) + (1.0 if j % 64 >= 32 else 0.0) for j in range(N)])
+    q = (u + 0.05 * torch.randn((B, N, Hq, D), generator=g)).to(torch.bfloat16)
+    k = (amp[None, :, None, None] * u * 8.0 + 0.05 * torch.randn((B, N, Hkv, D), generator=g)).to(torch.bfloat16)
+    v = torch.randn((B, N, Hkv, D), generator=g).to(torch.bfloat16)
+    rows = torch.tensor([[5, 40, 63, 64, 95, 96, 127, 150, 191, 200, 255, 256, 300, 319]], dtype=torch.int32)
+    say(f"[attention max jumps] D={D}")
+    out = ops.selective_attention(q.to(DEV), k.to(DEV), v.to(DEV), rows.to(DEV))
+    full = ops.full_prefill(q.to(DEV), k.to(DEV), v.to(DEV))
+    _, lse = ops.selective_attention_lse(q.to(DEV), k.to(DEV), v.to(DEV))
+    torch.cuda.synchronize()
+    assert_attn_close(H(out), O.attention(H(q), H(k), H(v), rows=rows.numpy()), "bf16", "selective")
+    assert_attn_close(H(full), O.attention(H(q), H(k), H(v)), "bf16", "full prefill")
+    lse_o = O.attention_lse(H(q), H(k))
+    # lse reaches about 45 here: the absolute bound of the eq3 tests plus fp32 rounding of it
+    err = np.abs(lse.cpu().numpy().astype(np.float64) - lse_o)
+    assert np.all(err <= 2e-5 + 1e-6 * np.abs(lse_o)), f"lse max err {err.max():.3e}"

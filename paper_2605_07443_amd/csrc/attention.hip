@@ -24,10 +24,10 @@
 //     are double-buffered in LDS (one barrier per tile) with the next tile's
 //     global loads in flight during compute. For D = 128 (not paged) the
 //     tiles go from HBM straight into LDS and every K/V read of the tile loop
-//     is issued as assembly (layouts and ordering at AttnBufDirect), and a
-//     tile is computed in halves of 32 keys so that the softmax of one half
-//     runs on the vector ALU beside the matrix products of the other
-//     (direct_tile).
+//     is issued as assembly (layouts and ordering at AttnBufDirect).
+//   * A tile is computed in halves of 32 keys, so that the softmax of one
+//     half runs on the vector ALU beside the matrix products of the other
+//     (compute_tile).
 //   * Workgroup ids are remapped so that all row tiles of one (request, KV
 //     head) run on the same XCD (ids are dealt round-robin over the 8 XCDs),
 //     sharing its L2 for the K/V stream. Each XCD starts its longest (latest)
@@ -490,16 +490,16 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
   const int t_mask = min(n_kv, wave_pmin / kKT);
   const int wave_last = pmax / kKT;   // tiles past it are masked for every row of this wave
 
-  // DIRECT: one KV tile in an order that lets the vector ALU work beside the
-  // matrix cores. Scores of keys 0..31 first; then the scores of keys 32..63
+  // One KV tile (either staging) in an order that lets the vector ALU work
+  // beside the matrix cores. Scores of keys 0..31 first; then the scores of keys 32..63
   // are issued while the probabilities of keys 0..31 are formed against the
   // current reference max; after the rescale decision (taken on the whole
-  // tile, as before), V^T P^T of keys 0..31 runs while the probabilities of
-  // keys 32..63 are formed. Without a rescale the reference max is unchanged,
-  // so every value is computed exactly as in the plain order; with one, the
-  // probabilities of keys 0..31 are recomputed from the scores, which are
-  // kept until the decision.
-  auto direct_tile = [&](int t, auto buf_tag, auto mask_tag) __attribute__((always_inline)) {
+  // tile), V^T P^T of keys 0..31 runs while the probabilities of keys 32..63
+  // are formed. Without a rescale the reference max is unchanged, so every
+  // value equals that of the plain order (all scores, then all
+  // probabilities); with one, the probabilities of keys 0..31 are recomputed
+  // from the scores, which are kept until the decision.
+  auto compute_tile = [&](int t, auto buf_tag, auto mask_tag) __attribute__((always_inline)) {
     constexpr int cur = decltype(buf_tag)::value;
     constexpr bool MASKED = decltype(mask_tag)::value;
     f32x4 s[4][2];
@@ -568,11 +568,26 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
       pb[h][nb] = __builtin_bit_cast(bf16x8, w);
     };
 
+    // without DIRECT: K fragments through ordinary LDS reads (padded layout)
+    auto mmp = [&](auto G) {
+      constexpr int gi = decltype(G)::value;
+      constexpr int h = gi / (KG / 2), r = gi % (KG / 2);
+      constexpr int kb = 2 * h + r % 2, dc = r / 2;
+      const bf16x8 a = __builtin_bit_cast(
+          bf16x8, *reinterpret_cast<const u32x4*>(kfrag(buf_tag, kb * 16 + c16, dc * 4 + q4)));
+      s[kb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[0][dc], s[kb][0], 0, 0, 0);
+      s[kb][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[1][dc], s[kb][1], 0, 0, 0);
+    };
     __builtin_amdgcn_s_setprio(1);
-    static_for<0, KAHEAD + 1>(rdk);
-    static_for<0, KG / 2>(mm);
-    // scores of keys 32..63 on the matrix cores; keys 0..31 on the vector ALU
-    static_for<KG / 2, KG>(mm);
+    if constexpr (DIRECT) {
+      static_for<0, KAHEAD + 1>(rdk);
+      static_for<0, KG / 2>(mm);
+      // scores of keys 32..63 on the matrix cores; keys 0..31 on the vector ALU
+      static_for<KG / 2, KG>(mm);
+    } else {
+      static_for<0, KG / 2>(mmp);
+      static_for<KG / 2, KG>(mmp);
+    }
     mask_half(0);
     float m0[2];
 #pragma unroll
@@ -629,8 +644,22 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
       o[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][1], o[db][1], 0, 0, 0);
       if constexpr (gi + AHEAD + 1 < NG) rd(std::integral_constant<int, gi + AHEAD + 1>{});
     };
-    static_for<0, AHEAD + 1>(rd);
-    static_for<0, DB>(pv);
+    // without DIRECT: transposed reads of the padded V tile
+    auto pvp = [&](auto G) {
+      constexpr int gi = decltype(G)::value;
+      constexpr int kc = gi / DB, db = gi % DB;
+      const u32x2 l2 = lds_read_tr4(vtr(buf_tag, kc * 32 + tr_row, db * 16 + tr_col));
+      const u32x2 h2 = lds_read_tr4(vtr(buf_tag, kc * 32 + 16 + tr_row, db * 16 + tr_col));
+      const bf16x8 a = __builtin_bit_cast(bf16x8, u32x4{l2[0], l2[1], h2[0], h2[1]});
+      o[db][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][0], o[db][0], 0, 0, 0);
+      o[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][1], o[db][1], 0, 0, 0);
+    };
+    if constexpr (DIRECT) {
+      static_for<0, AHEAD + 1>(rd);
+      static_for<0, DB>(pv);
+    } else {
+      static_for<0, DB>(pvp);
+    }
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) probs(1, nb, m_run[nb] * scale_log2e);
     if constexpr (LSE) {
@@ -638,7 +667,8 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
       for (int nb = 0; nb < 2; ++nb)
         l32[nb] = (((l32[nb] + ls[0][nb]) + ls[1][nb]) + ls[2][nb]) + ls[3][nb];
     }
-    static_for<DB, NG>(pv);
+    if constexpr (DIRECT) static_for<DB, NG>(pv);
+    else static_for<DB, NG>(pvp);
 #pragma unroll
     for (int kc = 0; kc < 2; ++kc) {
       l_acc[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[kc][0], l_acc[0], 0, 0, 0);
@@ -661,111 +691,9 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
 
     // a wave skips the tiles past all of its rows (their weights are zero)
     if (t <= wave_last) {
-    if constexpr (DIRECT) {
-      if (MASK) direct_tile(t, buf_tag, std::true_type{});
-      else direct_tile(t, buf_tag, std::false_type{});
-    } else {
-    // ---- S^T for 64 keys x 32 queries (8 independent accumulators)
-    f32x4 s[4][2];
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb) s[kb][0] = s[kb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-    __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-    for (int dc = 0; dc < DC; ++dc)
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(kfrag(buf_tag, kb * 16 + c16, dc * 4 + q4)));
-        s[kb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[0][dc], s[kb][0], 0, 0, 0);
-        s[kb][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[1][dc], s[kb][1], 0, 0, 0);
-      }
-    __builtin_amdgcn_s_setprio(0);
-
-    if (MASK) {
-      const int j0 = t * kKT;
-#pragma unroll
-      for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            if (j0 + kb * 16 + q4 * 4 + i > pos[nb]) s[kb][nb][i] = -INFINITY;
+      if (MASK) compute_tile(t, buf_tag, std::true_type{});
+      else compute_tile(t, buf_tag, std::false_type{});
     }
-
-    // ---- online softmax per query column: p = 2^(s*c - m*c), c = scale*log2(e)
-    float mx[2];
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-      float m = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-        m = __builtin_elementwise_maximum(
-            __builtin_elementwise_maximum(m, s[kb][nb][0]),
-            __builtin_elementwise_maximum(__builtin_elementwise_maximum(s[kb][nb][1], s[kb][nb][2]),
-                                          s[kb][nb][3]));
-      mx[nb] = max_over_rows(m);
-    }
-    // a query sees key 0 in the first tile, so the reference max is finite after it
-    if (__ballot(mx[0] * scale_log2e - m_run[0] * scale_log2e > kLazy ||
-                 mx[1] * scale_log2e - m_run[1] * scale_log2e > kLazy) != 0) {
-#pragma unroll
-      for (int nb = 0; nb < 2; ++nb) {
-        const float m_new = fmaxf(m_run[nb], mx[nb]);
-        const float alpha = __builtin_amdgcn_exp2f((m_run[nb] - m_new) * scale_log2e);
-        l_acc[nb] *= alpha;
-        if constexpr (LSE) l32[nb] *= alpha;
-#pragma unroll
-        for (int db = 0; db < DB; ++db) o[db][nb] *= alpha;
-        m_run[nb] = m_new;
-      }
-    }
-    bf16x8 pb[2][2];
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-      const float mc = m_run[nb] * scale_log2e;
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          s[kb][nb][i] = __builtin_amdgcn_exp2f(fmaf(s[kb][nb][i], scale_log2e, -mc));
-      if constexpr (LSE) {
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-          l32[nb] += (s[kb][nb][0] + s[kb][nb][1]) + (s[kb][nb][2] + s[kb][nb][3]);
-      }
-#pragma unroll
-      for (int kc = 0; kc < 2; ++kc) {
-        u32x4 w = {pack_bf16x2(s[2 * kc][nb][0], s[2 * kc][nb][1]),
-                   pack_bf16x2(s[2 * kc][nb][2], s[2 * kc][nb][3]),
-                   pack_bf16x2(s[2 * kc + 1][nb][0], s[2 * kc + 1][nb][1]),
-                   pack_bf16x2(s[2 * kc + 1][nb][2], s[2 * kc + 1][nb][3])};
-        pb[kc][nb] = __builtin_bit_cast(bf16x8, w);
-      }
-    }
-
-    // ---- O^T += V^T P^T. A operand: lane (c16, q4) needs dim db*16 + c16 of
-    // keys kc*32 + q4*4 + {0..3} and kc*32 + 16 + q4*4 + {0..3}: the key
-    // order of the P^T operand above.
-    __builtin_amdgcn_s_setprio(1);
-    {
-#pragma unroll
-      for (int kc = 0; kc < 2; ++kc)
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          const u32x2 lo = lds_read_tr4(vtr(buf_tag, kc * 32 + tr_row, db * 16 + tr_col));
-          const u32x2 hi = lds_read_tr4(vtr(buf_tag, kc * 32 + 16 + tr_row, db * 16 + tr_col));
-          const bf16x8 a = __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
-          o[db][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][0], o[db][0], 0, 0, 0);
-          o[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[kc][1], o[db][1], 0, 0, 0);
-        }
-    }
-#pragma unroll
-    for (int kc = 0; kc < 2; ++kc) {
-      l_acc[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[kc][0], l_acc[0], 0, 0, 0);
-      l_acc[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[kc][1], l_acc[1], 0, 0, 0);
-    }
-    __builtin_amdgcn_s_setprio(0);
-    }  // not DIRECT
-    }  // t <= wave_last
 
     // ---- stage the next tile into the other buffer, prefetch the one after
     if constexpr (DIRECT) {

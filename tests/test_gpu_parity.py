@@ -311,3 +311,38 @@ def test_attention_max_jumps_inside_tiles(D):
     # lse reaches about 45 here: the absolute bound of the eq3 tests plus fp32 rounding of it
     err = np.abs(lse.cpu().numpy().astype(np.float64) - lse_o)
     assert np.all(err <= 2e-5 + 1e-6 * np.abs(lse_o)), f"lse max err {err.max():.3e}"
+
+
+def test_patch_with_more_than_64_segments():
+    """Requests of 150 segments (the patch kernel tests a position against 64
+    segments at a time): assembly, selection and patched K/V bit-exact with
+    the oracle."""
+    B, Hkv, D, BL = 2, 2, 64, 16
+    rng = np.random.default_rng(11)
+    lens = rng.integers(1, BL + 1, 150)
+    kinds = np.where(np.arange(150) % 3 == 0, -1, np.arange(150) % 2)  # fresh, pool 0, pool 1
+    starts = np.concatenate([[0], np.cumsum(lens)[:-1]])
+    N = int(lens.sum())
+    blocks = rng.integers(0, 40, 150)
+    seg = np.stack([starts, lens, kinds, np.where(kinds < 0, 0, blocks)], 1).astype(np.int32)
+    segs_h = np.ascontiguousarray(np.broadcast_to(seg, (B, 150, 4)))
+    g = torch.Generator(device="cpu").manual_seed(11)
+    pools = [(torch.randn((40, BL, Hkv, D), generator=g).to(torch.bfloat16).to(DEV),
+              torch.randn((40, BL, Hkv, D), generator=g).to(torch.bfloat16).to(DEV)) for _ in range(2)]
+    kf = torch.randn((B, N, Hkv, D), generator=g).to(torch.bfloat16).to(DEV)
+    vf = torch.randn((B, N, Hkv, D), generator=g).to(torch.bfloat16).to(DEV)
+    segs = ops.prepare_segments(segs_h, N, pools, DEV)
+    k = (N - segs.n_fresh) // 4
+    say(f"[patch, 150 segments] N={N} k={k}")
+    ka, va = ops.kv_assemble(pools, segs, kf, vf)
+    torch.cuda.synchronize()
+    hp = [(H(pk), H(pv)) for pk, pv in pools]
+    ka0, va0 = O.assemble(H(kf), H(vf), hp, segs_h)
+    np.testing.assert_array_equal(H(ka), ka0)
+    rows, sc = ops.select_tokens(segs, k, kf, vf, ka, va)
+    torch.cuda.synchronize()
+    rows_h = rows.cpu().numpy()
+    np.testing.assert_array_equal(rows_h, O.topk(segs_h, N, k, sc.cpu().numpy()))
+    kp, vp = O.patch(segs_h, rows_h, H(kf), H(vf), ka0, va0)
+    np.testing.assert_array_equal(H(ka), kp)
+    np.testing.assert_array_equal(H(va), vp)

@@ -3,14 +3,18 @@
 // accumulation on the matrix cores (v_mfma_f32_16x16x32_bf16).
 //
 // Both operands are k-contiguous, which is the native operand order of the
-// MFMA: a lane's A fragment is 8 consecutive k of one X row and its B
-// fragment 8 consecutive k of one W row. A workgroup computes a 128 x 128
-// tile of Y with 4 waves of 64 x 64 (4 x 4 accumulator blocks each); X and W
-// tiles of 64 k stream through double-buffered LDS (rows padded to 144 bytes,
-// so the 16-byte fragment reads of 16 consecutive rows are conflict-free),
-// with the next tile's global loads in flight during the MFMAs. Tiles are
-// ordered n-fastest within groups of 8 row tiles, so the workgroups running
-// together share both operands in L2.
+// MFMA: a lane's fragment is 8 consecutive k of one W row (the MFMA's A
+// operand) or of one X row (its B operand). With W as A the accumulators hold
+// Y^T, so each lane ends with 4 consecutive outputs of one row and the
+// epilogue stores 8-byte packs instead of single values. A workgroup computes
+// a 128 x 128 tile of Y with 4 waves of 64 x 64 (4 x 4 accumulator blocks
+// each); X and W tiles of 64 k stream through double-buffered LDS (rows
+// padded to 144 bytes, so the 16-byte fragment reads of 16 consecutive rows
+// are conflict-free), with the next tile's global loads in flight during the
+// MFMAs. Consecutive workgroups walk the 8 row tiles of a group before moving
+// to the next column tile; as workgroups are dealt to the 8 XCDs in turn,
+// each XCD keeps one row tile of X in its L2 while the column tiles of W
+// stream past.
 #include <type_traits>
 
 #include "rc_common.h"
@@ -26,6 +30,50 @@ constexpr int kGGroup = 8;  // row tiles per ordering group
 constexpr int kGUnits = kGK / 8;                              // 16-byte units per tile row
 constexpr int kGPer = kGM * kGUnits / kGThreads;              // units per thread per operand (4)
 
+using u32x2 = uint32_t __attribute__((ext_vector_type(2)));
+
+// Epilogue of a wave tile of NI x NJ accumulator blocks. The W fragment is the
+// MFMA's A operand and the X fragment its B operand, so block (i, j) holds
+// Y^T and a lane holds columns q4*4 .. q4*4+3 of row c16: four consecutive
+// outputs of one row, stored as one 8-byte pack when the row layout allows
+// it (vec: n % 4 == 0 and 8-byte aligned y and residual), else one by one.
+// The residual is added in fp32 before the single rounding.
+template <int NI, int NJ>
+__device__ __forceinline__ void store_wave_tile(const f32x4 (&acc)[NI][NJ], const uint16_t* __restrict__ res,
+                                                uint16_t* __restrict__ y, int64_t M, int n, int64_t r0,
+                                                int c0, int c16, int q4, bool vec) {
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    const int64_t gr = r0 + i * 16 + c16;
+    if (gr >= M) continue;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int gc = c0 + j * 16 + q4 * 4;
+      float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+      if (vec && gc + 3 < n) {
+        if (res) {
+          const u32x2 rr = *reinterpret_cast<const u32x2*>(res + gr * n + gc);
+          v[0] += bf16_to_f32(static_cast<uint16_t>(rr[0]));
+          v[1] += bf16_to_f32(static_cast<uint16_t>(rr[0] >> 16));
+          v[2] += bf16_to_f32(static_cast<uint16_t>(rr[1]));
+          v[3] += bf16_to_f32(static_cast<uint16_t>(rr[1] >> 16));
+        }
+        const u32x2 o = {static_cast<uint32_t>(f32_to_bf16(v[0])) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16),
+                         static_cast<uint32_t>(f32_to_bf16(v[2])) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16)};
+        *reinterpret_cast<u32x2*>(y + gr * n + gc) = o;
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          if (gc + r >= n) continue;
+          float t = v[r];
+          if (res) t += bf16_to_f32(res[gr * n + gc + r]);
+          y[gr * n + gc + r] = f32_to_bf16(t);
+        }
+      }
+    }
+  }
+}
+
 struct GemmSmem {
   uint16_t a[2][kGM][kGK + kGPad];
   uint16_t b[2][kGN][kGK + kGPad];
@@ -34,9 +82,9 @@ struct GemmSmem {
 __global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void gemm_bf16_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ w,
                       const uint16_t* __restrict__ res, uint16_t* __restrict__ y, int64_t M, int n,
-                      int k, int tiles_m, int tiles_n) {
+                      int k, int tiles_m, int tiles_n, int vec) {
   __shared__ GemmSmem sm;
-  // ---- tile of this workgroup: groups of kGGroup row tiles, n fastest inside
+  // ---- tile of this workgroup: groups of kGGroup row tiles, row tile fastest inside
   const int64_t bid = blockIdx.x;
   const int64_t per_group = static_cast<int64_t>(kGGroup) * tiles_n;
   const int64_t grp = bid / per_group;
@@ -110,7 +158,7 @@ void gemm_bf16_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
     }
     if (kt + 1 < n_kt) {
       store(cur ^ 1);
@@ -119,22 +167,7 @@ void gemm_bf16_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict
     __syncthreads();
   }
 
-  // ---- epilogue: lane holds rows q4*4 + r of column c16 of each 16 x 16 block
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int gc = n0 + wn + j * 16 + c16;
-      if (gc >= n) continue;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int64_t gr = m0 + wm + i * 16 + q4 * 4 + r;
-        if (gr >= M) continue;
-        float v = acc[i][j][r];
-        if (res) v += bf16_to_f32(res[gr * n + gc]);
-        y[gr * n + gc] = f32_to_bf16(v);
-      }
-    }
+  store_wave_tile(acc, res, y, M, n, m0 + wm, n0 + wn, c16, q4, vec != 0);
 }
 
 // Large tiles for k % 64 == 0: a 256 x 256 tile per workgroup of 8 waves,
@@ -157,7 +190,7 @@ struct GemmBuf {
 __global__ __launch_bounds__(kBThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void gemm_bf16_big_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ w,
                           const uint16_t* __restrict__ res, uint16_t* __restrict__ y, int64_t M,
-                          int n, int k, int tiles_m, int tiles_n) {
+                          int n, int k, int tiles_m, int tiles_n, int vec) {
   __shared__ GemmBuf s0, s1;
   const int64_t bid = blockIdx.x;
   const int64_t per_group = static_cast<int64_t>(kGGroup) * tiles_n;
@@ -224,7 +257,7 @@ void gemm_bf16_big_kernel(const uint16_t* __restrict__ x, const uint16_t* __rest
                                                        &src.a[ra * kGK + ((u ^ ((ra >> 1) & 7)) * 8)]));
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa, fb[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[j], fa, acc[i][j], 0, 0, 0);
       }
     }
   };
@@ -246,22 +279,7 @@ void gemm_bf16_big_kernel(const uint16_t* __restrict__ x, const uint16_t* __rest
     __syncthreads();
   }
   if (kt < n_kt) compute(B0{});
-
-#pragma unroll
-  for (int i = 0; i < 8; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int gc = n0 + wn + j * 16 + c16;
-      if (gc >= n) continue;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int64_t gr = m0 + wm + i * 16 + q4 * 4 + r;
-        if (gr >= M) continue;
-        float v = acc[i][j][r];
-        if (res) v += bf16_to_f32(res[gr * n + gc]);
-        y[gr * n + gc] = f32_to_bf16(v);
-      }
-    }
+  store_wave_tile(acc, res, y, M, n, m0 + wm, n0 + wn, c16, q4, vec != 0);
 }
 
 }  // namespace
@@ -280,6 +298,8 @@ extern "C" int rc_gemm_bf16(int64_t M, int32_t n, int32_t k, const void* x, cons
   const uint16_t* xs = static_cast<const uint16_t*>(x);
   const uint16_t* rs = static_cast<const uint16_t*>(residual);
   uint16_t* ys = static_cast<uint16_t*>(y);
+  const int vec = n % 4 == 0 && reinterpret_cast<uintptr_t>(y) % 8 == 0 &&
+                  reinterpret_cast<uintptr_t>(residual) % 8 == 0;
   if (k % kGK == 0 && M >= kBM && n >= kBN) {
     // whole 256-row tiles on the big kernel; a tail of fewer than 256 rows
     // goes to the 128 x 128 kernel below (a partial big tile would cost as
@@ -290,7 +310,7 @@ extern "C" int rc_gemm_bf16(int64_t M, int32_t n, int32_t k, const void* x, cons
     if (tm * tn > 0x7fffffff) return fail(RC_ERR_UNSUPPORTED, "grid too large");
     hipLaunchKernelGGL(gemm_bf16_big_kernel, dim3(static_cast<unsigned>(tm * tn)), dim3(kBThreads), 0,
                        stream, xs, static_cast<const uint16_t*>(w), rs, ys, M_main, n, k,
-                       static_cast<int>(tm), tn);
+                       static_cast<int>(tm), tn, vec);
     if (int st = check_launch("rc_gemm_bf16")) return st;
     if (M_main == M) return RC_OK;
     xs += M_main * k;
@@ -304,6 +324,6 @@ extern "C" int rc_gemm_bf16(int64_t M, int32_t n, int32_t k, const void* x, cons
   if (blocks > 0x7fffffff) return fail(RC_ERR_UNSUPPORTED, "grid too large");
   hipLaunchKernelGGL(gemm_bf16_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kGThreads), 0,
                      stream, xs, static_cast<const uint16_t*>(w), rs, ys, M, n, k,
-                     static_cast<int>(tiles_m), tiles_n);
+                     static_cast<int>(tiles_m), tiles_n, vec);
   return check_launch("rc_gemm_bf16");
 }

@@ -49,6 +49,31 @@ def test_gemm_small_against_fp64(M, n, k, res):
     np.testing.assert_allclose(y.cpu().double().numpy(), want.numpy(), rtol=8e-3, atol=2e-3)
 
 
+@pytest.mark.parametrize("M,n,k,shift", [(300, 640, 256, 1), (300, 640, 256, 4), (100, 96, 64, 1), (513, 512, 128, 2)])
+def test_gemm_unaligned_output_and_residual(M, n, k, shift):
+    """Output and residual start `shift` elements into larger buffers: with a
+    2-byte or 4-byte aligned start the epilogue stores value by value, with
+    an 8-byte aligned one it stores packs of 4; both kernels (whole 256-row
+    tiles and the row tail). The sentinels around the output stay untouched."""
+    say(f"[gemm unaligned] M={M} n={n} k={k} shift={shift}")
+    g = torch.Generator().manual_seed(M + 3 * n + shift)
+    x = torch.randn((M, k), generator=g).to(torch.bfloat16)
+    w = (torch.randn((n, k), generator=g) / k ** 0.5).to(torch.bfloat16)
+    r = torch.randn((M, n), generator=g).to(torch.bfloat16)
+    rbuf = torch.zeros(M * n + 2 * shift, dtype=torch.bfloat16)
+    rbuf[shift:shift + M * n] = r.reshape(-1)
+    ybuf = torch.full((M * n + 2 * shift,), 7.0, dtype=torch.bfloat16, device=DEV)
+    out = ybuf[shift:shift + M * n].view(M, n)
+    res = rbuf.to(DEV)[shift:shift + M * n].view(M, n)
+    ops.gemm(x.to(DEV), w.to(DEV), res, out=out)
+    torch.cuda.synchronize()
+    yb = ybuf.cpu()
+    assert bool((yb[:shift] == 7.0).all()) and bool((yb[shift + M * n:] == 7.0).all())
+    want = x.double() @ w.double().T + r.double()
+    np.testing.assert_allclose(yb[shift:shift + M * n].view(M, n).double().numpy(), want.numpy(),
+                               rtol=8e-3, atol=2e-3)
+
+
 @pytest.mark.parametrize("M,n,k", [(4160, 28672, 4096), (4160, 4096, 14336), (24064, 6144, 4096)])
 def test_gemm_llama_shapes_sampled_rows(M, n, k):
     """The stack's projection shapes; 12 sampled rows checked in fp64."""

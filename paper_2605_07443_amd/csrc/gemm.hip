@@ -268,12 +268,18 @@ void gemm_bf16_big_kernel(const uint16_t* __restrict__ x, const uint16_t* __rest
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   int kt = 0;
+  // the scheduling barriers keep each tile's loads ahead of the MFMAs of the
+  // tile before it: left free, the scheduler sinks them to the end of that
+  // tile (less address-register pressure), where the wait right after them
+  // exposes the whole memory latency
   for (; kt + 1 < n_kt; kt += 2) {
     issue(kt + 1, B1{});
+    __builtin_amdgcn_sched_barrier(0);
     compute(B0{});
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (kt + 2 < n_kt) issue(kt + 2, B0{});
+    __builtin_amdgcn_sched_barrier(0);
     compute(B1{});
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();

@@ -235,7 +235,8 @@ def main():
     digest = {"rc_kv_assemble": source_digest("assemble.hip"),
               "rc_select_tokens": source_digest("select.hip"),
               "rc_selective_attention": source_digest("attention.hip"),
-              "rc_attention_mass": source_digest("mass.hip")}
+              "rc_attention_mass": source_digest("mass.hip"),
+              "rc_gemm_bf16": source_digest("gemm.hip")}
     if tr and tr.get("source_digest", {}).get(dominant) == digest[dominant]:
         traffic = tr.get("kernels", {}).get(dominant, {}).get("hbm_bytes")
     roofline = {"kernel": dominant, "bound": dk["bound"], "achieved": dk["achieved"],

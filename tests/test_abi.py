@@ -237,3 +237,41 @@ def test_paged_attention_validation(lib):
     assert call(shape=_shape(dtype=0)) == -2          # bf16 only
     assert call(shape=_shape(N=16385)) == -2
     assert call(pools=_pools(1, nb=0)) == -1
+
+
+@no_gpu
+def test_layer_calls_validation(lib):
+    """Host checks of the decoder-layer calls: bad sizes, NULL pointers and
+    aliasing fail with a status and a message before anything is enqueued;
+    zero rows succeed without a launch."""
+    def gemm(M=300, n=64, k=64, x=FAKE, w=FAKE + 8, res=None, y=FAKE + 16):
+        return lib.rc_gemm_bf16(M, n, k, x, w, res, y, None)
+
+    assert gemm(x=None) == -1 and gemm(w=None) == -1 and gemm(y=None) == -1
+    assert gemm(M=-1) == -1 and gemm(n=0) == -1
+    for k in (0, 4, 12, 100):
+        st, msg = _err(gemm(k=k), lib)
+        assert st == -1 and "k" in msg
+    st, msg = _err(gemm(res=FAKE + 16), lib)          # residual aliases the output
+    assert st == -1 and "alias" in msg
+    assert gemm(M=0) == 0
+
+    def norm(M=4, H=64, eps=1e-5, x=FAKE, g=FAKE + 8, y=FAKE + 16):
+        return lib.rc_rmsnorm(M, H, x, g, ctypes.c_float(eps), y, None)
+
+    assert norm(x=None) == -1 and norm(g=None) == -1
+    assert norm(H=12) == -1 and norm(H=0) == -1 and norm(M=-1) == -1
+    assert norm(H=8192 + 8) == -2
+    assert norm(eps=-1.0) == -1 and norm(eps=float("inf")) == -1 and norm(eps=float("nan")) == -1
+    assert norm(M=0) == 0
+
+    assert lib.rc_silu_mul(4, 12, FAKE, FAKE + 8, None) == -1
+    assert lib.rc_silu_mul(-1, 16, FAKE, FAKE + 8, None) == -1
+    assert lib.rc_silu_mul(4, 16, None, FAKE + 8, None) == -1
+    assert lib.rc_silu_mul(0, 16, FAKE, FAKE + 8, None) == 0
+
+    rows = ctypes.cast(FAKE + 32, ctypes.POINTER(ctypes.c_int32))
+    assert lib.rc_gather_rows(2, 8, 4, 24, FAKE, rows, FAKE + 8, None) == -1   # row_bytes % 16
+    assert lib.rc_gather_rows(0, 8, 4, 32, FAKE, rows, FAKE + 8, None) == -1
+    assert lib.rc_gather_rows(2, 8, 4, 32, None, rows, FAKE + 8, None) == -1
+    assert lib.rc_gather_rows(2, 8, 0, 32, FAKE, rows, FAKE + 8, None) == 0

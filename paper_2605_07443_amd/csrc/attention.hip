@@ -294,6 +294,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
   const size_t tile_step = static_cast<size_t>(kKT) * stride;
   u32x4 kreg[DIRECT ? 1 : KU], vreg[DIRECT ? 1 : KU];
   int pdelta[PAGED ? PK : 1];  // paged: rotation of each staged key (0: none)
+  int pseg[PAGED ? PK : 1] = {};  // paged: last segment starting at or before each slot's key
   // DIRECT: wave w fills rows 16w .. 16w+15 of both tiles with 4 + 4 loads;
   // lane l writes chunk l % 16 of row 16w + 4j + l / 16 and so fetches the
   // data chunk that the swizzle stores there. Keys past N repeat key N - 1
@@ -354,8 +355,13 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
         const uint16_t* vs = nullptr;
         int d = 0;
         if (j < N) {
-          const int sg = find_segment(s_psegs, S, j);
-          const int4 sgm = sg >= 0 ? s_psegs[sg] : int4{0, 0, -1, 0};
+          // tiles are staged in increasing order, so a slot's key only moves
+          // forward: advance its segment instead of searching for it
+          int sg = pseg[i];
+          while (sg + 1 < S && s_psegs[sg + 1].x <= j) ++sg;
+          pseg[i] = sg;
+          const int4 sg0 = s_psegs[sg];
+          const int4 sgm = (sg0.x <= j && j < sg0.x + sg0.y) ? sg0 : int4{0, 0, -1, 0};
           const bool fresh = sgm.z < 0 || ((s_sel[j >> 5] >> (j & 31)) & 1u);
           if (fresh) {
             const size_t o = (static_cast<size_t>(b) * N + j) * stride + static_cast<size_t>(g) * D + col0;

@@ -126,7 +126,7 @@ def main():
 
     _lib.load()  # fails loudly when the HIP library is not built
     dev = torch.device("cuda:0")
-    cfg = inputs.CONFIGS[args.config]
+    cfg = inputs.WORKLOADS[args.config]
     pct = cfg.pct if args.pct is None else args.pct
     k = cfg.k_for(pct)
     R = cfg.n_fresh + k

@@ -116,7 +116,7 @@ class Config:
 # recommendation prompts the paper evaluates (median 2.2K-3.0K tokens, items
 # the majority of the prompt, Sec. IV-B); layer shapes are Llama-3-8B-like
 # (32 Q heads, 8 KV heads, head_dim 128) except the tiny fp32 case.
-CONFIGS = {
+WORKLOADS = {
     1: Config("tiny-fp32", "f32", B=1, Hq=8, Hkv=8, D=64, rope_base=10000.0, F=32,
               hist_len=128, hist_pool=4, n_items=4, item_len=64, item_pool=16, sigma=0.05,
               pct=15),
@@ -141,7 +141,7 @@ SWEEP_PCTS = (0, 5, 10, 15, 25, 50, 100)
 ITEM_POOL_MASK = 1 << 1
 
 # Small shapes for tests: several attention tiles, ragged tails, GQA and MHA.
-TEST_CONFIGS = {
+TEST_WORKLOADS = {
     "tiny-bf16": Config("tiny-bf16", "bf16", B=2, Hq=8, Hkv=2, D=128, rope_base=500000.0,
                         F=16, hist_len=64, hist_pool=4, n_items=3, item_len=48, item_pool=12),
     "ragged-bf16": Config("ragged-bf16", "bf16", B=3, Hq=16, Hkv=4, D=128,

@@ -205,7 +205,7 @@ def test_window_transform_matches_oracle(lib):
     same per-position rows and rotations (their tables may split differently)."""
     from paper_2605_07443_amd import inputs, ops
     for name in ("miss-bf16", "ragged-bf16", "tiny-bf16"):
-        cfg = inputs.TEST_CONFIGS[name]
+        cfg = inputs.TEST_WORKLOADS[name]
         w = inputs.make(cfg, 9)
         segs = w.segs.numpy()
         for W in (0, 1, 3, 37, 64, cfg.N - 1, cfg.N):

@@ -36,7 +36,7 @@ SMALL = ["tiny-bf16", "ragged-bf16", "mha-d64-bf16", "miss-bf16", "tiny-f32-gqa"
 @pytest.mark.parametrize("lam,ph,pi", [(0.5, 15, 15), (0.0, 30, 20), (1.0, 50, 0), (0.3, 0, 40),
                                        (0.5, 100, 100)])
 def test_eq3_stepwise_small(name, lam, ph, pi):
-    cfg = inputs.TEST_CONFIGS[name]
+    cfg = inputs.TEST_WORKLOADS[name]
     kh, ki = cfg.k_split(ph, pi)
     say(f"[eq3] {name} lambda={lam} budgets=({kh},{ki}) N={cfg.N} B={cfg.B}")
     w = inputs.make(cfg, 300 + ph + pi, device=DEV)
@@ -45,7 +45,7 @@ def test_eq3_stepwise_small(name, lam, ph, pi):
 
 
 def test_eq3_config1_tiny_fp32():
-    cfg = inputs.CONFIGS[1]
+    cfg = inputs.WORKLOADS[1]
     kh, ki = cfg.k_split(30)
     say(f"[eq3] config 1 budgets=({kh},{ki})")
     w = inputs.make(cfg, 1000, device=DEV)
@@ -81,7 +81,7 @@ def test_lse_and_mass_shapes(dtype, Hq, Hkv, D, N):
 
 
 def test_lse_of_selected_rows_matches_full_rows():
-    cfg = inputs.TEST_CONFIGS["ragged-bf16"]
+    cfg = inputs.TEST_WORKLOADS["ragged-bf16"]
     w = inputs.make(cfg, 17, device=DEV)
     rows = torch.tensor([[0, 5, 6, 40, cfg.N - 1], [1, 2, 3, 100, 200], [7, 8, 9, 10, 11]],
                         dtype=torch.int32, device=DEV)
@@ -98,7 +98,7 @@ def test_lse_of_selected_rows_matches_full_rows():
 
 
 def test_mass_is_deterministic():
-    cfg = inputs.TEST_CONFIGS["tiny-bf16"]
+    cfg = inputs.TEST_WORKLOADS["tiny-bf16"]
     w = inputs.make(cfg, 23, device=DEV)
     _, lse = ops.selective_attention_lse(w.q, w.k_fresh, w.v_fresh)
     a = ops.attention_mass(w.q, w.k_fresh, lse)
@@ -110,7 +110,7 @@ def test_mass_is_deterministic():
 def test_split_topk_special_values_on_gpu():
     """Per-class selection on hand-made scores with NaN, +inf, ties and
     all-equal classes, against the oracle split top-k."""
-    cfg = inputs.TEST_CONFIGS["miss-bf16"]
+    cfg = inputs.TEST_WORKLOADS["miss-bf16"]
     w = inputs.make(cfg, 3, device=DEV)
     segs = ops.prepare_segments(w.segs, cfg.N, w.pools, DEV)
     rng = np.random.default_rng(4)
@@ -138,7 +138,7 @@ def test_split_topk_special_values_on_gpu():
 
 def test_eq3_selects_attention_sinks_on_gpu():
     """lambda = 0: item keys that every query attends to are selected."""
-    cfg = inputs.TEST_CONFIGS["tiny-bf16"]
+    cfg = inputs.TEST_WORKLOADS["tiny-bf16"]
     w = inputs.make(cfg, 41, device=DEV)
     u = torch.randn(cfg.D, generator=torch.Generator().manual_seed(5)).to(DEV)
     w.q[:] = u.to(w.q.dtype)
@@ -158,7 +158,7 @@ def test_eq3_full_workloads(cid):
     """Workload sizes in the launch configuration the benchmark times: the
     oracle's quadratic lse/mass work is checked for KV group 0 of the first
     and last request; scores, rows and patch everywhere."""
-    cfg = inputs.CONFIGS[cid]
+    cfg = inputs.WORKLOADS[cid]
     kh, ki = cfg.k_split(15)
     say(f"[eq3] config {cid} B={cfg.B} N={cfg.N} budgets=({kh},{ki})")
     w = inputs.make(cfg, 1000 * cid, device=DEV)

@@ -61,7 +61,7 @@ SMALL = ["tiny-bf16", "ragged-bf16", "mha-d64-bf16", "miss-bf16"]
 @pytest.mark.parametrize("name", SMALL)
 @pytest.mark.parametrize("pct", [0, 15, 100])
 def test_paged_equals_assembled_small(name, pct):
-    cfg = inputs.TEST_CONFIGS[name]
+    cfg = inputs.TEST_WORKLOADS[name]
     say(f"[paged] {name} pct={pct}")
     w = inputs.make(cfg, 500 + pct, device=DEV)
     say(f"  {_both(cfg, w, w.segs.numpy(), cfg.k_for(pct))}")
@@ -72,7 +72,7 @@ def test_paged_equals_assembled_small(name, pct):
 def test_sliding_window_both_paths(name, W):
     """The last W positions become fresh segments: they are always rows, carry
     fresh K/V, and both paths agree with each other and the oracle."""
-    cfg = inputs.TEST_CONFIGS[name]
+    cfg = inputs.TEST_WORKLOADS[name]
     say(f"[window] {name} W={W}")
     w = inputs.make(cfg, 600 + W, device=DEV)
     segs_w = ops.segments_with_window(w.segs.numpy(), cfg.N, W)
@@ -94,7 +94,7 @@ def test_sliding_window_both_paths(name, W):
 def test_paged_unsorted_rows_and_duplicates():
     """Rows in any order, with repeats, still read fresh K/V for every listed
     position and match the assembled path patched at the same rows."""
-    cfg = inputs.TEST_CONFIGS["ragged-bf16"]
+    cfg = inputs.TEST_WORKLOADS["ragged-bf16"]
     w = inputs.make(cfg, 77, device=DEV)
     segs = ops.prepare_segments(w.segs, cfg.N, w.pools, DEV)
     cos, sin = ops.rope_table(cfg.N, cfg.D, cfg.rope_base, DEV)
@@ -117,7 +117,7 @@ def test_paged_unsorted_rows_and_duplicates():
 def test_paged_full_workloads(cid, stride):
     """Workload sizes in the benchmark's launch configuration: exact equality
     with the assembled path everywhere, oracle check on sampled rows."""
-    cfg = inputs.CONFIGS[cid]
+    cfg = inputs.WORKLOADS[cid]
     say(f"[paged] config {cid} B={cfg.B} N={cfg.N} S={cfg.n_items + 2}")
     w = inputs.make(cfg, 1000 * cid, device=DEV)
     say(f"  {_both(cfg, w, w.segs.numpy(), cfg.k, stride=stride)}")

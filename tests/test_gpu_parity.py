@@ -35,7 +35,7 @@ SMALL = ["tiny-bf16", "ragged-bf16", "mha-d64-bf16", "miss-bf16", "tiny-f32-gqa"
 @pytest.mark.parametrize("name", SMALL)
 @pytest.mark.parametrize("pct", [0, 15, 40, 100])
 def test_stepwise_small(name, pct):
-    cfg = inputs.TEST_CONFIGS[name]
+    cfg = inputs.TEST_WORKLOADS[name]
     say(f"[stepwise] {name} pct={pct} N={cfg.N} B={cfg.B}")
     w = inputs.make(cfg, 100 + pct, device=DEV)
     stats, _ = run_stepwise(cfg, w, cfg.k_for(pct), DEV)
@@ -43,7 +43,7 @@ def test_stepwise_small(name, pct):
 
 
 def test_stepwise_config1_tiny_fp32():
-    cfg = inputs.CONFIGS[1]
+    cfg = inputs.WORKLOADS[1]
     say(f"[stepwise] config 1 N={cfg.N}")
     w = inputs.make(cfg, 1000, device=DEV)
     stats, _ = run_stepwise(cfg, w, cfg.k, DEV)
@@ -51,7 +51,7 @@ def test_stepwise_config1_tiny_fp32():
 
 
 def test_planted_heavy_hitters_selected_on_gpu():
-    cfg = inputs.TEST_CONFIGS["tiny-bf16"]
+    cfg = inputs.TEST_WORKLOADS["tiny-bf16"]
     w = inputs.make(cfg, 5, device=DEV, planted=6)
     _, r = run_stepwise(cfg, w, cfg.k, DEV)
     rows = r["rows"].cpu().numpy()
@@ -143,7 +143,7 @@ def test_attention_fp32_full_and_selected():
 @pytest.mark.parametrize("name", ["tiny-bf16", "tiny-f32-gqa", "miss-bf16"])
 def test_full_ratio_equals_full_prefill_on_gpu(name):
     """Selecting every cached token = Full-Recompute, bit for bit on the GPU."""
-    cfg = inputs.TEST_CONFIGS[name]
+    cfg = inputs.TEST_WORKLOADS[name]
     w = inputs.make(cfg, 31, device=DEV)
     segs = ops.prepare_segments(w.segs, cfg.N, w.pools, DEV)
     cos, sin = ops.rope_table(cfg.N, cfg.D, cfg.rope_base, DEV)
@@ -157,7 +157,7 @@ def test_full_ratio_equals_full_prefill_on_gpu(name):
 
 @pytest.mark.parametrize("pct", [0, 10, 50])
 def test_zero_perturbation_equals_full_prefill_on_gpu(pct):
-    cfg = inputs.TEST_CONFIGS["ragged-bf16"]
+    cfg = inputs.TEST_WORKLOADS["ragged-bf16"]
     w = inputs.make(cfg, 32, device=DEV, sigma=0.0)
     segs = ops.prepare_segments(w.segs, cfg.N, w.pools, DEV)
     cos, sin = ops.rope_table(cfg.N, cfg.D, cfg.rope_base, DEV)
@@ -170,7 +170,7 @@ def test_zero_perturbation_equals_full_prefill_on_gpu(pct):
 
 
 def test_instruction_rows_equal_full_prefill_at_any_noise():
-    cfg = inputs.TEST_CONFIGS["tiny-bf16"]
+    cfg = inputs.TEST_WORKLOADS["tiny-bf16"]
     w = inputs.make(cfg, 33, device=DEV, sigma=0.3)
     segs = ops.prepare_segments(w.segs, cfg.N, w.pools, DEV)
     cos, sin = ops.rope_table(cfg.N, cfg.D, cfg.rope_base, DEV)
@@ -185,7 +185,7 @@ def test_instruction_rows_equal_full_prefill_at_any_noise():
 
 
 def test_pipeline_is_deterministic():
-    cfg = inputs.TEST_CONFIGS["ragged-bf16"]
+    cfg = inputs.TEST_WORKLOADS["ragged-bf16"]
     w = inputs.make(cfg, 34, device=DEV)
     segs = ops.prepare_segments(w.segs, cfg.N, w.pools, DEV)
     cos, sin = ops.rope_table(cfg.N, cfg.D, cfg.rope_base, DEV)
@@ -234,7 +234,7 @@ def test_single_token_segments_and_all_cached_prompt():
 
 
 def test_scores_in_special_values_match_oracle():
-    cfg = inputs.TEST_CONFIGS["ragged-bf16"]
+    cfg = inputs.TEST_WORKLOADS["ragged-bf16"]
     w = inputs.make(cfg, 35, device=DEV)
     segs = ops.prepare_segments(w.segs, cfg.N, w.pools, DEV)
     rng = np.random.default_rng(0)
@@ -257,7 +257,7 @@ def test_scores_in_special_values_match_oracle():
 @pytest.mark.parametrize("cid,pct,stride", [(2, 15, 16), (3, 10, 32), (5, 15, 64),
                                             (4, 0, 16), (4, 15, 16), (4, 50, 64), (4, 100, 128)])
 def test_stepwise_full_workloads(cid, pct, stride):
-    cfg = inputs.CONFIGS[cid]
+    cfg = inputs.WORKLOADS[cid]
     say(f"[full workload] config {cid} pct={pct} B={cfg.B} N={cfg.N} pools="
         f"{cfg.hist_pool}x{cfg.hist_len},{cfg.item_pool}x{cfg.item_len}")
     w = inputs.make(cfg, 1000 * cid, device=DEV)
@@ -269,7 +269,7 @@ def test_stepwise_full_workloads(cid, pct, stride):
 
 @pytest.mark.parametrize("cid,stride", [(2, 64), (3, 256)])
 def test_full_prefill_full_workloads(cid, stride):
-    cfg = inputs.CONFIGS[cid]
+    cfg = inputs.WORKLOADS[cid]
     say(f"[full prefill] config {cid}")
     g = torch.Generator(device=DEV).manual_seed(cid)
     q = torch.randn((cfg.B, cfg.N, cfg.Hq, cfg.D), generator=g, device=DEV).to(torch.bfloat16)

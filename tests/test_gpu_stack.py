@@ -142,14 +142,14 @@ def _run_and_check(cfg, n_layers, Hd, I, seed, W, pct, requests=None):
                                     ("mha-d64-bf16", 3)])
 @pytest.mark.parametrize("pct", [15, 50])
 def test_stack_small(name, W, pct):
-    cfg = inputs.TEST_CONFIGS[name]
+    cfg = inputs.TEST_WORKLOADS[name]
     say(f"[stack] {name} W={W} pct={pct}")
     stats, _ = _run_and_check(cfg, 3, 256, 512, 70 + pct, W, pct)
     say(f"  rel L2 per request {stats}")
 
 
 def test_stack_every_row_selected_equals_full():
-    cfg = inputs.TEST_CONFIGS["ragged-bf16"]
+    cfg = inputs.TEST_WORKLOADS["ragged-bf16"]
     x, layers, pools, segs0 = inputs.make_stack(cfg, 81, 3, 256, 512, device=DEV)
     segs = ops.prepare_segments(segs0, cfg.N, pools[0], DEV)
     cos, sin = ops.rope_table(cfg.N, cfg.D, cfg.rope_base, DEV)
@@ -163,7 +163,7 @@ def test_stack_every_row_selected_equals_full():
 def test_stack_full_workload_llama_dims():
     """Workload 2 with Llama-3-8B layer dimensions (H 4096, MLP 14336), two
     layers; the oracle checks requests 0 and B-1 (the GPU runs all eight)."""
-    cfg = inputs.CONFIGS[2]
+    cfg = inputs.WORKLOADS[2]
     say("[stack] config 2, 2 layers, H=4096")
     stats, _ = _run_and_check(cfg, 2, 4096, 14336, 2002, 16, 15, requests=[0, cfg.B - 1])
     say(f"  rel L2 {stats}")

@@ -39,7 +39,7 @@ def _oracle_gather(cfg, w, tmap):
 @pytest.mark.parametrize("name", ["tiny-bf16", "ragged-bf16", "miss-bf16", "mha-d64-bf16",
                                   "tiny-f32-gqa"])
 def test_prototype_gather_bitexact_and_selection(name):
-    cfg = inputs.TEST_CONFIGS[name]
+    cfg = inputs.TEST_WORKLOADS[name]
     say(f"[tokens] {name}")
     tw = inputs.make_prototypes(cfg, 31, device=DEV, n_protos=97)
     w = tw.w
@@ -71,7 +71,7 @@ def test_prototype_gather_bitexact_and_selection(name):
 
 @pytest.mark.parametrize("name", ["tiny-bf16", "miss-bf16"])
 def test_segment_map_gather_equals_segment_gather(name):
-    cfg = inputs.TEST_CONFIGS[name]
+    cfg = inputs.TEST_WORKLOADS[name]
     w = inputs.make(cfg, 41, device=DEV)
     segs = ops.prepare_segments(w.segs, cfg.N, w.pools, DEV)
     cos, sin = ops.rope_table(cfg.N, cfg.D, cfg.rope_base, DEV)
@@ -88,7 +88,7 @@ def test_segment_map_gather_equals_segment_gather(name):
 def test_host_pinned_pool_equals_device_pool(cid, n_protos):
     """Prototype pool in pinned host memory (read over PCIe by the kernel)
     gives the same bytes as the same pool in HBM."""
-    cfg = inputs.TEST_CONFIGS[cid] if isinstance(cid, str) else inputs.CONFIGS[cid]
+    cfg = inputs.TEST_WORKLOADS[cid] if isinstance(cid, str) else inputs.WORKLOADS[cid]
     say(f"[host pool] {cid} n_protos={n_protos}")
     tw = inputs.make_prototypes(cfg, 51, device=DEV, n_protos=n_protos)
     w = tw.w
@@ -111,7 +111,7 @@ def test_host_pinned_pool_equals_device_pool(cid, n_protos):
 def test_overlapped_eq3_selection_equals_sequential(cid):
     """The gather from a pinned host pool on a second stream, overlapping the
     first layer in full, yields exactly the sequential result."""
-    cfg = inputs.TEST_CONFIGS[cid] if isinstance(cid, str) else inputs.CONFIGS[cid]
+    cfg = inputs.TEST_WORKLOADS[cid] if isinstance(cid, str) else inputs.WORKLOADS[cid]
     say(f"[overlap] {cid}")
     tw = inputs.make_prototypes(cfg, 61, device=DEV, n_protos=4096)
     w = tw.w

@@ -178,7 +178,7 @@ def test_zero_noise_realigned_keys_equal_fresh_keys(name):
     """With no cache noise, re-aligning a block stored at local positions to its
     absolute position reproduces the freshly computed key (up to rounding): this
     ties delta = dst_start and the rotation direction to the model's own RoPE."""
-    cfg = inputs.TEST_CONFIGS[name]
+    cfg = inputs.TEST_WORKLOADS[name]
     w = inputs.make(cfg, 11, sigma=0.0)
     cos, sin = O.rope_table(cfg.N, cfg.D, cfg.rope_base)
     pools = [(H(a), H(b)) for a, b in w.pools]
@@ -201,7 +201,7 @@ def test_deviation_matches_half_normal_closed_form(sigma):
     so d = sum of Hkv*D half-normals: E[d] = Hkv*D*sigma*sqrt(2/pi),
     sd(d) = sigma*sqrt(Hkv*D*(1 - 2/pi)). A dropped head, an L2 norm or an added
     V term moves the mean by many standard errors."""
-    cfg = inputs.CONFIGS[1]
+    cfg = inputs.WORKLOADS[1]
     w = inputs.make(cfg, 1000, sigma=sigma)
     cos, sin = O.rope_table(cfg.N, cfg.D, cfg.rope_base)
     pools = [(H(a), H(b)) for a, b in w.pools]
@@ -263,7 +263,7 @@ def test_topk_special_values_and_errors():
 
 
 def test_planted_heavy_hitters_are_selected():
-    cfg = inputs.CONFIGS[1]
+    cfg = inputs.WORKLOADS[1]
     w = inputs.make(cfg, 7, planted=10)
     cos, sin = O.rope_table(cfg.N, cfg.D, cfg.rope_base)
     pools = [(H(a), H(b)) for a, b in w.pools]
@@ -354,7 +354,7 @@ def _run(cfg, w, k):
 def test_full_ratio_equals_full_prefill(name):
     """Selecting every cached token patches every row with fresh KV and
     recomputes every row: the output is the full prefill, bit for bit."""
-    cfg = inputs.TEST_CONFIGS[name]
+    cfg = inputs.TEST_WORKLOADS[name]
     w = inputs.make(cfg, 21)
     r = _run(cfg, w, cfg.n_reused)
     full = O.attention(H(w.q), H(w.k_fresh), H(w.v_fresh))
@@ -366,7 +366,7 @@ def test_full_ratio_equals_full_prefill(name):
 @pytest.mark.parametrize("name", ["tiny-f32-gqa", "tiny-bf16"])
 @pytest.mark.parametrize("pct", [0, 15, 50])
 def test_zero_perturbation_equals_full_prefill(name, pct):
-    cfg = inputs.TEST_CONFIGS[name]
+    cfg = inputs.TEST_WORKLOADS[name]
     w = inputs.make(cfg, 22, sigma=0.0)
     r = _run(cfg, w, cfg.k_for(pct))
     full = O.attention(H(w.q), H(w.k_fresh), H(w.v_fresh))
@@ -380,7 +380,7 @@ def test_zero_perturbation_equals_full_prefill(name, pct):
 def test_noise_changes_output_but_not_instruction_rows(name):
     """Instruction rows attend only fresh keys, so they equal the full prefill at
     any noise level; cached rows that were not recomputed do see the noise."""
-    cfg = inputs.TEST_CONFIGS[name]
+    cfg = inputs.TEST_WORKLOADS[name]
     w = inputs.make(cfg, 23, sigma=0.2)
     r = _run(cfg, w, cfg.k)
     full = O.attention(H(w.q), H(w.k_fresh), H(w.v_fresh))
@@ -393,7 +393,7 @@ def test_noise_changes_output_but_not_instruction_rows(name):
 
 
 def test_cache_miss_segments_are_always_recomputed():
-    cfg = inputs.TEST_CONFIGS["miss-bf16"]
+    cfg = inputs.TEST_WORKLOADS["miss-bf16"]
     w = inputs.make(cfg, 24)
     r = _run(cfg, w, 0)
     fresh = [i for dst, ln, p, _ in w.segs[0].tolist() if p < 0 for i in range(dst, dst + ln)]
@@ -406,7 +406,7 @@ def test_cache_miss_segments_are_always_recomputed():
 # ---------------------------------------------------------------------------
 
 def test_generator_is_deterministic_and_tiles_the_prompt():
-    cfg = inputs.TEST_CONFIGS["ragged-bf16"]
+    cfg = inputs.TEST_WORKLOADS["ragged-bf16"]
     a = inputs.make(cfg, 5)
     b = inputs.make(cfg, 5)
     c = inputs.make(cfg, 6)
@@ -423,7 +423,7 @@ def test_generator_is_deterministic_and_tiles_the_prompt():
 
 @pytest.mark.parametrize("cid", [2, 3, 4, 5])
 def test_item_ids_follow_the_config(cid):
-    cfg = inputs.CONFIGS[cid]
+    cfg = inputs.WORKLOADS[cid]
     hist, items = inputs.sample_ids(cfg, 1000 * cid)
     assert items.shape == (cfg.B, cfg.n_items)
     assert int(items.min()) >= 0 and int(items.max()) < cfg.item_pool
@@ -433,7 +433,7 @@ def test_item_ids_follow_the_config(cid):
 
 
 def test_zipf_ids_are_heavy_tailed():
-    cfg = inputs.CONFIGS[2].with_(B=400)
+    cfg = inputs.WORKLOADS[2].with_(B=400)
     _, items = inputs.sample_ids(cfg, 3)
     counts = torch.bincount(items.reshape(-1), minlength=cfg.item_pool).sort(descending=True).values
     c = counts.numpy().astype(np.float64)
@@ -449,7 +449,7 @@ def test_zipf_ids_are_heavy_tailed():
 
 
 def test_config_sizes():
-    c = inputs.CONFIGS
+    c = inputs.WORKLOADS
     assert [c[i].N for i in range(1, 6)] == [416, 3008, 8160, 4096, 2080]
     assert [c[i].k for i in range(1, 6)] == [58, 442, 810, 600, 308]
     assert [c[i].R for i in range(1, 6)] == [90, 506, 874, 696, 340]
@@ -461,7 +461,7 @@ def test_config_sizes():
 # ---------------------------------------------------------------------------
 
 def test_window_makes_the_last_positions_fresh_and_keeps_the_rest():
-    cfg = inputs.TEST_CONFIGS["miss-bf16"]
+    cfg = inputs.TEST_WORKLOADS["miss-bf16"]
     w = inputs.make(cfg, 3)
     segs = w.segs.numpy()
     N = cfg.N
@@ -475,7 +475,7 @@ def test_window_makes_the_last_positions_fresh_and_keeps_the_rest():
 
 
 def test_window_recomputes_the_window_rows_with_fresh_kv():
-    cfg = inputs.TEST_CONFIGS["tiny-bf16"]
+    cfg = inputs.TEST_WORKLOADS["tiny-bf16"]
     w = inputs.make(cfg, 5)
     W = 20
     segs_w = O.segments_with_window(w.segs.numpy(), cfg.N, W)
@@ -510,7 +510,7 @@ def test_window_recomputes_the_window_rows_with_fresh_kv():
 def test_token_gather_equals_segment_gather(name):
     """The per-position map derived from a segment table reproduces the
     (separately pinned) segment gather bit for bit, rotation included."""
-    cfg = inputs.TEST_CONFIGS[name]
+    cfg = inputs.TEST_WORKLOADS[name]
     w = inputs.make(cfg, 12)
     cos, sin = O.rope_table(cfg.N, cfg.D, cfg.rope_base)
     pools = [(H(a), H(b)) for a, b in w.pools]
@@ -522,7 +522,7 @@ def test_token_gather_equals_segment_gather(name):
 
 
 def test_token_gather_names_rows_and_rotates_by_delta():
-    cfg = inputs.TEST_CONFIGS["tiny-bf16"]
+    cfg = inputs.TEST_WORKLOADS["tiny-bf16"]
     tw = inputs.make_prototypes(cfg, 4, n_protos=50, sigma=0.0)
     w = tw.w
     pools = [(H(a), H(b)) for a, b in w.pools]

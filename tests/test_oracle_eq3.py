@@ -127,7 +127,7 @@ def _assembled(cfg, seed, sigma=None):
 
 @pytest.mark.parametrize("name", ["tiny-f32-gqa", "tiny-bf16"])
 def test_score_reduces_to_its_terms(name):
-    cfg = inputs.TEST_CONFIGS[name]
+    cfg = inputs.TEST_WORKLOADS[name]
     w, ka, va = _assembled(cfg, 21)
     kf, vf, segs = H(w.k_fresh), H(w.v_fresh), w.segs.numpy()
     mass = O.attention_mass(H(w.q), kf).astype(np.float32)
@@ -160,7 +160,7 @@ def test_divergence_matches_half_normal_closed_form(sigma):
     cached token is a sum of 2 * Hkv * D half-normals: mean 2 n sigma sqrt(2/pi),
     sd sigma sqrt(2 n (1 - 2/pi)) with n = Hkv * D. Dropping the V term halves
     the mean."""
-    cfg = inputs.CONFIGS[1]
+    cfg = inputs.WORKLOADS[1]
     w, ka, va = _assembled(cfg, 1000, sigma)
     kf, vf = H(w.k_fresh), H(w.v_fresh)
     mass = np.zeros((cfg.B, cfg.Hkv, cfg.N), np.float32)
@@ -232,7 +232,7 @@ def _eq3(cfg, w, lam, kh, ki):
 
 
 def test_eq3_full_budgets_give_fresh_kv():
-    cfg = inputs.TEST_CONFIGS["tiny-bf16"]
+    cfg = inputs.TEST_WORKLOADS["tiny-bf16"]
     w = inputs.make(cfg, 31)
     r = _eq3(cfg, w, 0.5, cfg.n_hist_reused, cfg.n_item_reused)
     np.testing.assert_array_equal(r["k_asm"], H(w.k_fresh))
@@ -243,7 +243,7 @@ def test_eq3_full_budgets_give_fresh_kv():
 def test_eq3_selects_attention_sinks_and_drifted_history():
     """lambda = 0: item keys that every query attends to strongly are
     selected; lambda = 1: history tokens with 20x cache noise are selected."""
-    cfg = inputs.TEST_CONFIGS["tiny-f32-gqa"]
+    cfg = inputs.TEST_WORKLOADS["tiny-f32-gqa"]
     w = inputs.make(cfg, 41)
     q = w.q.clone()
     u = torch.randn(cfg.D, generator=torch.Generator().manual_seed(5))
@@ -268,7 +268,7 @@ def test_eq3_selects_attention_sinks_and_drifted_history():
 
 
 def test_eq3_intermediates_are_consistent():
-    cfg = inputs.TEST_CONFIGS["miss-bf16"]
+    cfg = inputs.TEST_WORKLOADS["miss-bf16"]
     w = inputs.make(cfg, 51)
     kh, ki = cfg.k_split(20, 30)
     r = _eq3(cfg, w, 0.4, kh, ki)

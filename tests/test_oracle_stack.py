@@ -59,7 +59,7 @@ def test_rope_at_matches_the_pinned_rotation():
 
 
 def _small_case(seed=3, n_layers=3):
-    cfg = inputs.TEST_CONFIGS["tiny-f32-gqa"]
+    cfg = inputs.TEST_WORKLOADS["tiny-f32-gqa"]
     w = inputs.make(cfg, seed)
     H, I = 96, 128
     x = np.random.default_rng(seed).standard_normal((cfg.B, cfg.N, H)).astype(np.float32)

@@ -213,8 +213,14 @@ int rc_rerope(const rc_shape* shape, void* k, const int32_t* delta, const float*
  *    order: rows [B, n_fresh + k] int32. Bit-exact for given scores.
  * 3. Patch (patch != 0): K_asm/V_asm rows of the k selected cached positions
  *    are overwritten with K_fresh/V_fresh rows.
- * n_fresh must equal the number of fresh positions of every request
- * (requests whose table disagrees get a truncated or padded row list).
+ * n_fresh is the number of fresh positions of every request. It is an
+ * argument because the segment table lives on the device and the row count
+ * R = n_fresh + k must be known on the host to size `rows` without a
+ * synchronisation. A request whose table disagrees with it is marked in its
+ * row list instead of being reported here (the library cannot read the table
+ * without a synchronisation): fewer fresh positions leave the unfilled tail
+ * of its list at -1, more fresh positions drop the tail and set the last
+ * entry to -1. rc_selective_attention turns a -1 row into NaN outputs.
  * Requires 0 <= k <= N - n_fresh; rows may be NULL when n_fresh + k == 0.
  * Hq in the shape is unused.
  * Errors: INVALID_ARG for NULL pointers, bad shape, k or n_fresh out of
@@ -232,7 +238,10 @@ int rc_select_tokens(const rc_shape* shape, const rc_segment* segs, int32_t S, i
  * fp32 accumulation and online softmax; bf16 inputs use the matrix cores.
  * q: [B, N, Hq, D]; rows: [B, R] int32, ascending within a request (any
  * order is correct, ascending is fastest); k, v: [B, N, Hkv, D];
- * out: [B, R, Hq, D]. Rows outside [0, N) are clamped into range.
+ * out: [B, R, Hq, D]. A listed row outside [0, N) (for instance the -1
+ * that rc_select_tokens writes for a request whose segment table disagrees
+ * with n_fresh) makes its output row NaN; no memory outside the tensors is
+ * read.
  * Errors: INVALID_ARG for NULL pointers, bad shape, R < 0, R != N without
  * rows, non-finite or non-positive scale; UNSUPPORTED for D, dtype, or a
  * bf16 group size that does not divide 128. R == 0 enqueues nothing (out may
@@ -246,8 +255,9 @@ int rc_selective_attention(const rc_shape* shape, const void* q, const int32_t* 
  *   lse[b,r,h] = ln sum_{j<=p} exp(scale * Q[b,p,h] . K[b,j,g]),
  * into lse: device [B, R, Hq] fp32 (fp32 sums of the unrounded exponentials).
  * With rows NULL (every row of the first layer, Sec. III-C.2b) this is the
- * input rc_attention_mass takes. Errors: those of rc_selective_attention,
- * and INVALID_ARG for a NULL lse with R > 0. */
+ * input rc_attention_mass takes. A row outside [0, N) makes its lse entries
+ * NaN, like its outputs. Errors: those of rc_selective_attention, and
+ * INVALID_ARG for a NULL lse with R > 0. */
 int rc_selective_attention_lse(const rc_shape* shape, const void* q, const int32_t* rows,
                                int32_t R, const void* k, const void* v, float scale, void* out,
                                float* lse, hipStream_t stream);
@@ -286,13 +296,17 @@ int rc_attention_mass(const rc_shape* shape, const void* q, const void* k, const
  *    the lower position -- together with the n_fresh fresh positions, in
  *    ascending order: rows [B, n_fresh + k_hist + k_item] int32. Bit-exact
  *    for given scores. A budget above its class's count in some request
- *    takes the whole class and pads the row list with N - 1.
+ *    takes the whole class and leaves the unfilled tail of that request's
+ *    row list at -1 (n_fresh disagreeing with the table is marked as in
+ *    rc_select_tokens).
  * 3. Patch (patch != 0): K_asm/V_asm rows of the selected cached positions
  *    get the K_fresh/V_fresh rows.
  * k_fresh/v_fresh/k_asm/v_asm: [B, N, Hkv, D]. Hq in the shape is unused.
  * Errors: INVALID_ARG for NULL pointers, bad shape, budgets or n_fresh out
- * of range, lambda outside [0, 1], mask bits beyond pool 7; UNSUPPORTED for
- * D, dtype, N > 16384, S > 1024. */
+ * of range, lambda outside [0, 1], lambda = 1 with k_item > 0 (item tokens
+ * have no divergence term, so every item score would be 0 and the item
+ * budget would take the lowest positions instead of a ranking), mask bits
+ * beyond pool 7; UNSUPPORTED for D, dtype, N > 16384, S > 1024. */
 int rc_select_tokens_eq3(const rc_shape* shape, const rc_segment* segs, int32_t S,
                          int32_t n_fresh, uint32_t item_pool_mask, float lambda, int32_t k_hist,
                          int32_t k_item, const float* mass, const void* k_fresh,

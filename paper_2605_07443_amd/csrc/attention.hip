@@ -233,7 +233,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
 
   // ---- the two query vectors (S^T columns) this lane serves
   int pos[2], head[2], row[2];
-  bool valid[2];
+  bool valid[2], bad[2];
   int pmax = 0, pmin = 0x7fffffff;
 #pragma unroll
   for (int nb = 0; nb < 2; ++nb) {
@@ -242,10 +242,13 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
     const int hh = m - rl * G;
     const int r = tile * BR + rl - shift;
     valid[nb] = hh < G && r >= 0 && r < R;
+    bad[nb] = false;
     int p = 0;
     if (valid[nb]) {
       p = SELECTIVE ? rows[static_cast<size_t>(b) * R + r] : r;
-      p = min(max(p, 0), N - 1);
+      // a listed position outside [0, N) computes row 0 and stores NaN
+      bad[nb] = p < 0 || p >= N;
+      p = bad[nb] ? 0 : p;
       pmax = max(pmax, p);
       pmin = min(pmin, p);
     }
@@ -727,7 +730,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
       l += __shfl_xor(l, 32, 64);
       if (valid[nb] && q4 == 0)
         lse[(static_cast<size_t>(b) * R + row[nb]) * Hq + head[nb]] =
-            (m_run[nb] * scale_log2e + __log2f(l)) * 0.69314718055994531f;
+            bad[nb] ? __builtin_nanf("") : (m_run[nb] * scale_log2e + __log2f(l)) * 0.69314718055994531f;
     }
   }
 
@@ -739,8 +742,9 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
     uint16_t* orow = out + ((static_cast<size_t>(b) * R + row[nb]) * Hq + head[nb]) * D;
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
-      const u32x2 w = {pack_bf16x2(o[db][nb][0] * inv, o[db][nb][1] * inv),
-                       pack_bf16x2(o[db][nb][2] * inv, o[db][nb][3] * inv)};
+      const u32x2 w = bad[nb] ? u32x2{0x7fc07fc0u, 0x7fc07fc0u}
+                              : u32x2{pack_bf16x2(o[db][nb][0] * inv, o[db][nb][1] * inv),
+                                      pack_bf16x2(o[db][nb][2] * inv, o[db][nb][3] * inv)};
       *reinterpret_cast<u32x2*>(orow + db * 16 + q4 * 4) = w;
     }
   }
@@ -768,7 +772,8 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(const float* __restrict__
   const int r = static_cast<int>(br % R);
   const int b = static_cast<int>(br / R);
   int p = rows ? rows[static_cast<size_t>(b) * R + r] : r;
-  p = min(max(p, 0), N - 1);
+  const bool bad = p < 0 || p >= N;   // computes row 0, stores NaN
+  p = bad ? 0 : p;
   const int g = h / (Hq / Hkv);
   const float* qrow = q + ((static_cast<size_t>(b) * N + p) * Hq + h) * D;
   for (int d = lane; d < D; d += 64) s_q[wave][d] = qrow[d];
@@ -807,9 +812,10 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(const float* __restrict__
     m = m_new;
   }
   float* orow = out + ((static_cast<size_t>(b) * R + r) * Hq + h) * D;
+  const float nan = __builtin_nanf("");
 #pragma unroll
-  for (int e = 0; e < PER; ++e) orow[lane * PER + e] = acc[e] / l;
-  if (lse && lane == 0) lse[(static_cast<size_t>(b) * R + r) * Hq + h] = m + logf(l);
+  for (int e = 0; e < PER; ++e) orow[lane * PER + e] = bad ? nan : acc[e] / l;
+  if (lse && lane == 0) lse[(static_cast<size_t>(b) * R + r) * Hq + h] = bad ? nan : m + logf(l);
 }
 
 }  // namespace

@@ -5,13 +5,14 @@
 //   deviation_kernel  one wave per position: L1 distance between the fresh
 //                     and the assembled key row (HBM-bound, 16-byte loads,
 //                     wave reduction)
-//   topk_kernel       one workgroup per request, keys held in registers:
-//                     range-adaptive radix select of the k-th largest score
-//                     key (11-bit digits, LDS histograms), then the fresh and
-//                     selected positions written in ascending order from
-//                     per-wave counts
-//   patch_kernel      one wave per listed row: copies the fresh K/V row over
-//                     the assembled one when the position is cached
+//   topk_kernel       keys held in registers: range-adaptive radix select of
+//                     the k-th largest score key (11-bit digits, LDS
+//                     histograms), then the fresh and selected positions
+//                     written in ascending order from per-wave counts; with
+//                     the patch, several workgroups per request select the
+//                     same rows and each copies the fresh K/V rows of its
+//                     share of the selected cached positions over the
+//                     assembled ones (one wave per row)
 #include "rc_common.h"
 
 namespace rc {
@@ -60,6 +61,8 @@ __global__ __launch_bounds__(64 * kDevWaves) void deviation_kernel(
 // ---------------------------------------------------------------------- top-k
 
 constexpr int kTopkMaxPer = 16;  // positions per thread at most
+constexpr int kPatchList = 2048;  // list slots of one workgroup's share of the patch
+constexpr int kSelectTargetWgs = 256;  // workgroups of a patching launch: one per compute unit
 constexpr int kBins = 2048;                           // 11-bit digits
 constexpr int kDigitBits = 11;
 constexpr int kCoarse = 64;                           // coarse bins of 32 digits
@@ -107,7 +110,7 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
                                     __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
 }
 
-// One workgroup per request. Candidates are positions outside fresh
+// Workgroups (part, b) of request b. Candidates are positions outside fresh
 // segments; each belongs to one of two classes: class 0 (history, or every
 // cached position when item_mask is 0) and class 1 (blocks of the pools set
 // in item_mask). Class c keeps its k_c largest keys, key of position i =
@@ -127,11 +130,17 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
 // histograms rotate over three LDS buffers, so that a pass costs two
 // barriers. The output is written from per-(j, wave) counts with one
 // barrier: each lane's slot is the count of taken positions before it.
-template <int NC, int NJ, int TPB>
+// Every part of a request computes the same selection; part 0 writes rows,
+// and with PATCH part p copies the rows of the cached positions whose output
+// slots are p, p + parts, ... (collected in an LDS list, one wave per row).
+template <int NC, int NJ, int TPB, bool PATCH>
 __global__ __launch_bounds__(TPB) void topk_kernel(
     const float* __restrict__ scores, const int4* __restrict__ segs, int S, int N,
-    uint32_t item_mask, int k0, int k1, int R, int32_t* __restrict__ rows) {
+    uint32_t item_mask, int k0, int k1, int R, int32_t* __restrict__ rows, int row_units,
+    const char* __restrict__ k_fresh, const char* __restrict__ v_fresh, char* __restrict__ k_asm,
+    char* __restrict__ v_asm) {
   __shared__ int4 s_segs[kMaxSegments];
+  __shared__ int s_list[PATCH ? kPatchList : 1];        // this workgroup's share of the patch
   __shared__ uint32_t s_hist[3][kBins];
   __shared__ uint32_t s_coarse[3][kCoarse];
   constexpr int W = TPB / 64;                           // waves
@@ -140,7 +149,9 @@ __global__ __launch_bounds__(TPB) void topk_kernel(
   __shared__ uint32_t s_bounds[2][3];                   // per class: min key, max key, candidates
   __shared__ uint32_t s_sel[2];                         // boundary digit, keys above it
 
-  const int b = blockIdx.x;
+  const int b = blockIdx.y;
+  const int part = blockIdx.x;   // which share of the patch (every part selects)
+  const int parts = gridDim.x;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -167,6 +178,9 @@ __global__ __launch_bounds__(TPB) void topk_kernel(
   if (tid < kCoarse) {
     s_coarse[0][tid] = 0u;
     s_coarse[1][tid] = 0u;
+  }
+  if constexpr (PATCH) {
+    for (int q = tid; q < kPatchList; q += TPB) s_list[q] = -1;
   }
   if (tid < 2) {
     s_bounds[tid][0] = 0xffffffffu;
@@ -362,11 +376,60 @@ __global__ __launch_bounds__(TPB) void topk_kernel(
                       (e1 && r1 < static_cast<uint32_t>(need[1]));
     const uint32_t out = gt_before + min(t0_before, static_cast<uint32_t>(need[0])) +
                          min(t1_before, static_cast<uint32_t>(need[1])) + lanes_below(__ballot(take));
-    if (take && out < static_cast<uint32_t>(R))
-      rows[static_cast<size_t>(b) * R + out] = j * TPB + tid;
+    // A list longer than R (more fresh positions than n_fresh) loses its
+    // tail; its last entry is then -1 so that the request is recognisable.
+    if (part == 0 && take && out < static_cast<uint32_t>(R))
+      rows[static_cast<size_t>(b) * R + out] =
+          (total > R && out == static_cast<uint32_t>(R - 1)) ? -1 : j * TPB + tid;
+    if constexpr (PATCH) {
+      // selected cached positions of slots part, part + parts, ... go to this
+      // workgroup's list
+      const uint32_t c = (cls >> (2 * j)) & 3u;
+      if (take && (c == 1u || c == 2u) && out < static_cast<uint32_t>(R) &&
+          static_cast<int>(out % parts) == part)
+        s_list[out / parts] = j * TPB + tid;
+    }
   }
-  // pad a short list (inconsistent n_fresh) with the last position
-  for (int r = total + tid; r < R; r += TPB) rows[static_cast<size_t>(b) * R + r] = N - 1;
+  // a list shorter than R (fewer fresh positions than n_fresh, or a budget
+  // above its class's size) is padded with -1
+  if (part == 0)
+    for (int r = total + tid; r < R; r += TPB) rows[static_cast<size_t>(b) * R + r] = -1;
+
+  if constexpr (PATCH) {
+    // (iii) heavy-hitter update: one wave per listed position copies the
+    // fresh K and V rows over the assembled ones (16-byte units)
+    __syncthreads();
+    const int slots = (R + parts - 1) / parts;
+    for (int sl = wave; sl < slots; sl += TPB / 64) {
+      const int i = s_list[sl];
+      if (i < 0) continue;
+      const size_t off = (static_cast<size_t>(b) * N + i) * row_units;
+      const u32x4* kf = reinterpret_cast<const u32x4*>(k_fresh) + off;
+      const u32x4* vf = reinterpret_cast<const u32x4*>(v_fresh) + off;
+      u32x4* ka = reinterpret_cast<u32x4*>(k_asm) + off;
+      u32x4* va = reinterpret_cast<u32x4*>(v_asm) + off;
+      for (int u0 = 0; u0 < row_units; u0 += 128) {
+        const int u1 = u0 + lane, u2 = u0 + 64 + lane;
+        u32x4 ka1, va1, ka2, va2;
+        if (u1 < row_units) {
+          ka1 = __builtin_nontemporal_load(kf + u1);
+          va1 = __builtin_nontemporal_load(vf + u1);
+        }
+        if (u2 < row_units) {
+          ka2 = __builtin_nontemporal_load(kf + u2);
+          va2 = __builtin_nontemporal_load(vf + u2);
+        }
+        if (u1 < row_units) {
+          ka[u1] = ka1;
+          va[u1] = va1;
+        }
+        if (u2 < row_units) {
+          ka[u2] = ka2;
+          va[u2] = va2;
+        }
+      }
+    }
+  }
 }
 
 // ------------------------------------------------------------------ Eq. (3)
@@ -426,67 +489,6 @@ __global__ __launch_bounds__(64 * kDevWaves) void eq3_score_kernel(
       for (int g = lane; g < Hkv; g += 64) m += mass[(static_cast<size_t>(b) * Hkv + g) * N + i];
     m = wave_sum(m);
     if (lane == 0 && i < N) scores[static_cast<size_t>(b) * N + i] = (1.f - lambda) * m + lambda * d;
-  }
-}
-
-// ---------------------------------------------------------------------- patch
-
-constexpr int kPatchThreads = 256;  // one wave per selected row
-
-// Wave w of workgroup x copies row x * 4 + w of the list when its position is
-// cached: the lanes test 64 segments at a time against the position (one
-// ballot), so no segment table is staged and no barrier is needed.
-__global__ __launch_bounds__(kPatchThreads) void patch_kernel(
-    const int4* __restrict__ segs, int S, int N, const int32_t* __restrict__ rows, int R,
-    int row_units, const char* __restrict__ k_fresh, const char* __restrict__ v_fresh,
-    char* __restrict__ k_asm, char* __restrict__ v_asm) {
-  const int b = blockIdx.y;
-  const int lane = threadIdx.x & 63;
-  const int r = blockIdx.x * (kPatchThreads / 64) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  if (r >= R) return;
-  const int i = rows[static_cast<size_t>(b) * R + r];
-  if (i < 0 || i >= N) return;
-  bool cached = false;
-  for (int s0 = 0; s0 < S; s0 += 64) {
-    const int sidx = s0 + lane;
-    bool hit = false;
-    int pool = -1;
-    if (sidx < S) {
-      const int4 g = segs[static_cast<size_t>(b) * S + sidx];
-      hit = g.x <= i && i - g.x < g.y;
-      pool = g.z;
-    }
-    const uint64_t m = __ballot(hit);
-    if (m != 0) {
-      cached = __builtin_amdgcn_readlane(pool, __builtin_ctzll(m)) >= 0;
-      break;
-    }
-  }
-  if (!cached) return;  // fresh position (or in no segment)
-  const size_t off = (static_cast<size_t>(b) * N + i) * row_units;
-  const u32x4* kf = reinterpret_cast<const u32x4*>(k_fresh) + off;
-  const u32x4* vf = reinterpret_cast<const u32x4*>(v_fresh) + off;
-  u32x4* ka = reinterpret_cast<u32x4*>(k_asm) + off;
-  u32x4* va = reinterpret_cast<u32x4*>(v_asm) + off;
-  for (int u0 = 0; u0 < row_units; u0 += 128) {
-    const int u1 = u0 + lane, u2 = u0 + 64 + lane;
-    u32x4 k1, v1, k2, v2;
-    if (u1 < row_units) {
-      k1 = __builtin_nontemporal_load(kf + u1);
-      v1 = __builtin_nontemporal_load(vf + u1);
-    }
-    if (u2 < row_units) {
-      k2 = __builtin_nontemporal_load(kf + u2);
-      v2 = __builtin_nontemporal_load(vf + u2);
-    }
-    if (u1 < row_units) {
-      ka[u1] = k1;
-      va[u1] = v1;
-    }
-    if (u2 < row_units) {
-      ka[u2] = k2;
-      va[u2] = v2;
-    }
   }
 }
 
@@ -565,40 +567,48 @@ int select_impl(const rc_shape* shape, const rc_segment* segs, int32_t S, int32_
   }
   if (R > 0) {
     // NC = 1 when class 1 takes nothing (its candidates are simply not
-    // taken); NJ = positions per thread (rounded up to an even count past 8)
+    // taken); NJ = positions per thread (rounded up to an even count past 8).
+    // With the patch, several workgroups per request each select (the same
+    // rows, deterministically) and copy their share of the selected rows, so
+    // that the copy runs on many compute units; only the first writes rows.
+    const bool do_patch = patch && ksum > 0;
+    int parts = 1;
+    if (do_patch) {
+      parts = max((kSelectTargetWgs + B - 1) / B, (R + kPatchList - 1) / kPatchList);
+      parts = min(parts, 64);
+      if ((R + parts - 1) / parts > kPatchList) return fail(RC_ERR_UNSUPPORTED, "R=%d too large", R);
+    }
+    const char* kf = static_cast<const char*>(k_fresh);
+    const char* vf = static_cast<const char*>(v_fresh);
+    char* ka = static_cast<char*>(k_asm);
+    char* va = static_cast<char*>(v_asm);
     auto launch = [&](auto kern, int tpb) {
-      hipLaunchKernelGGL(kern, dim3(B), dim3(tpb), 0, stream, sc, segs4, S, N, item_mask, k0, k1,
-                         R, rows);
+      hipLaunchKernelGGL(kern, dim3(parts, B), dim3(tpb), 0, stream, sc, segs4, S, N, item_mask, k0,
+                         k1, R, rows, row_units, kf, vf, ka, va);
     };
-    auto by_chunks = [&](auto nc) {
+    auto by_chunks = [&](auto nc, auto pt) {
       constexpr int NC = decltype(nc)::value;
+      constexpr bool PT = decltype(pt)::value;
       switch ((N + 1023) / 1024) {
-        case 1: launch(topk_kernel<NC, 1, 1024>, 1024); break;
-        case 2: launch(topk_kernel<NC, 2, 1024>, 1024); break;
-        case 3: launch(topk_kernel<NC, 3, 1024>, 1024); break;
-        case 4: launch(topk_kernel<NC, 4, 1024>, 1024); break;
-        case 5: launch(topk_kernel<NC, 5, 1024>, 1024); break;
-        case 6: launch(topk_kernel<NC, 6, 1024>, 1024); break;
-        case 7: launch(topk_kernel<NC, 7, 1024>, 1024); break;
-        case 8: launch(topk_kernel<NC, 8, 1024>, 1024); break;
-        case 9: case 10: launch(topk_kernel<NC, 10, 1024>, 1024); break;
-        case 11: case 12: launch(topk_kernel<NC, 12, 1024>, 1024); break;
-        default: launch(topk_kernel<NC, 16, 1024>, 1024); break;
+        case 1: launch(topk_kernel<NC, 1, 1024, PT>, 1024); break;
+        case 2: launch(topk_kernel<NC, 2, 1024, PT>, 1024); break;
+        case 3: launch(topk_kernel<NC, 3, 1024, PT>, 1024); break;
+        case 4: launch(topk_kernel<NC, 4, 1024, PT>, 1024); break;
+        case 5: launch(topk_kernel<NC, 5, 1024, PT>, 1024); break;
+        case 6: launch(topk_kernel<NC, 6, 1024, PT>, 1024); break;
+        case 7: launch(topk_kernel<NC, 7, 1024, PT>, 1024); break;
+        case 8: launch(topk_kernel<NC, 8, 1024, PT>, 1024); break;
+        case 9: case 10: launch(topk_kernel<NC, 10, 1024, PT>, 1024); break;
+        case 11: case 12: launch(topk_kernel<NC, 12, 1024, PT>, 1024); break;
+        default: launch(topk_kernel<NC, 16, 1024, PT>, 1024); break;
       }
     };
+    using One = std::integral_constant<int, 1>;
+    using Two = std::integral_constant<int, 2>;
     if (k1 > 0)
-      by_chunks(std::integral_constant<int, 2>{});
+      do_patch ? by_chunks(Two{}, std::true_type{}) : by_chunks(Two{}, std::false_type{});
     else
-      by_chunks(std::integral_constant<int, 1>{});
-    if (int st = check_launch(what)) return st;
-  }
-  if (patch && ksum > 0) {
-    const int rows_per_wg = kPatchThreads / 64;
-    dim3 grid((R + rows_per_wg - 1) / rows_per_wg, B);
-    hipLaunchKernelGGL(patch_kernel, grid, dim3(kPatchThreads), 0, stream, segs4, S, N, rows, R,
-                       row_units, static_cast<const char*>(k_fresh),
-                       static_cast<const char*>(v_fresh), static_cast<char*>(k_asm),
-                       static_cast<char*>(v_asm));
+      do_patch ? by_chunks(One{}, std::true_type{}) : by_chunks(One{}, std::false_type{});
     if (int st = check_launch(what)) return st;
   }
   return RC_OK;
@@ -627,6 +637,10 @@ extern "C" int rc_select_tokens_eq3(const rc_shape* shape, const rc_segment* seg
   rc::clear_error();
   if (item_pool_mask >> rc::kMaxPools)
     return rc::fail(RC_ERR_INVALID_ARG, "item_pool_mask names pools beyond %d", rc::kMaxPools);
+  // item tokens are scored (1 - lambda) * mass: at lambda = 1 every item score
+  // is 0 and an item budget would take the lowest positions, not a ranking
+  if (!scores_in && lambda == 1.f && k_item > 0)
+    return rc::fail(RC_ERR_INVALID_ARG, "lambda = 1 leaves item tokens unranked (k_item=%d > 0)", k_item);
   return rc::select_impl(shape, segs, S, n_fresh, true, item_pool_mask, lambda, k_hist, k_item,
                          mass, k_fresh, v_fresh, k_asm, v_asm, scores_in, scores_out, rows, patch,
                          stream, "rc_select_tokens_eq3");

@@ -63,6 +63,7 @@ class Config:
     sigma: float = 0.05
     pct: int = 15
     miss_items: tuple = ()   # item slots served as fresh (cache misses)
+    miss_hist: bool = False  # history served as fresh (a cache miss)
 
     @property
     def N(self) -> int:
@@ -70,7 +71,7 @@ class Config:
 
     @property
     def n_fresh(self) -> int:
-        return self.F + len(self.miss_items) * self.item_len
+        return self.F + len(self.miss_items) * self.item_len + (self.hist_len if self.miss_hist else 0)
 
     @property
     def n_reused(self) -> int:
@@ -86,7 +87,7 @@ class Config:
 
     @property
     def n_hist_reused(self) -> int:
-        return self.hist_len
+        return 0 if self.miss_hist else self.hist_len
 
     @property
     def n_item_reused(self) -> int:
@@ -156,6 +157,10 @@ TEST_WORKLOADS = {
     "tiny-f32-gqa": Config("tiny-f32-gqa", "f32", B=2, Hq=8, Hkv=2, D=64, rope_base=10000.0,
                            F=9, hist_len=40, hist_pool=3, n_items=3, item_len=21,
                            item_pool=7, pct=25),
+    # every segment a cache miss: nothing is reused, every position is fresh
+    "allfresh-bf16": Config("allfresh-bf16", "bf16", B=2, Hq=8, Hkv=2, D=128,
+                            rope_base=500000.0, F=16, hist_len=64, hist_pool=4, n_items=3,
+                            item_len=48, item_pool=12, miss_items=(0, 1, 2), miss_hist=True),
 }
 
 
@@ -244,7 +249,8 @@ def segment_table(cfg: Config, hist: torch.Tensor, items: torch.Tensor) -> torch
     segs = torch.empty((cfg.B, S, 4), dtype=torch.int32)
     for b in range(cfg.B):
         segs[b, 0] = torch.tensor([0, cfg.F, -1, 0])
-        segs[b, 1] = torch.tensor([cfg.F, cfg.hist_len, 0, int(hist[b])])
+        segs[b, 1] = (torch.tensor([cfg.F, cfg.hist_len, -1, 0]) if cfg.miss_hist
+                      else torch.tensor([cfg.F, cfg.hist_len, 0, int(hist[b])]))
         for i in range(cfg.n_items):
             dst = cfg.F + cfg.hist_len + i * cfg.item_len
             if i in cfg.miss_items:

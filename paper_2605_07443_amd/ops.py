@@ -9,6 +9,7 @@ from __future__ import annotations
 
 import ctypes
 import math
+import os
 from dataclasses import dataclass
 
 import numpy as np
@@ -17,6 +18,25 @@ import torch
 from . import _lib
 from ._lib import RcPool, RcShape, check
 from .inputs import LayerWeights
+
+
+# Debug mode (RCLLM_DEBUG=1): row lists are checked after the selection and
+# before attention, at the cost of a synchronisation per call. The library
+# marks a request whose segment table disagrees with n_fresh (or whose budget
+# exceeds its class) with -1 entries in its row list instead of failing, since
+# it cannot read device tables without a synchronisation.
+DEBUG = os.environ.get("RCLLM_DEBUG", "") not in ("", "0")
+
+
+def check_rows(rows: torch.Tensor, N: int, what: str) -> None:
+    """Raise if any listed row lies outside [0, N); names the requests."""
+    if rows.numel() == 0:
+        return
+    r = rows.detach().cpu()
+    bad = ((r < 0) | (r >= N)).any(dim=1).nonzero().flatten().tolist()
+    if bad:
+        raise RuntimeError(f"{what}: requests {bad} have row-list entries outside [0, {N}) "
+                           f"(segment table disagreeing with n_fresh, or a budget above its class)")
 
 
 def _dtype_code(t: torch.Tensor) -> int:
@@ -216,6 +236,8 @@ def select_tokens(segs: Segments, k: int, k_fresh, v_fresh, k_asm, v_asm, scores
         None if scores_in is None else _dev(scores_in, "scores_in"),
         None if scores_out is None else _dev(scores_out, "scores_out"),
         _dev(rows, "rows"), 1 if patch else 0, _stream(stream)))
+    if DEBUG:
+        check_rows(rows, N, "rc_select_tokens")
     return rows, (scores_out if scores_out is not None else scores_in)
 
 
@@ -230,6 +252,8 @@ def selective_attention(q, k, v, rows=None, scale=None, out=None, stream=None):
         raise ValueError("rows must be int32 [B, R]")
     scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
     out = torch.empty((B, R, Hq, D), dtype=q.dtype, device=q.device) if out is None else out
+    if DEBUG and rows is not None:
+        check_rows(rows, N, "rc_selective_attention")
     check(_lib.load().rc_selective_attention(
         ctypes.byref(_shape(B, N, Hq, Hkv, D, _dtype_code(q))), _dev(q, "q"),
         None if rows is None else _dev(rows, "rows"), R, _dev(k, "k"), _dev(v, "v"),
@@ -306,6 +330,8 @@ def select_tokens_eq3(segs: Segments, item_mask: int, lam: float, k_hist: int, k
         None if scores_in is None else _dev(scores_in, "scores_in"),
         None if scores_out is None else _dev(scores_out, "scores_out"),
         _dev(rows, "rows"), 1 if patch else 0, _stream(stream)))
+    if DEBUG:
+        check_rows(rows, N, "rc_select_tokens_eq3")
     return rows, (scores_out if scores_out is not None else scores_in)
 
 

@@ -198,6 +198,10 @@ def test_select_eq3_validation(lib):
     assert call(rows=None) == -1
     assert call(scores_out=None) == -1
     assert call(shape=_shape(N=16385)) == -2
+    # lambda = 1 scores every item token 0: an item budget is rejected, a
+    # history-only budget is not
+    st, msg = _err(call(lam=1.0, kh=5, ki=1), lib)
+    assert st == -1 and "lambda = 1" in msg
 
 
 def test_window_transform_matches_oracle(lib):

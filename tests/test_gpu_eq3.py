@@ -153,7 +153,7 @@ def test_eq3_selects_attention_sinks_on_gpu():
         assert set(sinks) <= set(rows[b].tolist())
 
 
-@pytest.mark.parametrize("cid", [2, 5])
+@pytest.mark.parametrize("cid", [2, 3, 4, 5])
 def test_eq3_full_workloads(cid):
     """Workload sizes in the launch configuration the benchmark times: the
     oracle's quadratic lse/mass work is checked for KV group 0 of the first

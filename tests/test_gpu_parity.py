@@ -29,7 +29,7 @@ def _lib_loaded():
 
 # ---------------------------------------------------------------- small shapes
 
-SMALL = ["tiny-bf16", "ragged-bf16", "mha-d64-bf16", "miss-bf16", "tiny-f32-gqa"]
+SMALL = ["tiny-bf16", "ragged-bf16", "mha-d64-bf16", "miss-bf16", "tiny-f32-gqa", "allfresh-bf16"]
 
 
 @pytest.mark.parametrize("name", SMALL)
@@ -255,7 +255,8 @@ def test_scores_in_special_values_match_oracle():
 # ------------------------------------------------------------- full workloads
 
 @pytest.mark.parametrize("cid,pct,stride", [(2, 15, 16), (3, 10, 32), (5, 15, 64),
-                                            (4, 0, 16), (4, 15, 16), (4, 50, 64), (4, 100, 128)])
+                                            (4, 0, 16), (4, 5, 16), (4, 10, 16), (4, 15, 16),
+                                            (4, 25, 32), (4, 50, 64), (4, 100, 128)])
 def test_stepwise_full_workloads(cid, pct, stride):
     cfg = inputs.WORKLOADS[cid]
     say(f"[full workload] config {cid} pct={pct} B={cfg.B} N={cfg.N} pools="
@@ -267,7 +268,7 @@ def test_stepwise_full_workloads(cid, pct, stride):
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("cid,stride", [(2, 64), (3, 256)])
+@pytest.mark.parametrize("cid,stride", [(2, 64), (3, 256), (4, 128), (5, 256)])
 def test_full_prefill_full_workloads(cid, stride):
     cfg = inputs.WORKLOADS[cid]
     say(f"[full prefill] config {cid}")
@@ -346,3 +347,83 @@ def test_patch_with_more_than_64_segments():
     kp, vp = O.patch(segs_h, rows_h, H(kf), H(vf), ka0, va0)
     np.testing.assert_array_equal(H(ka), kp)
     np.testing.assert_array_equal(H(va), vp)
+
+
+# ------------------------------------------------- cache misses, bad row lists
+
+def test_all_fresh_prompt_equals_full_prefill():
+    """Every segment a cache miss (computed on the fly, Sec. III-C.2a): nothing
+    is reused, the assembled K/V are the fresh rows, no position is selected
+    (k = 0 at any ratio), every position is a row, and the output is the
+    Full-Recompute output bit for bit."""
+    cfg = inputs.TEST_WORKLOADS["allfresh-bf16"]
+    assert cfg.n_reused == 0
+    w = inputs.make(cfg, 41, device=DEV)
+    segs = ops.prepare_segments(w.segs, cfg.N, w.pools, DEV)
+    cos, sin = ops.rope_table(cfg.N, cfg.D, cfg.rope_base, DEV)
+    bufs = ops.selective_prefill(w.q, w.k_fresh, w.v_fresh, w.pools, segs, cfg.k_for(15), cos, sin)
+    full = ops.full_prefill(w.q, w.k_fresh, w.v_fresh)
+    torch.cuda.synchronize()
+    assert torch.equal(bufs.rows.cpu(), torch.arange(cfg.N, dtype=torch.int32).repeat(cfg.B, 1))
+    assert torch.equal(bufs.k_asm, w.k_fresh) and torch.equal(bufs.v_asm, w.v_fresh)
+    assert bool((bufs.scores == 0).all())
+    assert torch.equal(bufs.out, full)
+
+
+def test_row_list_marks_inconsistent_fresh_count():
+    """A segment table whose fresh count differs from the n_fresh passed in
+    (possible only when the caller builds the table itself): the library
+    cannot read the device table on the host, so it marks the request's row
+    list with -1 (short list: unfilled tail; long list: last entry), the
+    attention writes NaN for those rows and leaves the others exact, and the
+    wrapper's debug check names the request."""
+    cfg = inputs.TEST_WORKLOADS["tiny-bf16"]
+    w = inputs.make(cfg, 42, device=DEV)
+    good = ops.prepare_segments(w.segs, cfg.N, w.pools, DEV)
+    cos, sin = ops.rope_table(cfg.N, cfg.D, cfg.rope_base, DEV)
+    k = cfg.k
+    k_asm, v_asm = ops.kv_assemble(w.pools, good, w.k_fresh, w.v_fresh, cos, sin)
+    rows_ok, sc = ops.select_tokens(good, k, w.k_fresh, w.v_fresh, k_asm.clone(), v_asm.clone(),
+                                    patch=False)
+    for delta in (3, -3):
+        bad = ops.Segments(dev=good.dev, host=good.host, n_fresh=good.n_fresh + delta, N=good.N)
+        rows, _ = ops.select_tokens(bad, k, w.k_fresh, w.v_fresh, k_asm.clone(), v_asm.clone(),
+                                    scores_in=sc, patch=False)
+        torch.cuda.synchronize()
+        r, ok = rows.cpu().numpy(), rows_ok.cpu().numpy()
+        R = r.shape[1]
+        if delta > 0:     # short list: the taken rows, then -1
+            np.testing.assert_array_equal(r[:, :ok.shape[1]], ok)
+            assert (r[:, ok.shape[1]:] == -1).all()
+        else:             # long list: truncated, last entry -1
+            np.testing.assert_array_equal(r[:, :R - 1], ok[:, :R - 1])
+            assert (r[:, R - 1] == -1).all()
+        with pytest.raises(RuntimeError, match="requests \\[0, 1\\]"):
+            ops.check_rows(rows, cfg.N, "test")
+        out = ops.selective_attention(w.q, k_asm, v_asm, rows)
+        torch.cuda.synchronize()
+        o = H(out)
+        neg = r < 0
+        assert np.isnan(O.as_f32(o[neg])).all()
+        good_rows = np.where(neg, 0, r).astype(np.int32)
+        ref = O.attention(H(w.q), H(k_asm), H(v_asm), rows=good_rows)
+        assert_attn_close(o[~neg], ref[~neg], "bf16", "rows next to marked rows")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_attention_rows_outside_range_give_nan(dtype):
+    """Listed rows outside [0, N) yield NaN outputs (and lse), nothing else
+    changes: the kernels read only in-range rows."""
+    B, N, Hq, Hkv, D = 2, 200, 8, 2, 128
+    g = torch.Generator(device="cpu").manual_seed(9)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    q, k, v = (torch.randn((B, N, h, D), generator=g).to(tdt) for h in (Hq, Hkv, Hkv))
+    rows = torch.tensor([[-1, 3, 50, 199], [0, N, 120, 1 << 30]], dtype=torch.int32)
+    out, lse = ops.selective_attention_lse(q.to(DEV), k.to(DEV), v.to(DEV), rows.to(DEV))
+    torch.cuda.synchronize()
+    bad = np.array([[1, 0, 0, 0], [0, 1, 0, 1]], bool)
+    o, l = O.as_f32(H(out)), lse.cpu().numpy()
+    assert np.isnan(o[bad]).all() and np.isnan(l[bad]).all()
+    assert np.isfinite(o[~bad]).all() and np.isfinite(l[~bad]).all()
+    ref = O.attention(H(q), H(k), H(v), rows=np.where(bad, 0, rows.numpy()).astype(np.int32))
+    assert_attn_close(H(out)[~bad], ref[~bad], dtype, "in-range rows")

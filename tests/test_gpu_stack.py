@@ -6,10 +6,10 @@ called through the C ABI.
 
 Bar: rows bit-exact on identical scores (the oracle's top-k of the GPU's
 layer-1 scores); layer-1 scores within 2e-2 relative of the oracle's (the
-fresh keys come from a bf16 projection chain); final hidden states of the
-selected rows within 3e-2 relative L2 of the fp64 oracle (about nine bf16
-roundings per layer at 2^-9 each, three layers); every row selected equals
-the full recompute exactly."""
+fresh keys come from a bf16 projection chain); final hidden states checked
+row by row against the fp64 oracle: every selected row within 3e-2 relative
+L2 and every element within 0.1 of its row's RMS (bounds derived at
+_check_rows); every row selected equals the full recompute exactly."""
 import numpy as np
 import pytest
 import torch
@@ -99,6 +99,33 @@ def _rel_l2(a, b):
     return float(np.linalg.norm(a - b) / np.linalg.norm(b))
 
 
+# Per-row bounds. A layer rounds to bf16 about nine times (norm output, Q/K/V,
+# attention output, O projection + residual, norm, gate/up, SwiGLU, down
+# projection + residual), each a relative error of at most 2^-9; the errors
+# of a final state are sums of many such independent roundings carried
+# through the projections, so they are close to Gaussian, with a measured
+# relative L2 of 0.5-0.6% per request over two or three layers. Per row:
+# relative L2 at most 3e-2 (5x the measured error); per element at most
+# 0.1 of the row's RMS (about 16 standard deviations of a 0.6% error, so a
+# single wrong element of a row, one wrong head or a misplaced row fails it).
+ROW_REL_L2 = 3e-2
+ROW_MAX_ABS_OF_RMS = 0.1
+
+
+def _check_rows(got, ref, what):
+    """got, ref: [R, H] final states of one request's selected rows."""
+    err = np.abs(got - ref)
+    rms = np.sqrt(np.mean(ref * ref, axis=1))
+    rel = np.linalg.norm(got - ref, axis=1) / np.linalg.norm(ref, axis=1)
+    worst = int(np.argmax(rel))
+    assert rel.max() <= ROW_REL_L2, f"{what}: row {worst} relative L2 {rel.max():.3e}"
+    ratio = err.max(axis=1) / rms
+    r = int(np.argmax(ratio))
+    assert ratio.max() <= ROW_MAX_ABS_OF_RMS, (
+        f"{what}: row {r} max |err| {err[r].max():.3e} = {ratio.max():.3f} x its RMS")
+    return float(rel.max()), float(ratio.max())
+
+
 def _run_and_check(cfg, n_layers, Hd, I, seed, W, pct, requests=None):
     x, layers, pools, segs0 = inputs.make_stack(cfg, seed, n_layers, Hd, I, device=DEV)
     segs_np = ops.segments_with_window(segs0.numpy(), cfg.N, W) if W else segs0.numpy()
@@ -133,8 +160,8 @@ def _run_and_check(cfg, n_layers, Hd, I, seed, W, pct, requests=None):
         np.testing.assert_allclose(sc_g[b], sc_o, rtol=2e-2, atol=1e-2, err_msg=f"scores b={b}")
         got = O.as_f32(H(out[b])).astype(np.float64)
         e = _rel_l2(got, xo[0])
-        assert e <= 3e-2, f"request {b}: relative L2 error {e:.3e}"
-        stats[b] = round(e, 5)
+        row_rel, row_max = _check_rows(got, xo[0], f"request {b}")
+        stats[b] = (round(e, 5), round(row_rel, 5), round(row_max, 4))
     return stats, (x, layers, pools, segs, cos, sin, k, out, rows)
 
 
@@ -145,7 +172,7 @@ def test_stack_small(name, W, pct):
     cfg = inputs.TEST_WORKLOADS[name]
     say(f"[stack] {name} W={W} pct={pct}")
     stats, _ = _run_and_check(cfg, 3, 256, 512, 70 + pct, W, pct)
-    say(f"  rel L2 per request {stats}")
+    say(f"  per request (rel L2, worst row rel L2, worst row max|err|/RMS) {stats}")
 
 
 def test_stack_every_row_selected_equals_full():

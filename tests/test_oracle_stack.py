@@ -130,3 +130,125 @@ def test_exact_cache_makes_the_selected_rows_exact():
     sel_n, _ = O.decoder_stack_selective(x, layers, pools, segs, rows, cos, sin, cfg.Hq,
                                          cfg.rope_base, EPS, dt=0)
     assert np.abs(sel_n - want).max() > 1e-2
+
+
+# ---------------------------------------------------------------------------
+# Closed form of the whole block (no oracle code on the expected side).
+# With the query projection zero every score is 0, so each row's causal
+# softmax is uniform and the attention output of row p is the mean of the
+# value rows 0..p of its KV group. With gate rows [A; -A], up rows [B; B] and
+# down columns [C, -C] the MLP is C((A n) * (B n)), because
+# silu(t) - silu(-t) = t. One layer is then
+#     n  = x / sqrt(mean(x^2) + eps) * g_attn
+#     h  = x + concat_h(prefix-mean of V n over j <= p, group h // G) W_o^T
+#     n2 = h / sqrt(mean(h^2) + eps) * g_mlp
+#     x' = h + ((A n2) * (B n2)) C^T
+# which fixes the q/k/v split order, the GQA head-to-group map, the causal
+# mask (j <= p), the orientation of W_o, both residuals, both norm gains and
+# their places, the gate/up order and pairing, and the orientation of W_down.
+# ---------------------------------------------------------------------------
+
+def _closed_form_layers(n_layers, H, Hq, Hkv, D, m, seed):
+    rng = np.random.default_rng(seed)
+    layers = []
+    for _ in range(n_layers):
+        w_qkv = rng.standard_normal(((Hq + 2 * Hkv) * D, H)) / math.sqrt(H)
+        w_qkv[:Hq * D] = 0.0                                   # q = 0: uniform softmax
+        A = rng.standard_normal((m, H)) / math.sqrt(H)
+        Bm = rng.standard_normal((m, H)) / math.sqrt(H)
+        C = rng.standard_normal((H, m)) / math.sqrt(m)
+        layers.append(dict(
+            w_qkv=w_qkv.astype(np.float32),
+            w_o=(rng.standard_normal((H, Hq * D)) / math.sqrt(Hq * D)).astype(np.float32),
+            w_gu=np.concatenate([A, -A, Bm, Bm]).astype(np.float32),    # gate [A; -A], up [B; B]
+            w_down=np.concatenate([C, -C], axis=1).astype(np.float32),  # [C, -C]
+            g_attn=(1 + 0.2 * rng.standard_normal(H)).astype(np.float32),
+            g_mlp=(1 + 0.2 * rng.standard_normal(H)).astype(np.float32)))
+    return layers
+
+
+def _cf_norm(x, g):
+    return x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + EPS) * g
+
+
+def _cf_prefix_mean(v, upto):
+    """mean of v[0..p] for every p in upto: v [N, Hkv, D] -> [len(upto), Hkv, D]."""
+    csum = np.cumsum(v, axis=0)
+    return np.stack([csum[p] / (p + 1) for p in upto])
+
+
+def _cf_mlp(h, L, m):
+    n2 = _cf_norm(h, L["g_mlp"].astype(np.float64))
+    A = L["w_gu"][:m].astype(np.float64)
+    Bm = L["w_gu"][2 * m:3 * m].astype(np.float64)
+    C = L["w_down"][:, :m].astype(np.float64)
+    return h + ((n2 @ A.T) * (n2 @ Bm.T)) @ C.T
+
+
+def _cf_attend_rows(vals, rows, Hq, Hkv, Wo):
+    """Uniform causal attention of `rows` over value rows `vals` [N, Hkv, D],
+    heads mapped to groups h // (Hq / Hkv), through W_o."""
+    G = Hq // Hkv
+    pm = _cf_prefix_mean(vals, rows)                       # [R, Hkv, D]
+    heads = pm[:, np.arange(Hq) // G]                      # [R, Hq, D]
+    return heads.reshape(len(rows), -1) @ Wo.T
+
+
+@pytest.mark.parametrize("Hq,Hkv", [(4, 2), (6, 3), (4, 4)])
+def test_full_stack_matches_closed_form(Hq, Hkv):
+    B, N, H, D, m = 2, 11, 20, 8, 6
+    layers = _closed_form_layers(2, H, Hq, Hkv, D, m, seed=Hq * 10 + Hkv)
+    x = np.random.default_rng(3).standard_normal((B, N, H)).astype(np.float32)
+    got = O.decoder_stack_full(x, layers, Hq, Hkv, D, 500000.0, EPS)
+    X = x.astype(np.float64)
+    for L in layers:
+        Wv = L["w_qkv"][(Hq + Hkv) * D:].astype(np.float64)
+        Wo = L["w_o"].astype(np.float64)
+        nxt = np.empty_like(X)
+        for b in range(B):
+            n = _cf_norm(X[b], L["g_attn"].astype(np.float64))
+            v = (n @ Wv.T).reshape(N, Hkv, D)
+            h = X[b] + _cf_attend_rows(v, np.arange(N), Hq, Hkv, Wo)
+            nxt[b] = _cf_mlp(h, L, m)
+        X = nxt
+    # the oracle's attention stores its inputs and outputs in fp32
+    np.testing.assert_allclose(got, X, rtol=2e-6, atol=2e-6)
+
+
+def test_selective_stack_matches_closed_form():
+    """Later layers attend over their cache: pool value rows at cached
+    positions that are not listed, the listed rows' own projected values
+    elsewhere. Checks the gather's block and offset, the overwrite of listed
+    positions, and that later layers continue from the listed rows' states."""
+    Hq, Hkv, D, H, m, N = 4, 2, 8, 20, 6, 12
+    rng = np.random.default_rng(5)
+    # fresh [0, 3), pool 0 block 1 at [3, 8), pool 1 block 0 at [8, 12)
+    segs = np.array([[[0, 3, -1, 0], [3, 5, 0, 1], [8, 4, 1, 0]]], np.int32)
+    pools_by_layer = []
+    for _ in range(3):
+        p0 = [rng.standard_normal((2, 5, Hkv, D)).astype(np.float32) for _ in range(2)]
+        p1 = [rng.standard_normal((1, 4, Hkv, D)).astype(np.float32) for _ in range(2)]
+        pools_by_layer.append([tuple(p0), tuple(p1)])
+    rows = np.array([[0, 1, 2, 5, 9, 11]], np.int32)
+    layers = _closed_form_layers(3, H, Hq, Hkv, D, m, seed=17)
+    x = rng.standard_normal((1, N, H)).astype(np.float32)
+    cos, sin = O.rope_table(N, D, 500000.0)
+    got, _ = O.decoder_stack_selective(x, layers, pools_by_layer, segs, rows, cos, sin, Hq,
+                                       500000.0, EPS, dt=0)
+    r = rows[0]
+    X = x[0].astype(np.float64)
+    # layer 1: every row projected, the listed rows attend over the fresh values
+    L = layers[0]
+    Wv = L["w_qkv"][(Hq + Hkv) * D:].astype(np.float64)
+    v = (_cf_norm(X, L["g_attn"].astype(np.float64)) @ Wv.T).reshape(N, Hkv, D)
+    h = X[r] + _cf_attend_rows(v, r, Hq, Hkv, L["w_o"].astype(np.float64))
+    xs = _cf_mlp(h, L, m)
+    for L, pools in zip(layers[1:], pools_by_layer[1:]):
+        Wv = L["w_qkv"][(Hq + Hkv) * D:].astype(np.float64)
+        cache = np.zeros((N, Hkv, D))
+        cache[3:8] = pools[0][1][1, :5]          # pool 0 block 1, offsets 0..4
+        cache[8:12] = pools[1][1][0, :4]         # pool 1 block 0
+        cache[r] = (_cf_norm(xs, L["g_attn"].astype(np.float64)) @ Wv.T).reshape(len(r), Hkv, D)
+        h = xs + _cf_attend_rows(cache, r, Hq, Hkv, L["w_o"].astype(np.float64))
+        xs = _cf_mlp(h, L, m)
+    np.testing.assert_allclose(got[0], xs, rtol=2e-6, atol=2e-6)

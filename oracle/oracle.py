@@ -29,7 +29,9 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 SRC_PATH = os.path.join(_HERE, "rcref.c")
-LIB_PATH = os.path.join(_HERE, "librcref.so")
+# RCREF_LIB names another build of rcref.c (the sanitizer test loads an
+# ASan/UBSan build this way)
+LIB_PATH = os.environ.get("RCREF_LIB") or os.path.join(_HERE, "librcref.so")
 
 _lib = None
 

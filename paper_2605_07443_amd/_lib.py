@@ -13,7 +13,9 @@ import os
 import torch  # noqa: F401  (loads the HIP runtime the library must share)
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(PKG, "librcllm.so")
+# RCLLM_LIB names another build of the library (e.g. one whose host code is
+# built with AddressSanitizer); default: the in-tree build
+LIB_PATH = os.environ.get("RCLLM_LIB") or os.path.join(PKG, "librcllm.so")
 
 RC_OK, RC_ERR_INVALID_ARG, RC_ERR_UNSUPPORTED, RC_ERR_HIP = 0, -1, -2, -3
 RC_F32, RC_BF16 = 0, 1

@@ -20,7 +20,8 @@ namespace {
 using u32x4 = u32x4_t;
 
 constexpr int kThreads = 256;
-constexpr int kMaxTok = 256;      // positions per workgroup (small rows)
+constexpr int kMaxTok = 64;       // positions per workgroup (8 KiB of the smallest key row, 128 B)
+constexpr int kFewSegments = 64;  // segment capacity in LDS of the common instance
 constexpr int kKPer = 1;                 // key pairs per thread per pass
 constexpr int kVPer = 2;                 // value units per thread per pass
 constexpr int kKItems = kKPer * kThreads;   // key pairs per pass
@@ -38,7 +39,10 @@ constexpr int kRowBytesPerWg = kKItems * 32;  // key-row bytes of a workgroup (8
 // MAP (with ASSEMBLE): sources come from a per-position map {pool, row,
 // delta, -} instead of the segment table (single-token prototypes).
 // Every load of a workgroup's 16-byte units is issued before the first use.
-template <int ES, bool ASSEMBLE, bool SCORE, bool WRITE = true, bool MAP = false>
+// MAXS: segments the LDS table holds (S <= MAXS); a small table keeps the
+// workgroup's LDS small, so that more workgroups fit a compute unit.
+template <int ES, bool ASSEMBLE, bool SCORE, bool WRITE = true, bool MAP = false,
+          int MAXS = kMaxSegments>
 __global__ __launch_bounds__(kThreads) void kv_rows_kernel(
     PoolArgs pools, const int4* __restrict__ segs, int S, int N, int tok_per_wg, int row_units,
     int head_units, const char* __restrict__ k_fresh, const char* __restrict__ v_fresh,
@@ -47,7 +51,7 @@ __global__ __launch_bounds__(kThreads) void kv_rows_kernel(
     const float* __restrict__ sin_t, int max_pos, int half, char* __restrict__ k_out,
     char* __restrict__ v_out, float* __restrict__ scores) {
   constexpr int E = 16 / ES;  // elements per 16-byte unit
-  __shared__ int4 s_segs[(ASSEMBLE && !MAP) ? kMaxSegments : 1];
+  __shared__ int4 s_segs[(ASSEMBLE && !MAP) ? MAXS : 1];
   __shared__ const char* s_srck[kMaxTok];
   __shared__ const char* s_srcv[kMaxTok];
   __shared__ int s_delta[kMaxTok];
@@ -266,15 +270,22 @@ int launch_rows(const rc_shape* s, const PoolArgs& pools, const int4* segs, int 
       if (s->dtype == RC_BF16) args(kv_rows_kernel<2, true, false, true, true>);
       else args(kv_rows_kernel<4, true, false, true, true>);
     }
-  } else if (scores && !k_out) {
-    if (s->dtype == RC_BF16) args(kv_rows_kernel<2, true, true, false>);
-    else args(kv_rows_kernel<4, true, true, false>);
-  } else if (scores) {
-    if (s->dtype == RC_BF16) args(kv_rows_kernel<2, true, true>);
-    else args(kv_rows_kernel<4, true, true>);
   } else {
-    if (s->dtype == RC_BF16) args(kv_rows_kernel<2, true, false>);
-    else args(kv_rows_kernel<4, true, false>);
+    auto seg_table = [&](auto few) {
+      constexpr int MS = decltype(few)::value ? kFewSegments : kMaxSegments;
+      if (scores && !k_out) {
+        if (s->dtype == RC_BF16) args(kv_rows_kernel<2, true, true, false, false, MS>);
+        else args(kv_rows_kernel<4, true, true, false, false, MS>);
+      } else if (scores) {
+        if (s->dtype == RC_BF16) args(kv_rows_kernel<2, true, true, true, false, MS>);
+        else args(kv_rows_kernel<4, true, true, true, false, MS>);
+      } else {
+        if (s->dtype == RC_BF16) args(kv_rows_kernel<2, true, false, true, false, MS>);
+        else args(kv_rows_kernel<4, true, false, true, false, MS>);
+      }
+    };
+    if (S <= kFewSegments) seg_table(std::true_type{});
+    else seg_table(std::false_type{});
   }
   return check_launch(MAP ? "rc_kv_gather_tokens" : ASSEMBLE ? "rc_kv_assemble" : "rc_rerope");
 }

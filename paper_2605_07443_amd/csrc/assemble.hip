@@ -2,16 +2,21 @@
 // standalone re-alignment pass (RcLLM, arXiv 2605.07443, Sec. III-C.3 steps
 // (i) and (ii); logical-to-physical block mapping of Sec. III-A).
 //
-// Both are HBM-bound copies. A workgroup of 256 threads owns TOK consecutive
-// positions of one request (TOK * key row = 8 KiB): it first
-// resolves each position to its source row (binary search of the request's
-// segment table staged in LDS), then streams 16-byte units. Source rows and
-// the assembled rows go through the caches with ordinary loads and stores
-// (pool rows of popular items recur across requests and batches, and the
-// attention reads the assembled rows next); the fresh key rows read for the
-// score are non-temporal. A key unit pairs
-// element block [j, j+E) of a head with [j+D/2, j+D/2+E) so the rotation of
-// the pairs (j, j+D/2) happens in registers between the load and the store.
+// Both are HBM-bound copies. The common case (a request of at most 64
+// segments, a key row of a power-of-two number of rotation pairs) runs on
+// kv_gather_kernel / rerope_wave_kernel: each wave owns a few positions, finds
+// each position's segment with one ballot over the request's segment table
+// (one entry per lane, no LDS), issues all of its 16-byte loads and stores
+// the rotated rows, without barriers. Other shapes and the token-granular
+// gather run on kv_rows_kernel, where a workgroup of 256 threads owns TOK
+// consecutive positions (TOK * key row = 8 KiB), resolves them through a
+// segment table staged in LDS (or a per-position map) and then streams the
+// rows. Source rows and assembled rows go through the caches with ordinary
+// loads and stores (pool rows of popular items recur across requests and
+// batches, and the attention reads the assembled rows next); the fresh key
+// rows read for the score are non-temporal. A key unit pairs element block
+// [j, j+E) of a head with [j+D/2, j+D/2+E) so the rotation of the pairs
+// (j, j+D/2) happens in registers between the load and the store.
 #include "rc_common.h"
 
 namespace rc {
@@ -230,9 +235,235 @@ __global__ __launch_bounds__(kThreads) void kv_rows_kernel(
   }
 }
 
+// Wave-level gather for requests of at most 64 segments whose key row has a
+// power-of-two number of pairs ppr dividing 64 * KP (every workload shape
+// here): no LDS and no barrier. Wave w of workgroup x owns the T = 64 KP /
+// ppr positions starting at (4 x + w) T of request blockIdx.y. The request's
+// segment table is held one entry per lane; a position's segment is the
+// lane whose range holds it (one ballot). Lane l carries key pairs
+// k * 64 + l (k < KP: position (k * 64 + l) / ppr, pair (k * 64 + l) % ppr)
+// and value units k * 64 + l (k < 2 KP) of those T positions; every load is
+// issued before the first use. The deviation of a position is the sum of its
+// pairs' partials in a fixed order (shuffles within the lanes of one
+// position when ppr < 64, then a wave sum), so the score is deterministic.
+template <int ES, bool SCORE, bool WRITE, int KP>
+__global__ __launch_bounds__(kThreads) void kv_gather_kernel(
+    PoolArgs pools, const int4* __restrict__ segs, int S, int N, int row_units, int head_units,
+    int log2_ppr, const char* __restrict__ k_fresh, const char* __restrict__ v_fresh,
+    const float* __restrict__ cos_t, const float* __restrict__ sin_t, int max_pos, int half,
+    char* __restrict__ k_out, char* __restrict__ v_out, float* __restrict__ scores) {
+  constexpr int E = 16 / ES;     // elements per 16-byte unit
+  constexpr int VP = 2 * KP;     // value units per lane
+  const int b = blockIdx.y;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int ppr = 1 << log2_ppr;
+  const int T = (64 * KP) >> log2_ppr;                   // positions of this wave
+  const int i0 = (blockIdx.x * (kThreads / 64) + wave) * T;
+  if (i0 >= N) return;
+  const size_t row_bytes = static_cast<size_t>(row_units) * 16;
+  const int half_units = head_units / 2;
+
+  const int4 sg = lane < S ? segs[static_cast<size_t>(b) * S + lane] : int4{0x7fffffff, 0, -1, 0};
+
+  // per-lane slots: the position of each key pair and value unit
+  int kt[KP], vt[VP];
+#pragma unroll
+  for (int k = 0; k < KP; ++k) kt[k] = (k * 64 + lane) >> log2_ppr;
+#pragma unroll
+  for (int k = 0; k < VP; ++k) vt[k] = (k * 64 + lane) / row_units;
+  const char* ksrc[KP] = {};
+  const char* vsrc[VP] = {};
+  int kd[KP] = {};
+  bool kc[KP] = {};
+  // resolve the wave's positions one at a time (uniform values)
+  for (int t = 0; t < T; ++t) {
+    const int i = i0 + t;
+    if (i >= N) break;
+    const uint64_t m = __ballot(sg.x <= i && i - sg.x < sg.y);
+    const char* sk = nullptr;
+    const char* sv = nullptr;
+    int d = 0;
+    bool cached = false;
+    if (m != 0) {
+      const int sl = __builtin_ctzll(m);
+      const int gx = __builtin_amdgcn_readlane(sg.x, sl);
+      const int gp = __builtin_amdgcn_readlane(sg.z, sl);
+      const int gb = __builtin_amdgcn_readlane(sg.w, sl);
+      if (gp < 0) {
+        const size_t off = (static_cast<size_t>(b) * N + i) * row_bytes;
+        sk = k_fresh + off;
+        sv = v_fresh + off;
+      } else if (gp < pools.n && gb >= 0 && gb < pools.num_blocks[gp] && gx >= 0 &&
+                 i - gx < pools.block_len[gp]) {
+        const size_t off = (static_cast<size_t>(gb) * pools.block_len[gp] + (i - gx)) * row_bytes;
+        sk = pools.k[gp] + off;
+        sv = pools.v[gp] + off;
+        cached = true;
+        if (cos_t != nullptr && gx < max_pos) d = gx;
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < KP; ++k)
+      if (kt[k] == t) {
+        ksrc[k] = sk;
+        kd[k] = d;
+        kc[k] = cached;
+      }
+#pragma unroll
+    for (int k = 0; k < VP; ++k)
+      if (vt[k] == t) vsrc[k] = sv;
+  }
+
+  // ---- issue every load
+  u32x4 ua[KP], ub[KP], fa[KP], fb[KP], vv[VP];
+  int kunit[KP];
+#pragma unroll
+  for (int k = 0; k < KP; ++k) {
+    const int pr = (k * 64 + lane) & (ppr - 1);
+    const int head = pr / half_units;
+    kunit[k] = head * head_units + (pr - head * half_units);
+    if (ksrc[k] != nullptr) {
+      const u32x4* src = reinterpret_cast<const u32x4*>(ksrc[k]);
+      ua[k] = src[kunit[k]];
+      ub[k] = src[kunit[k] + half_units];
+      if (SCORE && kc[k]) {
+        const u32x4* fr = reinterpret_cast<const u32x4*>(
+            k_fresh + (static_cast<size_t>(b) * N + i0 + kt[k]) * row_bytes);
+        fa[k] = __builtin_nontemporal_load(fr + kunit[k]);
+        fb[k] = __builtin_nontemporal_load(fr + kunit[k] + half_units);
+      }
+    }
+  }
+  if constexpr (WRITE) {
+#pragma unroll
+    for (int k = 0; k < VP; ++k)
+      if (vsrc[k] != nullptr) vv[k] = reinterpret_cast<const u32x4*>(vsrc[k])[(k * 64 + lane) % row_units];
+  }
+
+  // ---- keys: rotate, store, deviation partials
+  float part[KP];
+#pragma unroll
+  for (int k = 0; k < KP; ++k) {
+    part[k] = 0.f;
+    if (ksrc[k] == nullptr) continue;
+    if (kd[k] != 0) {
+      const int j0 = (kunit[k] % head_units) * E;   // element offset in the half
+      float c[E], sn[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        c[e] = cos_t[static_cast<size_t>(kd[k]) * half + j0 + e];
+        sn[e] = sin_t[static_cast<size_t>(kd[k]) * half + j0 + e];
+      }
+      rotate_unit<ES>(ua[k], ub[k], c, sn);
+    }
+    if constexpr (WRITE) {
+      u32x4* dst = reinterpret_cast<u32x4*>(k_out + (static_cast<size_t>(b) * N + i0 + kt[k]) * row_bytes);
+      dst[kunit[k]] = ua[k];
+      dst[kunit[k] + half_units] = ub[k];
+    }
+    if (SCORE && kc[k]) part[k] = absdiff_sum<ES>(fa[k], ua[k]) + absdiff_sum<ES>(fb[k], ub[k]);
+  }
+  if constexpr (WRITE) {
+#pragma unroll
+    for (int k = 0; k < VP; ++k) {
+      if (vsrc[k] == nullptr) continue;
+      u32x4* dst = reinterpret_cast<u32x4*>(v_out + (static_cast<size_t>(b) * N + i0 + vt[k]) * row_bytes);
+      dst[(k * 64 + lane) % row_units] = vv[k];
+    }
+  }
+
+  if constexpr (SCORE) {
+    if (ppr >= 64) {
+      // position t holds the slots k with (k * 64) >> log2_ppr == t: ppr / 64 of them
+      const int per = ppr >> 6;
+      for (int t = 0; t < T; ++t) {
+        float x = 0.f;
+#pragma unroll
+        for (int k = 0; k < KP; ++k)
+          if (k / per == t) x += part[k];
+        x = wave_sum(x);
+        if (lane == 0 && i0 + t < N) scores[static_cast<size_t>(b) * N + i0 + t] = x;
+      }
+    } else {
+      // each slot k: positions of ppr consecutive lanes; sum within them
+#pragma unroll
+      for (int k = 0; k < KP; ++k) {
+        float x = part[k];
+        for (int off = ppr >> 1; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
+        if ((lane & (ppr - 1)) == 0 && i0 + kt[k] < N)
+          scores[static_cast<size_t>(b) * N + i0 + kt[k]] = x;
+      }
+    }
+  }
+}
+
+// Standalone re-alignment with the wave-level layout of kv_gather_kernel: the
+// T positions of wave w of workgroup x are rotated in place, each by its own
+// delta (rows with delta 0 or |delta| >= max_pos are not touched).
+template <int ES, int KP>
+__global__ __launch_bounds__(kThreads) void rerope_wave_kernel(
+    int N, int row_units, int head_units, int log2_ppr, const int32_t* __restrict__ delta,
+    const float* __restrict__ cos_t, const float* __restrict__ sin_t, int max_pos, int half,
+    char* __restrict__ k) {
+  constexpr int E = 16 / ES;
+  const int b = blockIdx.y;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int ppr = 1 << log2_ppr;
+  const int T = (64 * KP) >> log2_ppr;
+  const int i0 = (blockIdx.x * (kThreads / 64) + wave) * T;
+  if (i0 >= N) return;
+  const size_t row_bytes = static_cast<size_t>(row_units) * 16;
+  const int half_units = head_units / 2;
+  u32x4 ua[KP], ub[KP];
+  int kd[KP], kunit[KP], kt[KP];
+#pragma unroll
+  for (int q = 0; q < KP; ++q) {
+    kt[q] = (q * 64 + lane) >> log2_ppr;
+    const int i = i0 + kt[q];
+    const int pr = (q * 64 + lane) & (ppr - 1);
+    const int head = pr / half_units;
+    kunit[q] = head * head_units + (pr - head * half_units);
+    const int d = i < N ? delta[static_cast<size_t>(b) * N + i] : 0;
+    kd[q] = (d != 0 && d < max_pos && -d < max_pos) ? d : 0;
+    if (kd[q] != 0) {
+      const u32x4* src = reinterpret_cast<const u32x4*>(k + (static_cast<size_t>(b) * N + i) * row_bytes);
+      ua[q] = src[kunit[q]];
+      ub[q] = src[kunit[q] + half_units];
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < KP; ++q) {
+    if (kd[q] == 0) continue;
+    const int a = kd[q] < 0 ? -kd[q] : kd[q];
+    const int j0 = (kunit[q] % head_units) * E;
+    float c[E], sn[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      c[e] = cos_t[static_cast<size_t>(a) * half + j0 + e];
+      const float sv = sin_t[static_cast<size_t>(a) * half + j0 + e];
+      sn[e] = kd[q] < 0 ? -sv : sv;
+    }
+    rotate_unit<ES>(ua[q], ub[q], c, sn);
+    u32x4* dst = reinterpret_cast<u32x4*>(k + (static_cast<size_t>(b) * N + i0 + kt[q]) * row_bytes);
+    dst[kunit[q]] = ua[q];
+    dst[kunit[q] + half_units] = ub[q];
+  }
+}
+
 int tokens_per_wg(int row_bytes) {
   int t = kRowBytesPerWg / row_bytes;
   return t < 1 ? 1 : (t > kMaxTok ? kMaxTok : t);
+}
+
+constexpr int kWaveGatherKP = 1;  // key pairs per lane of the wave-level gather
+
+// The wave-level gather serves requests of at most 64 segments whose key row
+// has a power-of-two pair count dividing 64 * KP.
+bool wave_gather_ok(const rc_shape& s, int S, int row_units) {
+  const int ppr = row_units / 2;
+  return S <= 64 && ppr >= 1 && (ppr & (ppr - 1)) == 0 && ppr <= 64 * kWaveGatherKP;
 }
 
 template <bool ASSEMBLE, bool MAP = false>
@@ -259,7 +490,18 @@ int launch_rows(const rc_shape* s, const PoolArgs& pools, const int4* segs, int 
                        static_cast<const char*>(v_fresh), delta, map, cos_t, sin_t, max_pos, s->D / 2,
                        static_cast<char*>(k_out), static_cast<char*>(v_out), scores);
   };
-  if (!ASSEMBLE) {
+  if (!ASSEMBLE && wave_gather_ok(*s, 1, row_units)) {
+    int log2_ppr = 0;
+    while ((1 << log2_ppr) < row_units / 2) ++log2_ppr;
+    const int T = (64 * kWaveGatherKP) >> log2_ppr;
+    dim3 g2((s->N + (kThreads / 64) * T - 1) / ((kThreads / 64) * T), s->B);
+    auto args2 = [&](auto kern) {
+      hipLaunchKernelGGL(kern, g2, dim3(kThreads), 0, stream, s->N, row_units, head_units, log2_ppr,
+                         delta, cos_t, sin_t, max_pos, s->D / 2, static_cast<char*>(k_out));
+    };
+    if (s->dtype == RC_BF16) args2(rerope_wave_kernel<2, kWaveGatherKP>);
+    else args2(rerope_wave_kernel<4, kWaveGatherKP>);
+  } else if (!ASSEMBLE) {
     if (s->dtype == RC_BF16) args(kv_rows_kernel<2, false, false>);
     else args(kv_rows_kernel<4, false, false>);
   } else if (MAP) {
@@ -269,6 +511,28 @@ int launch_rows(const rc_shape* s, const PoolArgs& pools, const int4* segs, int 
     } else {
       if (s->dtype == RC_BF16) args(kv_rows_kernel<2, true, false, true, true>);
       else args(kv_rows_kernel<4, true, false, true, true>);
+    }
+  } else if (wave_gather_ok(*s, S, row_units)) {
+    int log2_ppr = 0;
+    while ((1 << log2_ppr) < row_units / 2) ++log2_ppr;
+    const int T = (64 * kWaveGatherKP) >> log2_ppr;
+    dim3 g2((s->N + (kThreads / 64) * T - 1) / ((kThreads / 64) * T), s->B);
+    auto args2 = [&](auto kern) {
+      hipLaunchKernelGGL(kern, g2, dim3(kThreads), 0, stream, pools, segs, S, s->N, row_units,
+                         head_units, log2_ppr, static_cast<const char*>(k_fresh),
+                         static_cast<const char*>(v_fresh), cos_t, sin_t, max_pos, s->D / 2,
+                         static_cast<char*>(k_out), static_cast<char*>(v_out), scores);
+    };
+    constexpr int KP = kWaveGatherKP;
+    if (scores && !k_out) {
+      if (s->dtype == RC_BF16) args2(kv_gather_kernel<2, true, false, KP>);
+      else args2(kv_gather_kernel<4, true, false, KP>);
+    } else if (scores) {
+      if (s->dtype == RC_BF16) args2(kv_gather_kernel<2, true, true, KP>);
+      else args2(kv_gather_kernel<4, true, true, KP>);
+    } else {
+      if (s->dtype == RC_BF16) args2(kv_gather_kernel<2, false, true, KP>);
+      else args2(kv_gather_kernel<4, false, true, KP>);
     }
   } else {
     auto seg_table = [&](auto few) {

@@ -517,7 +517,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
     // K fragments in the order (dc, kb) within each half of the keys:
     // fragment gi of half h is key block 2h + gi % 2, d chunk gi / 2
     constexpr int KG = DC * 4;
-    constexpr int KAHEAD = 3;
+    constexpr int KAHEAD = 5;
     u32x4 kf[KG];
     auto rdk = [&](auto G) {
       constexpr int gi = decltype(G)::value;
@@ -635,7 +635,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
     // ---- O^T += V^T P^T: keys 0..31 while the vector ALU forms keys 32..63
     __builtin_amdgcn_s_setprio(1);
     constexpr int NG = 2 * DB;
-    constexpr int AHEAD = 3;
+    constexpr int AHEAD = 4;
     u32x2 lo[NG], hi[NG];
     auto rd = [&](auto G) {
       constexpr int gi = decltype(G)::value;

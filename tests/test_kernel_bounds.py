@@ -237,3 +237,58 @@ def test_kv_rows_kernel_bounds(score_only):
             it += 1
         assert k_items <= k_items_cap                        # one scoring pass (s_part size)
     _check("scores", np.array([0]), np.array([B * N]), B * N)
+
+
+WAVE_KP = int(_const("assemble.hip", "kWaveGatherKP"))
+
+
+@pytest.mark.parametrize("score_only", [False, True])
+def test_kv_gather_kernel_bounds(score_only):
+    """kv_gather_kernel (the wave-level assembly used when a request has at
+    most 64 segments and a key row has a power-of-two pair count): wave w of
+    block x owns positions (4x + w) T .. + T; lane l carries key pairs
+    k * 64 + l and value units k * 64 + l of them."""
+    es = 2
+    row_bytes = HKV * D * es
+    row_units = row_bytes // 16
+    head_units = D * es // 16
+    half_units = head_units // 2
+    E = 16 // es
+    half = D // 2
+    ppr = row_units // 2
+    assert ppr & (ppr - 1) == 0 and ppr <= 64 * WAVE_KP
+    log2_ppr = ppr.bit_length() - 1
+    T = (64 * WAVE_KP) >> log2_ppr
+    waves = ASM_THREADS // 64
+    grid_x = (N + waves * T - 1) // (waves * T)
+    segs = _window_segments()
+    assert segs.shape[0] <= 64
+    lane = np.arange(64)
+    for x in (0, grid_x - 1):
+        for w in range(waves):
+            i0 = (x * waves + w) * T
+            if i0 >= N:
+                continue
+            k = np.arange(WAVE_KP)[:, None]
+            q = k * 64 + lane                              # [KP, 64]
+            kt = q >> log2_ppr
+            pr = q & (ppr - 1)
+            head = pr // half_units
+            kunit = head * head_units + (pr - head * half_units)
+            assert (kunit + half_units).max() < row_units
+            live = i0 + kt < N
+            for b in (0, B - 1):
+                rows = (b * N + i0 + kt)[live]
+                ku = kunit[live]
+                _check("fresh / assembled key pairs", rows * row_bytes + ku * 16,
+                       rows * row_bytes + (ku + half_units) * 16 + 16, B * N * row_bytes)
+                _check("scores", b * N + i0 + kt[live], b * N + i0 + kt[live] + 1, B * N)
+            if not score_only:
+                kv = np.arange(2 * WAVE_KP)[:, None] * 64 + lane
+                vt, vu = kv // row_units, kv % row_units
+                vl = i0 + vt < N
+                rows = ((B - 1) * N + i0 + vt)[vl]
+                _check("value units", rows * row_bytes + vu[vl] * 16, rows * row_bytes + vu[vl] * 16 + 16,
+                       B * N * row_bytes)
+            j0 = (kunit % head_units) * E
+            assert (j0 + E).max() <= half

@@ -803,7 +803,6 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(const float* __restrict__
 #pragma unroll
     for (int e = 0; e < PER; ++e) acc[e] *= alpha;
     const int cnt = min(64, p - c + 1);
-#pragma unroll 8
     for (int jj = 0; jj < cnt; ++jj) {
       const float pw = __shfl(pj, jj, 64);
       const float* vr = vb + (c + jj) * kv_stride;

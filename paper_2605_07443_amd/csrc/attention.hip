@@ -25,9 +25,9 @@
 //     global loads in flight during compute. For D = 128 (not paged) the
 //     tiles go from HBM straight into LDS and every K/V read of the tile loop
 //     is issued as assembly (layouts and ordering at AttnBufDirect).
-//   * A tile is computed in halves of 32 keys, so that the softmax of one
-//     half runs on the vector ALU beside the matrix products of the other
-//     (compute_tile).
+//   * A tile is computed in halves of 32 keys, so that the probabilities of
+//     the second half are formed on the vector ALU beside the matrix
+//     products of the first (compute_tile).
 //   * Workgroup ids are remapped so that all row tiles of one (request, KV
 //     head) run on the same XCD (ids are dealt round-robin over the 8 XCDs),
 //     sharing its L2 for the K/V stream. Each XCD starts its longest (latest)
@@ -501,10 +501,12 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
 
   // One KV tile (either staging) in an order that lets the vector ALU work
   // beside the matrix cores. Scores of keys 0..31 first; then the scores of keys 32..63
-  // are issued while the probabilities of keys 0..31 are formed against the
-  // current reference max; after the rescale decision (taken on the whole
-  // tile), V^T P^T of keys 0..31 runs while the probabilities of keys 32..63
-  // are formed. Without a rescale the reference max is unchanged, so every
+  // are issued, with the probabilities of keys 0..31 against the current
+  // reference max placed between them (the compiler moves those below the
+  // rescale decision, whose path recomputes them; forcing them above it
+  // needs more than the 256 registers of two waves per SIMD and spills);
+  // after the rescale decision (taken on the whole tile), V^T P^T of keys
+  // 0..31 runs while the probabilities of keys 32..63 are formed. Without a rescale the reference max is unchanged, so every
   // value equals that of the plain order (all scores, then all
   // probabilities); with one, the probabilities of keys 0..31 are recomputed
   // from the scores, which are kept until the decision.

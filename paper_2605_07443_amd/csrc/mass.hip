@@ -35,9 +35,12 @@ constexpr int kMassXcds = 8;
 using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
 
 // Q tile rows padded to 16 mod 256 bytes: the B-operand reads (16 bytes from
-// 16 consecutive rows per quarter-wave) are then conflict-free.
+// 16 consecutive rows per quarter-wave) are then conflict-free. Declared
+// 16-byte aligned so that those reads and the staging stores are single
+// 16-byte LDS instructions (with the 4-byte alignment of the members alone
+// each is split into two 8-byte halves).
 template <int D>
-struct MassSmem {
+struct alignas(16) MassSmem {
   uint16_t q[2][kQV][D + 8];
   float lse2[2][kQV];  // lse * log2(e); +inf for padding vectors (weight 0)
 };

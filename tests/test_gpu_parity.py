@@ -349,6 +349,74 @@ def test_patch_with_more_than_64_segments():
     np.testing.assert_array_equal(H(va), vp)
 
 
+# ------------------------------------------------------- the most pools a call takes
+
+@pytest.mark.parametrize("dtype,D", [("bf16", 128), ("f32", 64)])
+def test_eight_pools_in_one_request(dtype, D):
+    """Eight pools (the most a call takes), each with its own block length and
+    block count, all referenced by every request, with a fresh segment between
+    them and blocks used whole and in part: fused gather + rotation bit-exact
+    with the oracle, scores within 1e-5, rows and patched K/V bit-exact,
+    attention within tolerance of the oracle; for bf16 the paged path equals
+    the assembled one bit for bit."""
+    B, Hq, Hkv, F = 2, 8, 2, 8
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    rng = np.random.default_rng(800 + D)
+    bls = [8, 12, 16, 20, 24, 32, 40, 48]
+    nbs = [5, 6, 7, 8, 9, 10, 11, 12]
+    order = list(range(8)) + list(range(7, -1, -1))
+    lens = [bls[p] if j < 8 else int(rng.integers(1, bls[p] + 1)) for j, p in enumerate(order)]
+    segs_h = []
+    for b in range(B):
+        seg, pos = [(0, F, -1, 0)], F
+        for j, p in enumerate(order):
+            seg.append((pos, lens[j], p, int(rng.integers(0, nbs[p]))))
+            pos += lens[j]
+            if j == 3:
+                seg.append((pos, 5, -1, 0))
+                pos += 5
+        segs_h.append(seg)
+    segs_h = np.ascontiguousarray(np.array(segs_h, np.int32))
+    N = int(segs_h[0, -1, 0] + segs_h[0, -1, 1])
+    g = torch.Generator().manual_seed(80 + D)
+    pools = [(torch.randn((nb, bl, Hkv, D), generator=g).to(tdt).to(DEV),
+              torch.randn((nb, bl, Hkv, D), generator=g).to(tdt).to(DEV)) for nb, bl in zip(nbs, bls)]
+    kf = torch.randn((B, N, Hkv, D), generator=g).to(tdt).to(DEV)
+    vf = torch.randn((B, N, Hkv, D), generator=g).to(tdt).to(DEV)
+    q = torch.randn((B, N, Hq, D), generator=g).to(tdt).to(DEV)
+    segs = ops.prepare_segments(segs_h, N, pools, DEV)
+    assert segs.n_fresh == F + 5
+    k = (segs.n_reused * 30 + 99) // 100
+    cos, sin = ops.rope_table(N, D, 10000.0, DEV)
+    say(f"[8 pools] {dtype} D={D} N={N} S={segs.S} k={k}")
+    scores = torch.empty((B, N), dtype=torch.float32, device=DEV)
+    ka, va = ops.kv_assemble(pools, segs, kf, vf, cos, sin, scores_out=scores)
+    a = ops.selective_prefill(q, kf, vf, pools, segs, k, cos, sin)
+    torch.cuda.synchronize()
+    hp = [(H(pk), H(pv)) for pk, pv in pools]
+    ocos, osin = O.rope_table(N, D, 10000.0)
+    ka0, va0 = O.assemble(H(kf), H(vf), hp, segs_h, ocos, osin)
+    np.testing.assert_array_equal(H(ka), ka0)
+    np.testing.assert_array_equal(H(va), va0)
+    np.testing.assert_allclose(scores.cpu().numpy(), O.deviation(H(kf), ka0), rtol=1e-5, atol=1e-5)
+    sc = a.scores.cpu().numpy()
+    rows = a.rows.cpu().numpy()
+    np.testing.assert_array_equal(rows, O.topk(segs_h, N, k, sc))
+    kp, vp = O.patch(segs_h, rows, H(kf), H(vf), ka0, va0)
+    np.testing.assert_array_equal(H(a.k_asm), kp)
+    np.testing.assert_array_equal(H(a.v_asm), vp)
+    sel = sample_rows(B, rows.shape[1], 1)
+    ref = np.concatenate(oracle_attention_rows(H(q), kp, vp, rows, sel))
+    got = np.concatenate([H(a.out)[b, idx] for b, idx in enumerate(sel)])
+    assert_attn_close(got, ref, dtype, "attention over eight pools")
+    if dtype == "bf16":
+        p = ops.paged_prefill(q, kf, vf, pools, segs, k, cos, sin)
+        torch.cuda.synchronize()
+        assert torch.equal(a.scores, p.scores)
+        assert torch.equal(a.rows, p.rows)
+        assert torch.equal(a.out, p.out), "paged attention differs from the assembled path"
+
+
 # ------------------------------------------------- cache misses, bad row lists
 
 def test_all_fresh_prompt_equals_full_prefill():

@@ -105,6 +105,27 @@ def test_attention_unsorted_rows_and_groups(Hq, Hkv, D):
     assert_attn_close(H(full), reff, "bf16", "full prefill")
 
 
+@pytest.mark.parametrize("Hq,Hkv", [(32, 1), (64, 1), (128, 1), (128, 2)])
+def test_attention_large_groups(Hq, Hkv):
+    """Group sizes 32, 64 and 128 (the largest that divides a workgroup's 128
+    query vectors): a workgroup then holds 4, 2 or 1 rows of all G heads;
+    selective rows (unsorted, duplicated) and full prefill against the
+    oracle, bf16 and D = 64."""
+    B, N, R, D = 2, 200, 37, 64
+    g = torch.Generator(device="cpu").manual_seed(Hq * 10 + Hkv)
+    q = torch.randn((B, N, Hq, D), generator=g).to(torch.bfloat16)
+    k = torch.randn((B, N, Hkv, D), generator=g).to(torch.bfloat16)
+    v = torch.randn((B, N, Hkv, D), generator=g).to(torch.bfloat16)
+    rows = torch.randint(0, N, (B, R), generator=g, dtype=torch.int32)
+    rows[1, :2] = torch.tensor([N - 1, N - 1], dtype=torch.int32)
+    say(f"[attention groups] Hq={Hq} Hkv={Hkv}")
+    out = ops.selective_attention(q.to(DEV), k.to(DEV), v.to(DEV), rows.to(DEV))
+    full = ops.full_prefill(q.to(DEV), k.to(DEV), v.to(DEV))
+    torch.cuda.synchronize()
+    assert_attn_close(H(out), O.attention(H(q), H(k), H(v), rows=rows.numpy()), "bf16", "selective")
+    assert_attn_close(H(full), O.attention(H(q), H(k), H(v)), "bf16", "full prefill")
+
+
 @pytest.mark.parametrize("N", [1, 17, 63, 64, 65, 127, 128, 129])
 @pytest.mark.parametrize("D", [64, 128])
 def test_attention_tile_boundary_lengths(N, D):

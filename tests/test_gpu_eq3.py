@@ -55,7 +55,8 @@ def test_eq3_config1_tiny_fp32():
 
 @pytest.mark.parametrize("dtype,Hq,Hkv,D,N", [("bf16", 32, 8, 128, 700), ("bf16", 8, 1, 128, 257),
                                               ("bf16", 16, 16, 64, 300), ("bf16", 4, 2, 64, 1),
-                                              ("f32", 8, 2, 64, 130)])
+                                              ("f32", 8, 2, 64, 130), ("bf16", 64, 1, 64, 150),
+                                              ("bf16", 128, 2, 64, 100)])
 def test_lse_and_mass_shapes(dtype, Hq, Hkv, D, N):
     """Full first layer with lse, then mass, on shapes that exercise the group
     sizes, a single-token prompt and ragged key blocks; the attention output

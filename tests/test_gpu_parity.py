@@ -372,17 +372,17 @@ def test_patch_with_more_than_64_segments():
 
 # ------------------------------------------------------- the most pools a call takes
 
-@pytest.mark.parametrize("dtype,D", [("bf16", 128), ("f32", 64)])
-def test_eight_pools_in_one_request(dtype, D):
+@pytest.mark.parametrize("dtype,D,Hq", [("bf16", 128, 8), ("f32", 64, 8), ("bf16", 64, 64)])
+def test_eight_pools_in_one_request(dtype, D, Hq):
     """Eight pools (the most a call takes), each with its own block length and
     block count, all referenced by every request, with a fresh segment between
     them and blocks used whole and in part: fused gather + rotation bit-exact
     with the oracle, scores within 1e-5, rows and patched K/V bit-exact,
     attention within tolerance of the oracle; for bf16 the paged path equals
-    the assembled one bit for bit."""
-    B, Hq, Hkv, F = 2, 8, 2, 8
+    the assembled one bit for bit (also with 32 query heads per KV head)."""
+    B, Hkv, F = 2, 2, 8
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
-    rng = np.random.default_rng(800 + D)
+    rng = np.random.default_rng(800 + D + Hq)
     bls = [8, 12, 16, 20, 24, 32, 40, 48]
     nbs = [5, 6, 7, 8, 9, 10, 11, 12]
     order = list(range(8)) + list(range(7, -1, -1))
@@ -399,7 +399,7 @@ def test_eight_pools_in_one_request(dtype, D):
         segs_h.append(seg)
     segs_h = np.ascontiguousarray(np.array(segs_h, np.int32))
     N = int(segs_h[0, -1, 0] + segs_h[0, -1, 1])
-    g = torch.Generator().manual_seed(80 + D)
+    g = torch.Generator().manual_seed(80 + D + Hq)
     pools = [(torch.randn((nb, bl, Hkv, D), generator=g).to(tdt).to(DEV),
               torch.randn((nb, bl, Hkv, D), generator=g).to(tdt).to(DEV)) for nb, bl in zip(nbs, bls)]
     kf = torch.randn((B, N, Hkv, D), generator=g).to(tdt).to(DEV)
@@ -409,7 +409,7 @@ def test_eight_pools_in_one_request(dtype, D):
     assert segs.n_fresh == F + 5
     k = (segs.n_reused * 30 + 99) // 100
     cos, sin = ops.rope_table(N, D, 10000.0, DEV)
-    say(f"[8 pools] {dtype} D={D} N={N} S={segs.S} k={k}")
+    say(f"[8 pools] {dtype} D={D} Hq={Hq} N={N} S={segs.S} k={k}")
     scores = torch.empty((B, N), dtype=torch.float32, device=DEV)
     ka, va = ops.kv_assemble(pools, segs, kf, vf, cos, sin, scores_out=scores)
     a = ops.selective_prefill(q, kf, vf, pools, segs, k, cos, sin)

@@ -133,3 +133,49 @@ def test_overlapped_eq3_selection_equals_sequential(cid):
     np.testing.assert_array_equal(
         b.rows.cpu().numpy(),
         O.topk_split(tw.status_segs.numpy(), cfg.N, mask, kh, ki, b.scores.cpu().numpy()))
+
+
+@pytest.mark.parametrize("dtype,D", [("bf16", 128), ("f32", 64)])
+def test_token_gather_eight_pools_signed_deltas(dtype, D):
+    """The per-position map over eight pools of different shapes (the most a
+    call takes), fresh positions in between, rows anywhere in a pool and
+    deltas of both signs (negative: rotation by cos(|d|), -sin(|d|)) and 0:
+    K/V bit-exact with the oracle and scores within 1e-5, one workgroup per
+    position block and a bounded grid alike, and with the pools in pinned
+    host memory."""
+    B, N, Hkv = 2, 300, 2
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    shapes = [(5, 8), (3, 16), (7, 4), (2, 32), (9, 8), (4, 12), (6, 10), (8, 6)]  # blocks, block length
+    g = torch.Generator().manual_seed(700 + D)
+    pools = [(torch.randn((nb, bl, Hkv, D), generator=g).to(tdt).to(DEV),
+              torch.randn((nb, bl, Hkv, D), generator=g).to(tdt).to(DEV)) for nb, bl in shapes]
+    kf = torch.randn((B, N, Hkv, D), generator=g).to(tdt).to(DEV)
+    vf = torch.randn((B, N, Hkv, D), generator=g).to(tdt).to(DEV)
+    rng = np.random.default_rng(700 + D)
+    tm = np.zeros((B, N, 4), np.int32)
+    tm[..., 0] = rng.integers(-1, 8, (B, N))
+    for b in range(B):
+        for i in range(N):
+            p = tm[b, i, 0]
+            if p >= 0:
+                tm[b, i, 1] = rng.integers(0, shapes[p][0] * shapes[p][1])
+                tm[b, i, 2] = 0 if rng.random() < 0.1 else rng.integers(-(N - 1), N)
+    tmap = torch.from_numpy(tm).to(DEV)
+    cos, sin = ops.rope_table(N, D, 10000.0, DEV)
+    say(f"[tokens, 8 pools] {dtype} D={D}")
+    s1 = torch.empty((B, N), dtype=torch.float32, device=DEV)
+    s2 = torch.empty_like(s1)
+    s3 = torch.empty_like(s1)
+    ka, va = ops.kv_gather_tokens(pools, tmap, kf, vf, cos, sin, scores_out=s1)
+    kb, vb = ops.kv_gather_tokens(pools, tmap, kf, vf, cos, sin, scores_out=s2, max_workgroups=3)
+    host = [ops.pin_pool(p) for p in pools]
+    kc, vc = ops.kv_gather_tokens(host, tmap, kf, vf, cos, sin, scores_out=s3)
+    torch.cuda.synchronize()
+    ocos, osin = O.rope_table(N, D, 10000.0)
+    ko, vo = O.gather_tokens(H(kf), H(vf), [(H(a), H(b)) for a, b in pools], tm, ocos, osin)
+    for kk, vv, ss, what in ((ka, va, s1, "device pools"), (kb, vb, s2, "bounded grid"),
+                             (kc, vc, s3, "host pools")):
+        np.testing.assert_array_equal(H(kk), ko, err_msg=f"K, {what}")
+        np.testing.assert_array_equal(H(vv), vo, err_msg=f"V, {what}")
+        np.testing.assert_allclose(ss.cpu().numpy(), O.deviation(H(kf), ko), rtol=1e-5, atol=1e-5,
+                                   err_msg=f"scores, {what}")

@@ -336,9 +336,10 @@ def test_attention_max_jumps_inside_tiles(D):
 
 
 def test_patch_with_more_than_64_segments():
-    """Requests of 150 segments (the patch kernel tests a position against 64
-    segments at a time): assembly, selection and patched K/V bit-exact with
-    the oracle."""
+    """Requests of 150 segments, more than the 64 that the wave-level gather
+    keeps in lane registers (the workgroup gather runs instead) and a long
+    class search in the selection: assembly, selection and patched K/V
+    bit-exact with the oracle."""
     B, Hkv, D, BL = 2, 2, 64, 16
     rng = np.random.default_rng(11)
     lens = rng.integers(1, BL + 1, 150)

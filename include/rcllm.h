@@ -379,9 +379,12 @@ int rc_segments_with_window(const rc_segment* segs_in, int32_t B, int32_t S, int
  *   y[m, j] = sum_i x[m, i] w[j, i] (+ residual[m, j]),  m < M, j < n, i < k
  * x: [M, k], w: [n, k], residual (optional) and y: [M, n]; all bf16 row-major
  * device tensors; fp32 accumulation, one rounding to bf16 (after adding the
- * residual in fp32). Deterministic.
+ * residual in fp32). Deterministic. y must not overlap x, w or residual: a
+ * short row tail (fewer than 256 rows after whole 256-row tiles) may be
+ * computed by split-K with its fp32 partial sums kept in the first rows of y
+ * until those rows are written, so the call allocates nothing.
  * Errors: INVALID_ARG for NULL pointers, M < 0, n < 1, k not a positive
- * multiple of 8, residual == y. */
+ * multiple of 8, y overlapping x, w or residual. */
 int rc_gemm_bf16(int64_t M, int32_t n, int32_t k, const void* x, const void* w,
                  const void* residual, void* y, hipStream_t stream);
 

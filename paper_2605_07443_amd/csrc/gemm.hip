@@ -288,6 +288,132 @@ void gemm_bf16_big_kernel(const uint16_t* __restrict__ x, const uint16_t* __rest
   store_wave_tile(acc, res, y, M, n, m0 + wm, n0 + wn, c16, q4, vec != 0);
 }
 
+// Row tail of fewer than 256 rows left by the 256 x 256 kernel, for shapes
+// where that tail would otherwise run as a few half-empty 128 x 128
+// workgroups through the whole k loop (a second round as long as the first):
+// split-K. Workgroup (column tile, row tile, split s) computes a 64 x 64 tile
+// over the k tiles [s * KT / S, (s + 1) * KT / S) and writes its fp32 partial
+// sums to part[s]; gemm_tail_reduce_kernel then adds the S partials in order
+// of s and the residual, and rounds once. The partials live in the first rows
+// of y, which the 256 x 256 kernel overwrites afterwards on the same stream,
+// so the call allocates nothing. Four waves, each 16 columns (W rows, read
+// straight from global memory one k tile ahead) x the 64 rows (X tile staged
+// in LDS); operand roles and fragment layout as in the kernels above.
+constexpr int kSThreads = 256;
+constexpr int kSM = 64, kSN = 64;
+constexpr int kSPer = kSM * kGUnits / kSThreads;   // X units per thread per k tile (2)
+
+struct GemmSplitSmem {
+  uint16_t x[2][kSM][kGK + kGPad];
+};
+
+__global__ __launch_bounds__(kSThreads)
+void gemm_bf16_splitk_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ w,
+                             float* __restrict__ part, int64_t M, int n, int k, int splits) {
+  __shared__ GemmSplitSmem sm;
+  const int n0 = blockIdx.x * kSN;
+  const int64_t m0 = static_cast<int64_t>(blockIdx.y) * kSM;
+  const int s = blockIdx.z;
+  const int KT = k / kGK;
+  const int kt0 = static_cast<int>(static_cast<int64_t>(s) * KT / splits);
+  const int kt1 = static_cast<int>(static_cast<int64_t>(s + 1) * KT / splits);
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int c16 = lane & 15;
+  const int q4 = lane >> 4;
+  const int wn = wave * 16;
+
+  u32x4 rx[kSPer];
+  auto load_x = [&](int kt) {
+#pragma unroll
+    for (int i = 0; i < kSPer; ++i) {
+      const int u = tid + i * kSThreads;
+      const int64_t gr = m0 + u / kGUnits;
+      const int kk = kt * kGK + (u % kGUnits) * 8;
+      rx[i] = gr < M ? *reinterpret_cast<const u32x4*>(x + gr * k + kk) : u32x4{0, 0, 0, 0};
+    }
+  };
+  auto store_x = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < kSPer; ++i) {
+      const int u = tid + i * kSThreads;
+      *reinterpret_cast<u32x4*>(&sm.x[buf][u / kGUnits][(u % kGUnits) * 8]) = rx[i];
+    }
+  };
+  // rows past n read row n - 1 (finite values whose sums are never stored).
+  // The W fragments of the current and of the next k tile are separate named
+  // registers (a runtime-indexed pair would become selects that wait for the
+  // load just issued).
+  const uint16_t* wrow = w + static_cast<int64_t>(min(n0 + wn + c16, n - 1)) * k + q4 * 8;
+  auto load_w = [&](int kt, bf16x8 (&f)[2]) {
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+      f[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(wrow + kt * kGK + ks * 32));
+  };
+  bf16x8 wcur[2], wnext[2];
+
+  f32x4 acc[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  if (kt0 < kt1) {
+    load_x(kt0);
+    load_w(kt0, wcur);
+    store_x(0);
+  }
+  __syncthreads();
+  if (kt0 + 1 < kt1) {
+    load_x(kt0 + 1);
+    load_w(kt0 + 1, wnext);
+  }
+  for (int kt = kt0; kt < kt1; ++kt) {
+    const int cur = (kt - kt0) & 1;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const bf16x8 fx = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u32x4*>(&sm.x[cur][i * 16 + c16][ks * 32 + q4 * 8]));
+        acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wcur[ks], fx, acc[i], 0, 0, 0);
+      }
+    }
+    if (kt + 1 < kt1) {
+      store_x(cur ^ 1);
+      wcur[0] = wnext[0];
+      wcur[1] = wnext[1];
+      if (kt + 2 < kt1) {
+        load_x(kt + 2);
+        load_w(kt + 2, wnext);
+      }
+    }
+    __syncthreads();
+  }
+  // lane holds rows i*16 + c16, columns q4*4 .. q4*4+3 of its wave's 16
+  float* ps = part + static_cast<int64_t>(s) * M * n;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int64_t gr = m0 + i * 16 + c16;
+    if (gr >= M) continue;
+    const int gc = n0 + wn + q4 * 4;
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (gc + r < n) ps[gr * n + gc + r] = acc[i][r];
+  }
+}
+
+// y[m, c] = bf16(sum over s of part[s][m, c] (+ residual[m, c])), s in order
+__global__ __launch_bounds__(256)
+void gemm_tail_reduce_kernel(const float* __restrict__ part, const uint16_t* __restrict__ res,
+                             uint16_t* __restrict__ y, int64_t count, int splits) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (e >= count) return;
+  float v = part[e];
+  for (int s = 1; s < splits; ++s) v += part[static_cast<int64_t>(s) * count + e];
+  if (res) v += bf16_to_f32(res[e]);
+  y[e] = f32_to_bf16(v);
+}
+
 }  // namespace
 }  // namespace rc
 
@@ -299,8 +425,15 @@ extern "C" int rc_gemm_bf16(int64_t M, int32_t n, int32_t k, const void* x, cons
   if (M < 0 || n < 1 || k < 8 || k % 8)
     return fail(RC_ERR_INVALID_ARG, "M=%lld n=%d k=%d (k a positive multiple of 8)",
                 static_cast<long long>(M), n, k);
-  if (residual == y) return fail(RC_ERR_INVALID_ARG, "residual must not alias y");
   if (M == 0) return RC_OK;
+  auto overlaps = [](const void* a, int64_t a_bytes, const void* b, int64_t b_bytes) {
+    const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
+    return a0 < b0 + static_cast<uintptr_t>(b_bytes) && b0 < a0 + static_cast<uintptr_t>(a_bytes);
+  };
+  const int64_t y_bytes = M * n * 2;
+  if (overlaps(y, y_bytes, x, M * k * 2) || overlaps(y, y_bytes, w, static_cast<int64_t>(n) * k * 2) ||
+      (residual && overlaps(y, y_bytes, residual, y_bytes)))
+    return fail(RC_ERR_INVALID_ARG, "y must not alias or overlap x, w or residual");
   const uint16_t* xs = static_cast<const uint16_t*>(x);
   const uint16_t* rs = static_cast<const uint16_t*>(residual);
   uint16_t* ys = static_cast<uint16_t*>(y);
@@ -308,12 +441,41 @@ extern "C" int rc_gemm_bf16(int64_t M, int32_t n, int32_t k, const void* x, cons
                   reinterpret_cast<uintptr_t>(residual) % 8 == 0;
   if (k % kGK == 0 && M >= kBM && n >= kBN) {
     // whole 256-row tiles on the big kernel; a tail of fewer than 256 rows
-    // goes to the 128 x 128 kernel below (a partial big tile would cost as
-    // much as a full one and, with few tiles per CU, a whole extra round)
+    // goes to split-K (below) when the 128 x 128 kernel would run it on few
+    // workgroups, else to that kernel (a partial big tile would cost as much
+    // as a full one and, with few tiles per CU, a whole extra round)
     const int64_t M_main = (M / kBM) * kBM;
     const int64_t tm = M_main / kBM;
     const int tn = (n + kBN - 1) / kBN;
     if (tm * tn > 0x7fffffff) return fail(RC_ERR_UNSUPPORTED, "grid too large");
+    const int64_t M_tail = M - M_main;
+    const int KT = k / kGK;
+    const int64_t small_tiles = ((M_tail + kGM - 1) / kGM) * ((n + kGN - 1) / kGN);
+    const int64_t split_tiles = ((M_tail + kSM - 1) / kSM) * ((n + kSN - 1) / kSN);
+    // splits: about 512 workgroups, at least 2 k tiles each, and the partials
+    // (splits x M_tail x n fp32) inside the first M_main rows of y (bf16)
+    int64_t splits64 = 512 / (split_tiles > 0 ? split_tiles : 1);
+    if (splits64 > KT / 2) splits64 = KT / 2;
+    if (M_tail > 0 && splits64 > M_main / (2 * M_tail)) splits64 = M_main / (2 * M_tail);
+    const int splits = static_cast<int>(splits64);
+    if (M_tail > 0 && small_tiles < 128 && splits >= 2 && reinterpret_cast<uintptr_t>(y) % 16 == 0) {
+      float* part = reinterpret_cast<float*>(ys);
+      hipLaunchKernelGGL(gemm_bf16_splitk_kernel,
+                         dim3(static_cast<unsigned>((n + kSN - 1) / kSN), static_cast<unsigned>((M_tail + kSM - 1) / kSM),
+                              static_cast<unsigned>(splits)),
+                         dim3(kSThreads), 0, stream, xs + M_main * k, static_cast<const uint16_t*>(w), part,
+                         M_tail, n, k, splits);
+      if (int st = check_launch("rc_gemm_bf16")) return st;
+      const int64_t count = M_tail * n;
+      hipLaunchKernelGGL(gemm_tail_reduce_kernel, dim3(static_cast<unsigned>((count + 255) / 256)), dim3(256), 0,
+                         stream, part, rs ? rs + M_main * n : nullptr, ys + M_main * n, count, splits);
+      if (int st = check_launch("rc_gemm_bf16")) return st;
+      // the body last: it overwrites the partials
+      hipLaunchKernelGGL(gemm_bf16_big_kernel, dim3(static_cast<unsigned>(tm * tn)), dim3(kBThreads), 0,
+                         stream, xs, static_cast<const uint16_t*>(w), rs, ys, M_main, n, k,
+                         static_cast<int>(tm), tn, vec);
+      return check_launch("rc_gemm_bf16");
+    }
     hipLaunchKernelGGL(gemm_bf16_big_kernel, dim3(static_cast<unsigned>(tm * tn)), dim3(kBThreads), 0,
                        stream, xs, static_cast<const uint16_t*>(w), rs, ys, M_main, n, k,
                        static_cast<int>(tm), tn, vec);

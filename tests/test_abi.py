@@ -258,6 +258,13 @@ def test_layer_calls_validation(lib):
         assert st == -1 and "k" in msg
     st, msg = _err(gemm(res=FAKE + 16), lib)          # residual aliases the output
     assert st == -1 and "alias" in msg
+    far = 1 << 30                                     # x, w and y apart; each overlap alone
+    st, msg = _err(gemm(x=FAKE, w=FAKE + far, y=FAKE + 300 * 64 * 2 - 2), lib)    # y's first element in x
+    assert st == -1 and "overlap" in msg
+    st, msg = _err(gemm(x=FAKE, w=FAKE + far, y=FAKE + 2 * far, res=FAKE + 2 * far + 2), lib)
+    assert st == -1 and "overlap" in msg
+    st, msg = _err(gemm(x=FAKE, w=FAKE + 2 * far - 2, y=FAKE + 2 * far - 64 * 64 * 2 + 2), lib)
+    assert st == -1 and "overlap" in msg
     assert gemm(M=0) == 0
 
     def norm(M=4, H=64, eps=1e-5, x=FAKE, g=FAKE + 8, y=FAKE + 16):

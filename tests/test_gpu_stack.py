@@ -35,10 +35,15 @@ def _lib_loaded():
 
 @pytest.mark.parametrize("M,n,k,res", [(1, 8, 8, False), (127, 100, 72, True), (129, 129, 200, False),
                                        (300, 640, 256, True), (256, 256, 4096, True),
-                                       (257, 260, 64, True), (513, 777, 192, False), (700, 300, 640, True)])
+                                       (257, 260, 64, True), (513, 777, 192, False), (700, 300, 640, True),
+                                       (300, 650, 512, True), (1279, 512, 1024, True)])
 def test_gemm_small_against_fp64(M, n, k, res):
     """Own MFMA GEMM against an fp64 host product of the same bf16 operands:
-    one bf16 rounding of the fp32 result (2^-8 relative) plus fp32 sums."""
+    one bf16 rounding of the fp32 result (2^-8 relative) plus fp32 sums. The
+    shapes reach every path: 128 x 128 tiles only, 256 x 256 tiles with a
+    128 x 128 row tail, and with a split-K row tail (300 x 640, 300 x 650:
+    partial column tiles, n not a multiple of 4; 1279 rows: a 255-row tail
+    over four row tiles)."""
     g = torch.Generator().manual_seed(M * 7 + n)
     x = torch.randn((M, k), generator=g).to(torch.bfloat16)
     w = (torch.randn((n, k), generator=g) / k ** 0.5).to(torch.bfloat16)

@@ -21,7 +21,7 @@ B, N, HID, INTER, R, HQ, HKV, D = 8, 3008, 4096, 14336, 520, 32, 8, 128
 
 def _const(src, name):
     text = open(os.path.join(CSRC, src)).read()
-    m = re.search(rf"constexpr int {name} = ([^;]+);", text)
+    m = re.search(rf"constexpr int [^;]*\b{name} = ([^,;]+)[,;]", text)
     assert m, f"{name} not found in {src}"
     return m.group(1).strip()
 
@@ -292,3 +292,62 @@ def test_kv_gather_kernel_bounds(score_only):
                        B * N * row_bytes)
             j0 = (kunit % head_units) * E
             assert (j0 + E).max() <= half
+
+
+def _gemm_split_plan(M, n, k):
+    """rc_gemm_bf16's choice for a row tail, restated: (M_main, M_tail, splits)
+    with splits >= 2 when the tail goes to split-K, else splits = 0."""
+    kBM, kGM, kGN, kGK = (int(_const("gemm.hip", c)) for c in ("kBM", "kGM", "kGN", "kGK"))
+    kSM, kSN = int(_const("gemm.hip", "kSM")), int(_const("gemm.hip", "kSN"))
+    M_main = (M // kBM) * kBM
+    M_tail = M - M_main
+    KT = k // kGK
+    small_tiles = -(-M_tail // kGM) * -(-n // kGN)
+    split_tiles = -(-M_tail // kSM) * -(-n // kSN)
+    s = 512 // max(split_tiles, 1)
+    s = min(s, KT // 2)
+    if M_tail > 0:
+        s = min(s, M_main // (2 * M_tail))
+    use = M_tail > 0 and small_tiles < 128 and s >= 2
+    return M_main, M_tail, (s if use else 0)
+
+
+@pytest.mark.parametrize("M,n,k", [(B * R, 3 * HQ * D // 2, HID), (B * R, HID, HID),
+                                   (B * R, 2 * INTER, HID), (B * R, HID, INTER),
+                                   (300, 650, 512), (1279, 512, 1024), (300, 640, 256)])
+def test_gemm_split_tail_bounds(M, n, k):
+    """The split-K row tail of rc_gemm_bf16 (gemm_bf16_splitk_kernel, then
+    gemm_tail_reduce_kernel) at the stack's 4,160-row projection shapes and
+    the GEMM test shapes: every X, W and partial access of every lane is in
+    its buffer, every split covers at least two k tiles, the partials fit
+    in the first M_main rows of y (whose bf16 bytes they borrow) and stay
+    clear of the tail rows the reduction writes."""
+    kSM, kSN, kGK = int(_const("gemm.hip", "kSM")), int(_const("gemm.hip", "kSN")), int(_const("gemm.hip", "kGK"))
+    threads = int(_const("gemm.hip", "kSThreads"))
+    M_main, M_tail, S = _gemm_split_plan(M, n, k)
+    if S == 0:
+        pytest.skip("tail not on split-K for this shape")
+    KT = k // kGK
+    assert S * M_tail * n * 4 <= M_main * n * 2          # partials inside y's body
+    for s in range(S):
+        kt0, kt1 = s * KT // S, (s + 1) * KT // S
+        assert kt1 - kt0 >= 2 and 0 <= kt0 and kt1 <= KT
+    # X staging: unit u = tid + i * threads, row u // 8 (guarded by M_tail),
+    # 16-byte unit at k offset kt * 64 + (u % 8) * 8 of row M_main + row
+    u = np.arange(threads)[:, None] + np.arange(kSM * 8 // threads)[None, :] * threads
+    rows = (np.arange(-(-M_tail // kSM))[:, None, None] * kSM + (u // 8)[None]).ravel()
+    rows = rows[rows < M_tail]
+    kk_max = (KT - 1) * kGK + 7 * 8
+    _check("split-K X", (M_main + rows) * k, (M_main + rows) * k + kk_max + 8, M * k)
+    # W fragments: row min(n0 + 16 * wave + c16, n - 1), k offset kt * 64 + ks * 32 + q4 * 8
+    n0 = np.arange(-(-n // kSN))[:, None] * kSN
+    wrow = np.minimum(n0 + np.arange(kSN)[None, :], n - 1).ravel()
+    _check("split-K W", wrow * k, wrow * k + (KT - 1) * kGK + 32 + 3 * 8 + 8, n * k)
+    # partial stores: part[s][row][col], row < M_tail, col < n (floats)
+    _check("split-K partials", 0, S * M_tail * n, S * M_tail * n)
+    # the reduction reads part[s * count + e] and writes y[M_main * n + e], e < count
+    count = M_tail * n
+    _check("reduce partials", 0, (S - 1) * count + count, S * count)
+    _check("reduce output", M_main * n, M_main * n + count, M * n)
+    # partial bytes end before the tail rows of y begin
+    assert S * count * 4 <= M_main * n * 2

@@ -137,7 +137,8 @@ def time_selective(cfg, k: int, batches, cos, sin, steps: int, warmup: int, stre
     coming first also keeps a short timed region in the state a long run
     reaches: right after the Full-Recompute leg's matrix work the shader
     clock is lower for some tens of milliseconds (20 timed steps measured
-    2.5% slower there). No host synchronisation between the passes."""
+    2.5% slower there). The host synchronises after the warm-up steps and
+    after the timed ones (that gap measured no slower than none)."""
     import torch
     from paper_2605_07443_amd import ops
     B, N, Hq, Hkv, D = cfg.B, cfg.N, cfg.Hq, cfg.Hkv, cfg.D
@@ -173,6 +174,7 @@ def time_selective(cfg, k: int, batches, cos, sin, steps: int, warmup: int, stre
     i_end.record(stream)
     for i in range(warmup):
         step(i)
+    torch.cuda.synchronize()   # the timed steps are bracketed by synchronisations
     t_start.record(stream)
     for i in range(steps):
         step(warmup + i)

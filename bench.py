@@ -67,6 +67,10 @@ def parse_args():
                     help="skip the other workloads (5 and 4 at 15%%, the ratio sweep on 4, 3 at 10%%, 1)")
     ap.add_argument("--no-full-prefill", action="store_true",
                     help="skip timing the Full-Recompute baseline")
+    ap.add_argument("--chain", choices=("auto", "copy", "vref"), default="auto",
+                    help="value rows: copied into the assembled V (copy) or read through a table "
+                         "of row addresses (vref); auto: vref where the library supports it "
+                         "(bf16, D = 128, at most 64 segments per request), else copy")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (HBM counter calibration)")
     return ap.parse_args()
@@ -112,6 +116,19 @@ def copy_calibration():
     print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 5}), flush=True)
 
 
+def use_vref(cfg, batches, chain: str) -> bool:
+    """Whether a workload runs the value-reference chain (see --chain)."""
+    ok = cfg.dtype == "bf16" and cfg.D == 128 and all(segs.S <= 64 for (_, segs, _) in batches)
+    if chain == "vref" and not ok:
+        raise SystemExit(f"--chain vref: workload {cfg.name} is outside the value-reference chain")
+    return chain == "vref" or (chain == "auto" and ok)
+
+
+def kern(kernels: dict, name: str) -> dict:
+    """Per-kernel figures by base name, whichever chain produced them."""
+    return kernels[name] if name in kernels else kernels[name + "_vref"]
+
+
 def make_batches(cfg, config_id: int, R: int, n_batches: int, dev):
     """`n_batches` independent request batches over one shared pool (so the
     working set exceeds the 256 MB Infinity Cache), each with its buffers."""
@@ -122,12 +139,14 @@ def make_batches(cfg, config_id: int, R: int, n_batches: int, dev):
         w = inputs.make(cfg, base + i, device=dev, pool_seed=base, pools=pools)
         pools = w.pools
         segs = ops.prepare_segments(w.segs, cfg.N, w.pools, dev)
-        bufs = ops.PrefillBuffers.alloc(cfg.B, cfg.N, cfg.Hq, cfg.Hkv, cfg.D, R, cfg.torch_dtype, dev)
+        bufs = ops.PrefillBuffers.alloc(cfg.B, cfg.N, cfg.Hq, cfg.Hkv, cfg.D, R, cfg.torch_dtype, dev,
+                                        v_ref=True)
         batches.append((w, segs, bufs))
     return batches
 
 
-def time_selective(cfg, k: int, batches, cos, sin, steps: int, warmup: int, stream) -> dict:
+def time_selective(cfg, k: int, batches, cos, sin, steps: int, warmup: int, stream,
+                   vref: bool = False) -> dict:
     """Per-kernel durations first: max(steps, 400) steps (gather + score ->
     top-k + patch -> attention, rotating over the batches) with HIP events on
     the launch stream between the kernels (each event record adds a gap to the
@@ -138,7 +157,9 @@ def time_selective(cfg, k: int, batches, cos, sin, steps: int, warmup: int, stre
     reaches: right after the Full-Recompute leg's matrix work the shader
     clock is lower for some tens of milliseconds (20 timed steps measured
     2.5% slower there). The host synchronises after the warm-up steps and
-    after the timed ones (that gap measured no slower than none)."""
+    after the timed ones (that gap measured no slower than none).
+    vref: the value-reference chain (K gathered and aligned, V read through a
+    table of row addresses) instead of the assembled copy."""
     import torch
     from paper_2605_07443_amd import ops
     B, N, Hq, Hkv, D = cfg.B, cfg.N, cfg.Hq, cfg.Hkv, cfg.D
@@ -149,15 +170,25 @@ def time_selective(cfg, k: int, batches, cos, sin, steps: int, warmup: int, stre
         w, segs, bufs = batches[i % len(batches)]
         if ev is not None:
             ev[0].record(stream)
-        ops.kv_assemble(w.pools, segs, w.k_fresh, w.v_fresh, cos, sin, bufs.k_asm, bufs.v_asm,
-                        scores_out=bufs.scores)
+        if vref:
+            ops.kv_assemble_vref(w.pools, segs, w.k_fresh, w.v_fresh, cos, sin, bufs.k_asm,
+                                 bufs.v_ref, scores_out=bufs.scores)
+        else:
+            ops.kv_assemble(w.pools, segs, w.k_fresh, w.v_fresh, cos, sin, bufs.k_asm, bufs.v_asm,
+                            scores_out=bufs.scores)
         if ev is not None:
             ev[1].record(stream)
-        ops.select_tokens(segs, k, w.k_fresh, w.v_fresh, bufs.k_asm, bufs.v_asm,
-                          scores_in=bufs.scores, rows_out=bufs.rows, patch=True)
+        if vref:
+            ops.select_tokens_vref(segs, k, w.k_fresh, w.v_fresh, bufs.k_asm, bufs.v_ref,
+                                   scores_in=bufs.scores, rows_out=bufs.rows)
+        else:
+            ops.select_tokens(segs, k, w.k_fresh, w.v_fresh, bufs.k_asm, bufs.v_asm,
+                              scores_in=bufs.scores, rows_out=bufs.rows, patch=True)
         if ev is not None:
             ev[2].record(stream)
-        if R > 0:
+        if R > 0 and vref:
+            ops.selective_attention_vref(w.q, bufs.k_asm, bufs.v_ref, bufs.rows, None, bufs.out)
+        elif R > 0:
             ops.selective_attention(w.q, bufs.k_asm, bufs.v_asm, bufs.rows, None, bufs.out)
         if ev is not None:
             ev[3].record(stream)
@@ -195,9 +226,16 @@ def time_selective(cfg, k: int, batches, cos, sin, steps: int, warmup: int, stre
 
     # assemble: read K,V rows, write K,V rows, read the fresh K row of every
     # cached position and write its score; select: read scores, write rows,
-    # patch k rows of K and V (read fresh, write assembled)
-    gather_bytes = 4.0 * B * N * row + 1.0 * B * (N - cfg.n_fresh) * row + 4.0 * B * N
-    select_bytes = 4.0 * B * N + 4.0 * B * R + 4.0 * B * k * row
+    # patch k rows of K and V (read fresh, write assembled). With value
+    # references the V rows are neither read nor written by these two: the
+    # gather writes one 8-byte address per position instead, the patch one
+    # per patched row.
+    if vref:
+        gather_bytes = 2.0 * B * N * row + 1.0 * B * (N - cfg.n_fresh) * row + 4.0 * B * N + 8.0 * B * N
+        select_bytes = 4.0 * B * N + 4.0 * B * R + 2.0 * B * k * row + 8.0 * B * k
+    else:
+        gather_bytes = 4.0 * B * N * row + 1.0 * B * (N - cfg.n_fresh) * row + 4.0 * B * N
+        select_bytes = 4.0 * B * N + 4.0 * B * R + 4.0 * B * k * row
     mfma_peak = BF16_PEAK_TFLOPS if cfg.dtype == "bf16" else F32_PEAK_TFLOPS
 
     def hbm(bytes_, ms):
@@ -206,10 +244,11 @@ def time_selective(cfg, k: int, batches, cos, sin, steps: int, warmup: int, stre
                 "frac": round(a / HBM_PEAK_GBS, 4), "bytes_per_launch": bytes_}
 
     att_tf = flops / (att_ms * 1e-3) / 1e12 if att_ms > 0 else 0.0
+    sfx = "_vref" if vref else ""
     kernels = {
-        "rc_kv_assemble": dict(us=round(asm_ms * 1e3, 2), **hbm(gather_bytes, asm_ms)),
-        "rc_select_tokens": dict(us=round(sel_ms * 1e3, 2), **hbm(select_bytes, sel_ms)),
-        "rc_selective_attention": {
+        "rc_kv_assemble" + sfx: dict(us=round(asm_ms * 1e3, 2), **hbm(gather_bytes, asm_ms)),
+        "rc_select_tokens" + sfx: dict(us=round(sel_ms * 1e3, 2), **hbm(select_bytes, sel_ms)),
+        "rc_selective_attention" + sfx: {
             "us": round(att_ms * 1e3, 2), "bound": "mfma" if cfg.dtype == "bf16" else "alu",
             "achieved": round(att_tf, 2), "peak": mfma_peak, "unit": "TFLOP/s",
             "frac": round(att_tf / mfma_peak, 4), "flops_per_launch": flops},
@@ -247,16 +286,19 @@ def other_workloads(args, dev, stream) -> dict:
             for (_, _, bufs) in batches:   # row and output buffers of this ratio
                 bufs.rows = torch.empty((cfg.B, R), dtype=torch.int32, device=dev)
                 bufs.out = torch.empty((cfg.B, R, cfg.Hq, cfg.D), dtype=cfg.torch_dtype, device=dev)
-            r = time_selective(cfg, k, batches, cos, sin, args.steps, args.warmup, stream)
+            vr = use_vref(cfg, batches, args.chain)
+            r = time_selective(cfg, k, batches, cos, sin, args.steps, args.warmup, stream, vref=vr)
             kk = r["kernels"]
             rows[str(pct)] = {
+                "chain": "vref" if vr else "copy",
                 "R": r["R"], "ms_per_step": r["ms_per_step"],
                 "selected_tokens_per_s": r["selected_tokens_per_s"],
                 "us_per_request": r["us_per_request"],
-                "gather_us": kk["rc_kv_assemble"]["us"], "gather_frac": kk["rc_kv_assemble"]["frac"],
-                "select_us": kk["rc_select_tokens"]["us"],
-                "attention_us": kk["rc_selective_attention"]["us"],
-                "attention_frac": kk["rc_selective_attention"]["frac"]}
+                "gather_us": kern(kk, "rc_kv_assemble")["us"],
+                "gather_frac": kern(kk, "rc_kv_assemble")["frac"],
+                "select_us": kern(kk, "rc_select_tokens")["us"],
+                "attention_us": kern(kk, "rc_selective_attention")["us"],
+                "attention_frac": kern(kk, "rc_selective_attention")["frac"]}
         name = f"config{cid}:{cfg.name}"
         out[name] = rows if len(pcts) > 1 else rows[str(pcts[0])]
         del batches
@@ -581,12 +623,21 @@ def main():
         f_ev[1].record(stream)
 
     # ---- the headline, timed last, right after the Full-Recompute work
-    head = time_selective(cfg, k, batches, cos, sin, args.steps, args.warmup, stream)
+    vref = use_vref(cfg, batches, args.chain)
+    head = time_selective(cfg, k, batches, cos, sin, args.steps, args.warmup, stream, vref=vref)
     ms_per_step = head["ms_per_step"]
     total_ms = head["total_ms"]
     kernels = head["kernels"]
     dominant = max(kernels, key=lambda n: kernels[n]["us"])
     dk = kernels[dominant]
+    # context: the chain that copies V into the assembled tensor, same batches
+    copy_chain = None
+    if vref:
+        c = time_selective(cfg, k, batches, cos, sin, args.steps, args.warmup, stream, vref=False)
+        copy_chain = {"ms_per_step": c["ms_per_step"],
+                      "value": round(B * R / (c["ms_per_step"] * 1e-3), 1),
+                      "kernels": c["kernels"],
+                      "vref_speedup": round(c["ms_per_step"] / ms_per_step, 3)}
     traffic = None
     tr = load_traffic(args.config, pct)
     digest = {"rc_kv_assemble": source_digest("assemble.hip"),
@@ -594,7 +645,8 @@ def main():
               "rc_selective_attention": source_digest("attention.hip"),
               "rc_attention_mass": source_digest("mass.hip"),
               "rc_gemm_bf16": source_digest("gemm.hip")}
-    if tr and tr.get("source_digest", {}).get(dominant) == digest[dominant]:
+    base_name = dominant[:-len("_vref")] if dominant.endswith("_vref") else dominant
+    if tr and tr.get("source_digest", {}).get(base_name) == digest[base_name]:
         traffic = tr.get("kernels", {}).get(dominant, {}).get("hbm_bytes")
     roofline = {"kernel": dominant, "bound": dk["bound"], "achieved": dk["achieved"],
                 "peak": dk["peak"], "unit": dk["unit"], "frac": dk["frac"], "traffic": traffic}
@@ -606,7 +658,7 @@ def main():
                 "selective_speedup": round(fms / ms_per_step, 3)}
         del fout
     if paged is not None:
-        paged["vs_assembled_step"] = round(ms_per_step / paged["ms"], 3)
+        paged["vs_headline_step"] = round(ms_per_step / paged["ms"], 3)
 
     # ---- CPU oracle on a bounded sample of the same workload
     cpu = None
@@ -652,12 +704,14 @@ def main():
         "vs_baseline": None,
         "dtype": cfg.dtype,
         "data": "synthetic",
-        "config": {"workload": f"config{args.config}:{cfg.name}", "B": B, "N": N,
+        "config": {"workload": f"config{args.config}:{cfg.name}",
+                   "chain": "vref" if vref else "copy", "B": B, "N": N,
                    "recompute_pct": pct, "selected_rows_per_request": R, "Hq": Hq, "Hkv": Hkv,
                    "D": D, "pools": [[cfg.hist_pool, cfg.hist_len], [cfg.item_pool, cfg.item_len]],
                    "batches_rotated": args.batches},
         "roofline": roofline,
         "kernels": kernels,
+        "assembled_copy_chain": copy_chain,
         "full_prefill": full,
         "rerope_standalone": rerope,
         "paged_prefill": paged,

@@ -48,6 +48,15 @@
  *                               live in pinned host memory (read over PCIe
  *                               by the kernel, zero-copy)
  *
+ * The same chain with the value rows taken by reference (only the key rows,
+ * which the alignment rotates, are copied; Sec. III-C.2a):
+ *
+ *   rc_kv_assemble_vref         assembly + alignment of K, and a table of
+ *                               value-row addresses (pool or fresh row)
+ *   rc_select_tokens_vref       top-k and correction (iii): fresh K rows
+ *                               copied, value entries redirected
+ *   rc_selective_attention_vref the attention, reading V through the table
+ *
  * Zero-copy variant and the local window:
  *
  *   rc_paged_attention          selective attention that reads K/V through
@@ -190,6 +199,26 @@ int rc_kv_assemble(const rc_shape* shape, const rc_pool* pools, int32_t n_pools,
                    const float* rope_cos, const float* rope_sin, int32_t max_pos, void* k_asm,
                    void* v_asm, float* scores_out, hipStream_t stream);
 
+/* rc_kv_assemble with the value rows taken by reference (Sec. III-C.3 (i)
+ * and (ii); the zero-copy retrieval of Sec. III-C.2a applied to V, which the
+ * alignment leaves unchanged): K_asm and scores_out exactly as rc_kv_assemble
+ * writes them, and instead of V_asm
+ *   v_ref[b*N + i] = byte address of the V row [Hkv, D] that rc_kv_assemble
+ *                    would copy to V_asm[b,i]: pool.v[block][i - dst_start]
+ *                    for a pool segment, V_fresh[b,i] for a fresh one, and
+ *                    V_fresh[b,i] for a position no valid segment covers.
+ * v_ref: device [B, N] uint64, must not alias an input; the table refers to
+ * the pools and to v_fresh, which must stay allocated and unchanged while it
+ * is used. k_asm and v_ref are required (no score-only form).
+ * Errors: those of rc_kv_assemble; UNSUPPORTED for S > 64 or a key row
+ * (Hkv * D * element size) that is not 32 bytes times a power of two up to
+ * 64 (64 bytes .. 2 KiB). */
+int rc_kv_assemble_vref(const rc_shape* shape, const rc_pool* pools, int32_t n_pools,
+                        const rc_segment* segs, int32_t S, const void* k_fresh,
+                        const void* v_fresh, const float* rope_cos, const float* rope_sin,
+                        int32_t max_pos, void* k_asm, uint64_t* v_ref, float* scores_out,
+                        hipStream_t stream);
+
 /* Standalone alignment (Sec. III-C.3 (ii)), in place: K[b,i] <- R(delta[b,i])
  * K[b,i] with the same fp32 operation order as rc_kv_assemble; a negative
  * delta uses cos(|delta|) and -sin(|delta|); rows with delta == 0 are not
@@ -230,6 +259,18 @@ int rc_select_tokens(const rc_shape* shape, const rc_segment* segs, int32_t S, i
                      void* v_asm, const float* scores_in, float* scores_out, int32_t* rows,
                      int32_t patch, hipStream_t stream);
 
+/* rc_select_tokens with patch = 1 over a value-reference table (Sec.
+ * III-C.3 (iii)): scores, rows and K_asm exactly as rc_select_tokens writes
+ * them, and for every selected cached position i of request b
+ *   v_ref[b*N + i] = byte address of V_fresh[b,i]
+ * instead of a copy of that row (other entries are left as they are).
+ * v_ref: device [B, N] uint64 from rc_kv_assemble_vref.
+ * Errors: those of rc_select_tokens with patch = 1. */
+int rc_select_tokens_vref(const rc_shape* shape, const rc_segment* segs, int32_t S,
+                          int32_t n_fresh, int32_t k, const void* k_fresh, const void* v_fresh,
+                          void* k_asm, uint64_t* v_ref, const float* scores_in,
+                          float* scores_out, int32_t* rows, hipStream_t stream);
+
 /* Selective attention (Eq. (1); Sec. III-C.2b: exact attention recomputed for
  * the selected rows over the full assembled context).
  * For r < R, p = rows[b*R + r] (or p = r when rows is NULL: Full-Recompute
@@ -261,6 +302,19 @@ int rc_selective_attention(const rc_shape* shape, const void* q, const int32_t* 
 int rc_selective_attention_lse(const rc_shape* shape, const void* q, const int32_t* rows,
                                int32_t R, const void* k, const void* v, float scale, void* out,
                                float* lse, hipStream_t stream);
+
+/* Attention as rc_selective_attention with the value rows taken by
+ * reference (Eq. (1); the gather of Sec. III-C.3 (i) then need not copy V):
+ * v_ref: device [B, N] of byte addresses, entry b*N + j the address of the
+ * V row [Hkv, D] that position j of request b uses (as written by
+ * rc_kv_assemble_vref and redirected by rc_select_tokens_vref). Outputs are
+ * bit-identical to rc_selective_attention over the V tensor those rows
+ * form. Every entry must address a readable V row: entries are not checked.
+ * bf16 with D = 128 only. Errors: those of rc_selective_attention;
+ * UNSUPPORTED for another dtype or D. */
+int rc_selective_attention_vref(const rc_shape* shape, const void* q, const int32_t* rows,
+                                int32_t R, const void* k, const uint64_t* v_ref, float scale,
+                                void* out, hipStream_t stream);
 
 /* Attention-mass term of Eq. (3) (Sec. III-C.2b: the first layer is computed
  * in full and a token's importance includes the attention weight it

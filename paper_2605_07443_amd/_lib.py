@@ -25,7 +25,8 @@ EXPORTS = ("rc_rope_table", "rc_kv_assemble", "rc_rerope", "rc_select_tokens",
            "rc_selective_attention", "rc_selective_attention_lse", "rc_attention_mass",
            "rc_select_tokens_eq3", "rc_paged_attention", "rc_segments_with_window",
            "rc_kv_gather_tokens", "rc_gemm_bf16", "rc_rmsnorm", "rc_qkv_rope", "rc_silu_mul",
-           "rc_gather_rows",
+           "rc_gather_rows", "rc_kv_assemble_vref", "rc_select_tokens_vref",
+           "rc_selective_attention_vref",
            "rc_status_string", "rc_last_error")
 
 
@@ -80,12 +81,13 @@ def load() -> ctypes.CDLL:
     L.rc_qkv_rope.argtypes = [P(RcShape), vp, vp, i32, vp, vp, i32, vp, vp, vp, vp]
     L.rc_silu_mul.argtypes = [i64, i32, vp, vp, vp]
     L.rc_gather_rows.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp]
-    for name in ("rc_rope_table", "rc_kv_assemble", "rc_rerope", "rc_select_tokens",
-                 "rc_selective_attention", "rc_selective_attention_lse", "rc_attention_mass",
-                 "rc_select_tokens_eq3", "rc_paged_attention", "rc_segments_with_window",
-                 "rc_kv_gather_tokens", "rc_gemm_bf16", "rc_rmsnorm", "rc_qkv_rope", "rc_silu_mul",
-                 "rc_gather_rows"):
-        getattr(L, name).restype = ctypes.c_int
+    L.rc_kv_assemble_vref.argtypes = L.rc_kv_assemble.argtypes
+    L.rc_select_tokens_vref.argtypes = [P(RcShape), vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp,
+                                        vp]
+    L.rc_selective_attention_vref.argtypes = [P(RcShape), vp, vp, i32, vp, vp, f32, vp, vp]
+    for name in EXPORTS:
+        if name not in ("rc_status_string", "rc_last_error"):
+            getattr(L, name).restype = ctypes.c_int
     L.rc_status_string.argtypes = [ctypes.c_int]
     L.rc_status_string.restype = ctypes.c_char_p
     L.rc_last_error.argtypes = []

@@ -246,7 +246,11 @@ __global__ __launch_bounds__(kThreads) void kv_rows_kernel(
 // issued before the first use. The deviation of a position is the sum of its
 // pairs' partials in a fixed order (shuffles within the lanes of one
 // position when ppr < 64, then a wave sum), so the score is deterministic.
-template <int ES, bool SCORE, bool WRITE, int KP>
+// VREF (with WRITE): value rows are not copied; v_out is then a table of one
+// 64-bit address per position, that of the row the copy would have read (the
+// pool row of a cached position, else the fresh row), lane t of the wave
+// writing the entry of its position t (T <= 64 with KP = 1).
+template <int ES, bool SCORE, bool WRITE, int KP, bool VREF = false>
 __global__ __launch_bounds__(kThreads) void kv_gather_kernel(
     PoolArgs pools, const int4* __restrict__ segs, int S, int N, int row_units, int head_units,
     int log2_ppr, const char* __restrict__ k_fresh, const char* __restrict__ v_fresh,
@@ -254,6 +258,7 @@ __global__ __launch_bounds__(kThreads) void kv_gather_kernel(
     char* __restrict__ k_out, char* __restrict__ v_out, float* __restrict__ scores) {
   constexpr int E = 16 / ES;     // elements per 16-byte unit
   constexpr int VP = 2 * KP;     // value units per lane
+  static_assert(!VREF || (WRITE && KP == 1), "value references need the writing instance, KP = 1");
   const int b = blockIdx.y;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -276,6 +281,7 @@ __global__ __launch_bounds__(kThreads) void kv_gather_kernel(
   const char* vsrc[VP] = {};
   int kd[KP] = {};
   bool kc[KP] = {};
+  uint64_t vref_own = 0;  // VREF: address of the value row of position lane
   // resolve the wave's positions one at a time (uniform values)
   for (int t = 0; t < T; ++t) {
     const int i = i0 + t;
@@ -310,9 +316,18 @@ __global__ __launch_bounds__(kThreads) void kv_gather_kernel(
         kd[k] = d;
         kc[k] = cached;
       }
+    if constexpr (VREF) {
+      const char* va = sv != nullptr ? sv : v_fresh + (static_cast<size_t>(b) * N + i) * row_bytes;
+      if (lane == t) vref_own = reinterpret_cast<uint64_t>(va);
+    } else {
 #pragma unroll
-    for (int k = 0; k < VP; ++k)
-      if (vt[k] == t) vsrc[k] = sv;
+      for (int k = 0; k < VP; ++k)
+        if (vt[k] == t) vsrc[k] = sv;
+    }
+  }
+  if constexpr (VREF) {
+    if (lane < T && i0 + lane < N)
+      reinterpret_cast<uint64_t*>(v_out)[static_cast<size_t>(b) * N + i0 + lane] = vref_own;
   }
 
   // ---- issue every load
@@ -335,7 +350,7 @@ __global__ __launch_bounds__(kThreads) void kv_gather_kernel(
       }
     }
   }
-  if constexpr (WRITE) {
+  if constexpr (WRITE && !VREF) {
 #pragma unroll
     for (int k = 0; k < VP; ++k)
       if (vsrc[k] != nullptr) vv[k] = reinterpret_cast<const u32x4*>(vsrc[k])[(k * 64 + lane) % row_units];
@@ -364,7 +379,7 @@ __global__ __launch_bounds__(kThreads) void kv_gather_kernel(
     }
     if (SCORE && kc[k]) part[k] = absdiff_sum<ES>(fa[k], ua[k]) + absdiff_sum<ES>(fb[k], ub[k]);
   }
-  if constexpr (WRITE) {
+  if constexpr (WRITE && !VREF) {
 #pragma unroll
     for (int k = 0; k < VP; ++k) {
       if (vsrc[k] == nullptr) continue;
@@ -470,7 +485,8 @@ template <bool ASSEMBLE, bool MAP = false>
 int launch_rows(const rc_shape* s, const PoolArgs& pools, const int4* segs, int S,
                 const void* k_fresh, const void* v_fresh, const int32_t* delta, const float* cos_t,
                 const float* sin_t, int max_pos, void* k_out, void* v_out, float* scores,
-                hipStream_t stream, const int4* map = nullptr, int max_wgs = 0) {
+                hipStream_t stream, const int4* map = nullptr, int max_wgs = 0,
+                bool vref = false) {
   const int es = elem_size(s->dtype);
   const int row_bytes = s->Hkv * s->D * es;
   const int row_units = row_bytes / 16;
@@ -524,7 +540,13 @@ int launch_rows(const rc_shape* s, const PoolArgs& pools, const int4* segs, int 
                          static_cast<char*>(k_out), static_cast<char*>(v_out), scores);
     };
     constexpr int KP = kWaveGatherKP;
-    if (scores && !k_out) {
+    if (vref && scores) {
+      if (s->dtype == RC_BF16) args2(kv_gather_kernel<2, true, true, KP, true>);
+      else args2(kv_gather_kernel<4, true, true, KP, true>);
+    } else if (vref) {
+      if (s->dtype == RC_BF16) args2(kv_gather_kernel<2, false, true, KP, true>);
+      else args2(kv_gather_kernel<4, false, true, KP, true>);
+    } else if (scores && !k_out) {
       if (s->dtype == RC_BF16) args2(kv_gather_kernel<2, true, false, KP>);
       else args2(kv_gather_kernel<4, true, false, KP>);
     } else if (scores) {
@@ -551,19 +573,23 @@ int launch_rows(const rc_shape* s, const PoolArgs& pools, const int4* segs, int 
     if (S <= kFewSegments) seg_table(std::true_type{});
     else seg_table(std::false_type{});
   }
-  return check_launch(MAP ? "rc_kv_gather_tokens" : ASSEMBLE ? "rc_kv_assemble" : "rc_rerope");
+  return check_launch(MAP ? "rc_kv_gather_tokens" : vref ? "rc_kv_assemble_vref"
+                      : ASSEMBLE ? "rc_kv_assemble" : "rc_rerope");
 }
 
 }  // namespace
 }  // namespace rc
 
-extern "C" int rc_kv_assemble(const rc_shape* shape, const rc_pool* pools, int32_t n_pools,
-                              const rc_segment* segs, int32_t S, const void* k_fresh,
-                              const void* v_fresh, const float* rope_cos, const float* rope_sin,
-                              int32_t max_pos, void* k_asm, void* v_asm, float* scores_out,
-                              hipStream_t stream) {
-  using namespace rc;
-  clear_error();
+namespace rc {
+namespace {
+
+// Checks and launch shared by rc_kv_assemble and rc_kv_assemble_vref (v_out:
+// the assembled value rows, or with vref the table of value-row addresses).
+int assemble_entry(const rc_shape* shape, const rc_pool* pools, int32_t n_pools,
+                   const rc_segment* segs, int32_t S, const void* k_fresh, const void* v_fresh,
+                   const float* rope_cos, const float* rope_sin, int32_t max_pos, void* k_asm,
+                   void* v_out, float* scores_out, hipStream_t stream, bool vref) {
+  const char* what = vref ? "v_ref" : "v_asm";
   if (int st = check_shape(shape, false)) return st;
   if (n_pools < 1 || n_pools > kMaxPools)
     return fail(n_pools > kMaxPools ? RC_ERR_UNSUPPORTED : RC_ERR_INVALID_ARG,
@@ -571,8 +597,10 @@ extern "C" int rc_kv_assemble(const rc_shape* shape, const rc_pool* pools, int32
   if (!pools) return fail(RC_ERR_INVALID_ARG, "pools is NULL");
   if (!segs || !k_fresh || !v_fresh)
     return fail(RC_ERR_INVALID_ARG, "segs, k_fresh and v_fresh must be non-NULL");
-  if ((k_asm == nullptr) != (v_asm == nullptr))
-    return fail(RC_ERR_INVALID_ARG, "k_asm and v_asm must both be given or both be NULL");
+  if (vref && (!k_asm || !v_out))
+    return fail(RC_ERR_INVALID_ARG, "k_asm and v_ref must be non-NULL");
+  if ((k_asm == nullptr) != (v_out == nullptr))
+    return fail(RC_ERR_INVALID_ARG, "k_asm and %s must both be given or both be NULL", what);
   if (!k_asm && !scores_out)
     return fail(RC_ERR_INVALID_ARG, "without k_asm/v_asm (score only) scores_out is required");
   if (S < 1) return fail(RC_ERR_INVALID_ARG, "S=%d must be >= 1", S);
@@ -581,8 +609,15 @@ extern "C" int rc_kv_assemble(const rc_shape* shape, const rc_pool* pools, int32
     return fail(RC_ERR_INVALID_ARG, "rope_cos and rope_sin must both be given or both be NULL");
   if (rope_cos && max_pos < shape->N)
     return fail(RC_ERR_INVALID_ARG, "max_pos=%d < N=%d", max_pos, shape->N);
-  if (k_asm && (k_asm == k_fresh || v_asm == v_fresh || k_asm == v_asm))
+  if (k_asm && (k_asm == k_fresh || v_out == v_fresh || k_asm == v_out))
     return fail(RC_ERR_INVALID_ARG, "outputs alias inputs");
+  if (vref) {
+    const int row_units = shape->Hkv * shape->D * elem_size(shape->dtype) / 16;
+    if (!wave_gather_ok(*shape, S, row_units))
+      return fail(RC_ERR_UNSUPPORTED,
+                  "value references need S <= 64 and a key row of a power-of-two number of "
+                  "32-byte pairs, at most 64 (S=%d, row of %d bytes)", S, row_units * 16);
+  }
   PoolArgs pa{};
   pa.n = n_pools;
   for (int p = 0; p < n_pools; ++p) {
@@ -594,8 +629,31 @@ extern "C" int rc_kv_assemble(const rc_shape* shape, const rc_pool* pools, int32
     pa.block_len[p] = pools[p].block_len;
   }
   return launch_rows<true>(shape, pa, reinterpret_cast<const int4*>(segs), S, k_fresh, v_fresh,
-                           nullptr, rope_cos, rope_sin, rope_cos ? max_pos : 0, k_asm, v_asm,
-                           scores_out, stream);
+                           nullptr, rope_cos, rope_sin, rope_cos ? max_pos : 0, k_asm, v_out,
+                           scores_out, stream, nullptr, 0, vref);
+}
+
+}  // namespace
+}  // namespace rc
+
+extern "C" int rc_kv_assemble(const rc_shape* shape, const rc_pool* pools, int32_t n_pools,
+                              const rc_segment* segs, int32_t S, const void* k_fresh,
+                              const void* v_fresh, const float* rope_cos, const float* rope_sin,
+                              int32_t max_pos, void* k_asm, void* v_asm, float* scores_out,
+                              hipStream_t stream) {
+  rc::clear_error();
+  return rc::assemble_entry(shape, pools, n_pools, segs, S, k_fresh, v_fresh, rope_cos, rope_sin,
+                            max_pos, k_asm, v_asm, scores_out, stream, false);
+}
+
+extern "C" int rc_kv_assemble_vref(const rc_shape* shape, const rc_pool* pools, int32_t n_pools,
+                                   const rc_segment* segs, int32_t S, const void* k_fresh,
+                                   const void* v_fresh, const float* rope_cos,
+                                   const float* rope_sin, int32_t max_pos, void* k_asm,
+                                   uint64_t* v_ref, float* scores_out, hipStream_t stream) {
+  rc::clear_error();
+  return rc::assemble_entry(shape, pools, n_pools, segs, S, k_fresh, v_fresh, rope_cos, rope_sin,
+                            max_pos, k_asm, v_ref, scores_out, stream, true);
 }
 
 extern "C" int rc_rerope(const rc_shape* shape, void* k, const int32_t* delta,

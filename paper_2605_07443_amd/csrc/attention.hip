@@ -132,6 +132,16 @@ __device__ __forceinline__ void dma16(uint32_t lds_addr, const void* gbase, uint
       : "memory");
 }
 
+// The same global->LDS load from a per-lane 64-bit address.
+__device__ __forceinline__ void dma16_abs(uint32_t lds_addr, const void* gaddr) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %2, off\n\ts_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds_addr), "v"(gaddr)
+      : "memory");
+}
+
 // A 16-byte LDS read at lds_addr + OFF bytes as assembly; valid after
 // lds_wait_tied has covered it.
 template <int OFF>
@@ -189,7 +199,7 @@ constexpr float kLazy = 8.f;
 // unrounded exponentials (the bf16 column sums only normalise O).
 // PAGED: k, v are the fresh tensors; other keys come from `pools` through
 // `segs` (S <= kPagedMaxSegments), rotated with the cos/sin tables when given.
-template <int D, bool SELECTIVE, bool LSE, bool PAGED>
+template <int D, bool SELECTIVE, bool LSE, bool PAGED, bool VREF = false>
 __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict__ rows, int R,
                       int N, int Hq, int Hkv, int G, int BR, int shift, const uint16_t* __restrict__ k,
@@ -204,6 +214,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
   constexpr int KU = kKT * UPR / kAttnThreads;   // K (and V) units per thread
   constexpr int KSTEP = kAttnThreads / UPR;      // keys between a thread's units
   constexpr bool DIRECT = (D == 128) && !PAGED;
+  static_assert(!VREF || DIRECT, "V rows by reference need the direct D = 128 staging");
   __shared__ std::conditional_t<DIRECT, AttnNone, AttnSmem<D>> sm;
   __shared__ std::conditional_t<DIRECT, AttnBufDirect, AttnNone> sbuf[2];
   __shared__ int s_ext[4];
@@ -313,8 +324,24 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
       const int row = wave * 16 + j * 4 + (lane >> 4);
       koff[j] = static_cast<uint32_t>((row * stride + g * D + (((lane & 15) ^ (row & 15)) * 8)) * 2);
       voff[j] = static_cast<uint32_t>((row * stride + g * D + (((lane & 15) ^ (2 * (row & 7))) * 8)) * 2);
+      // VREF: the byte offset of this lane's chunk within its V row
+      if constexpr (VREF) voff[j] = static_cast<uint32_t>((g * D + (((lane & 15) ^ (2 * (row & 7))) * 8)) * 2);
     }
   }
+  // VREF: v holds the address of every position's V row ([B, N], 8 bytes
+  // each); the entries of the rows this lane loads for the next tile are read
+  // one tile ahead (keys past N repeat key N - 1)
+  const uint64_t* vref = reinterpret_cast<const uint64_t*>(v);
+  uint64_t vent[VREF ? 4 : 1];
+  auto load_vent = [&](int t) {
+    if constexpr (VREF) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int key = min(t * kKT + wave * 16 + j * 4 + (lane >> 4), N - 1);
+        vent[j] = vref[static_cast<size_t>(b) * N + key];
+      }
+    }
+  };
   auto issue_tile = [&](int t, auto buf_tag) {
     if constexpr (DIRECT) {
       auto& dst = sbuf[decltype(buf_tag)::value];
@@ -326,8 +353,9 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
         for (int j = 0; j < 4; ++j) {
           dma16((uint32_t)(uintptr_t)((__attribute__((address_space(3))) uint16_t*)(&dst.k[(wave_u * 16 + j * 4) * 128])),
                 kt, koff[j]);
-          dma16((uint32_t)(uintptr_t)((__attribute__((address_space(3))) uint16_t*)(&dst.v[(wave_u * 16 + j * 4) * 128])),
-                vt, voff[j]);
+          const uint32_t vdst = (uint32_t)(uintptr_t)((__attribute__((address_space(3))) uint16_t*)(&dst.v[(wave_u * 16 + j * 4) * 128]));
+          if constexpr (VREF) dma16_abs(vdst, reinterpret_cast<const char*>(vent[j]) + voff[j]);
+          else dma16(vdst, vt, voff[j]);
         }
         return;
       }
@@ -342,9 +370,13 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
         __builtin_amdgcn_global_load_lds(
             (const __attribute__((address_space(1))) void*)(kr + ((ch ^ (row & 15)) * 8)),
             (__attribute__((address_space(3))) void*)(&dst.k[(wave * 16 + j * 4) * 128]), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds(
-            (const __attribute__((address_space(1))) void*)(vr + ((ch ^ (2 * (row & 7))) * 8)),
-            (__attribute__((address_space(3))) void*)(&dst.v[(wave * 16 + j * 4) * 128]), 16, 0, 0);
+        if constexpr (VREF)
+          dma16_abs((uint32_t)(uintptr_t)((__attribute__((address_space(3))) uint16_t*)(&dst.v[(wave_u * 16 + j * 4) * 128])),
+                    reinterpret_cast<const char*>(vent[j]) + voff[j]);
+        else
+          __builtin_amdgcn_global_load_lds(
+              (const __attribute__((address_space(1))) void*)(vr + ((ch ^ (2 * (row & 7))) * 8)),
+              (__attribute__((address_space(3))) void*)(&dst.v[(wave * 16 + j * 4) * 128]), 16, 0, 0);
       }
     }
   };
@@ -485,7 +517,9 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
   using Buf1 = std::integral_constant<int, 1>;
 
   if constexpr (DIRECT) {
+    load_vent(0);
     issue_tile(0, Buf0{});
+    if (n_kv > 1) load_vent(1);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
   } else {
@@ -697,7 +731,10 @@ void attn_bf16_kernel(const uint16_t* __restrict__ q, const int32_t* __restrict_
     using Next = std::integral_constant<int, cur ^ 1>;
     // DIRECT: the next tile flows into the other buffer during this one
     if constexpr (DIRECT) {
-      if (t + 1 < n_kv) issue_tile(t + 1, Next{});
+      if (t + 1 < n_kv) {
+        issue_tile(t + 1, Next{});
+        if (t + 2 < n_kv) load_vent(t + 2);
+      }
     }
 
     // a wave skips the tiles past all of its rows (their weights are zero)
@@ -838,7 +875,7 @@ struct Paged {
 // paged == nullptr: k, v are the assembled tensors; else the fresh tensors.
 int attention_impl(const rc_shape* shape, const void* q, const int32_t* rows, int32_t R,
                    const void* k, const void* v, float scale, void* out, float* lse,
-                   const Paged* paged, hipStream_t stream, const char* what) {
+                   const Paged* paged, hipStream_t stream, const char* what, bool vref = false) {
   if (int st = check_shape(shape, true)) return st;
   if (R < 0) return fail(RC_ERR_INVALID_ARG, "R=%d must be >= 0", R);
   if (!q || !k || !v || (!out && R > 0))
@@ -877,7 +914,10 @@ int attention_impl(const rc_shape* shape, const void* q, const int32_t* rows, in
                          scale_log2e, static_cast<uint16_t*>(out), lse, n_tiles, n_groups, gpx,
                          chunk, pg.pools, pg.segs, pg.S, pg.cos_t, pg.sin_t, pg.max_pos);
     };
-    if (paged) {
+    if (vref) {
+      rows ? launch(attn_bf16_kernel<128, true, false, false, true>)
+           : launch(attn_bf16_kernel<128, false, false, false, true>);
+    } else if (paged) {
       if (D == 128) launch(attn_bf16_kernel<128, true, false, true>);
       else launch(attn_bf16_kernel<64, true, false, true>);
     } else if (lse) {
@@ -930,6 +970,17 @@ extern "C" int rc_selective_attention_lse(const rc_shape* shape, const void* q,
   if (!lse && R > 0) return rc::fail(RC_ERR_INVALID_ARG, "lse must be non-NULL");
   return rc::attention_impl(shape, q, rows, R, k, v, scale, out, lse, nullptr, stream,
                             "rc_selective_attention_lse");
+}
+
+extern "C" int rc_selective_attention_vref(const rc_shape* shape, const void* q,
+                                           const int32_t* rows, int32_t R, const void* k,
+                                           const uint64_t* v_ref, float scale, void* out,
+                                           hipStream_t stream) {
+  rc::clear_error();
+  if (shape && (shape->dtype != RC_BF16 || shape->D != 128))
+    return rc::fail(RC_ERR_UNSUPPORTED, "V rows by reference: bf16 with D = 128 only");
+  return rc::attention_impl(shape, q, rows, R, k, v_ref, scale, out, nullptr, nullptr, stream,
+                            "rc_selective_attention_vref", true);
 }
 
 extern "C" int rc_paged_attention(const rc_shape* shape, const void* q, const int32_t* rows,

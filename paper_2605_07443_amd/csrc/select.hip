@@ -133,7 +133,10 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
 // Every part of a request computes the same selection; part 0 writes rows,
 // and with PATCH part p copies the rows of the cached positions whose output
 // slots are p, p + parts, ... (collected in an LDS list, one wave per row).
-template <int NC, int NJ, int TPB, bool PATCH>
+// VREF (with PATCH): v_asm is a table of 64-bit value-row addresses, one per
+// position; the patch copies the key row and points the position's entry at
+// its fresh value row instead of copying that row.
+template <int NC, int NJ, int TPB, bool PATCH, bool VREF = false>
 __global__ __launch_bounds__(TPB) void topk_kernel(
     const float* __restrict__ scores, const int4* __restrict__ segs, int S, int N,
     uint32_t item_mask, int k0, int k1, int R, int32_t* __restrict__ rows, int row_units,
@@ -144,6 +147,7 @@ __global__ __launch_bounds__(TPB) void topk_kernel(
   __shared__ uint32_t s_hist[3][kBins];
   __shared__ uint32_t s_coarse[3][kCoarse];
   constexpr int W = TPB / 64;                           // waves
+  static_assert(!VREF || PATCH, "value references are redirected by the patch");
   static_assert(W % 4 == 0 && NJ * W <= 256 && NJ <= kTopkMaxPer, "top-k shape");
   __shared__ uint32_t s_cnt[2][NJ * W];                  // per (j, wave): taken | ties << 16; ties of class 1
   __shared__ uint32_t s_bounds[2][3];                   // per class: min key, max key, candidates
@@ -395,7 +399,30 @@ __global__ __launch_bounds__(TPB) void topk_kernel(
   if (part == 0)
     for (int r = total + tid; r < R; r += TPB) rows[static_cast<size_t>(b) * R + r] = -1;
 
-  if constexpr (PATCH) {
+  if constexpr (PATCH && VREF) {
+    // (iii) heavy-hitter update: one wave per listed position copies the
+    // fresh K row over the assembled one and redirects the value entry
+    __syncthreads();
+    const int slots = (R + parts - 1) / parts;
+    for (int sl = wave; sl < slots; sl += TPB / 64) {
+      const int i = s_list[sl];
+      if (i < 0) continue;
+      const size_t off = (static_cast<size_t>(b) * N + i) * row_units;
+      const u32x4* kf = reinterpret_cast<const u32x4*>(k_fresh) + off;
+      u32x4* ka = reinterpret_cast<u32x4*>(k_asm) + off;
+      if (lane == 0)
+        reinterpret_cast<uint64_t*>(v_asm)[static_cast<size_t>(b) * N + i] =
+            reinterpret_cast<uint64_t>(reinterpret_cast<const u32x4*>(v_fresh) + off);
+      for (int u0 = 0; u0 < row_units; u0 += 128) {
+        const int u1 = u0 + lane, u2 = u0 + 64 + lane;
+        u32x4 ka1, ka2;
+        if (u1 < row_units) ka1 = __builtin_nontemporal_load(kf + u1);
+        if (u2 < row_units) ka2 = __builtin_nontemporal_load(kf + u2);
+        if (u1 < row_units) ka[u1] = ka1;
+        if (u2 < row_units) ka[u2] = ka2;
+      }
+    }
+  } else if constexpr (PATCH) {
     // (iii) heavy-hitter update: one wave per listed position copies the
     // fresh K and V rows over the assembled ones (16-byte units)
     __syncthreads();
@@ -505,7 +532,7 @@ int select_impl(const rc_shape* shape, const rc_segment* segs, int32_t S, int32_
                 bool eq3, uint32_t item_mask, float lambda, int32_t k0, int32_t k1,
                 const float* mass, const void* k_fresh, const void* v_fresh, void* k_asm,
                 void* v_asm, const float* scores_in, float* scores_out, int32_t* rows,
-                int32_t patch, hipStream_t stream, const char* what) {
+                int32_t patch, hipStream_t stream, const char* what, bool vref = false) {
   if (int st = check_shape(shape, false)) return st;
   const int N = shape->N, B = shape->B;
   const int ksum = k0 + k1;
@@ -527,7 +554,8 @@ int select_impl(const rc_shape* shape, const rc_segment* segs, int32_t S, int32_
   if (eq3 && !scores_in && !(lambda >= 0.f && lambda <= 1.f))
     return fail(RC_ERR_INVALID_ARG, "lambda must be in [0, 1]");
   if (patch && (!k_fresh || !v_fresh || !k_asm || !v_asm))
-    return fail(RC_ERR_INVALID_ARG, "patch needs k_fresh, v_fresh, k_asm and v_asm");
+    return fail(RC_ERR_INVALID_ARG, "patch needs k_fresh, v_fresh, k_asm and %s",
+                vref ? "v_ref" : "v_asm");
   if (B > 65535) return fail(RC_ERR_UNSUPPORTED, "B=%d exceeds 65535", B);
   const int es = elem_size(shape->dtype);
   const int row_units = shape->Hkv * shape->D * es / 16;
@@ -586,29 +614,33 @@ int select_impl(const rc_shape* shape, const rc_segment* segs, int32_t S, int32_
       hipLaunchKernelGGL(kern, dim3(parts, B), dim3(tpb), 0, stream, sc, segs4, S, N, item_mask, k0,
                          k1, R, rows, row_units, kf, vf, ka, va);
     };
-    auto by_chunks = [&](auto nc, auto pt) {
+    auto by_chunks = [&](auto nc, auto pt, auto vr) {
       constexpr int NC = decltype(nc)::value;
       constexpr bool PT = decltype(pt)::value;
+      constexpr bool VR = decltype(vr)::value && PT;
       switch ((N + 1023) / 1024) {
-        case 1: launch(topk_kernel<NC, 1, 1024, PT>, 1024); break;
-        case 2: launch(topk_kernel<NC, 2, 1024, PT>, 1024); break;
-        case 3: launch(topk_kernel<NC, 3, 1024, PT>, 1024); break;
-        case 4: launch(topk_kernel<NC, 4, 1024, PT>, 1024); break;
-        case 5: launch(topk_kernel<NC, 5, 1024, PT>, 1024); break;
-        case 6: launch(topk_kernel<NC, 6, 1024, PT>, 1024); break;
-        case 7: launch(topk_kernel<NC, 7, 1024, PT>, 1024); break;
-        case 8: launch(topk_kernel<NC, 8, 1024, PT>, 1024); break;
-        case 9: case 10: launch(topk_kernel<NC, 10, 1024, PT>, 1024); break;
-        case 11: case 12: launch(topk_kernel<NC, 12, 1024, PT>, 1024); break;
-        default: launch(topk_kernel<NC, 16, 1024, PT>, 1024); break;
+        case 1: launch(topk_kernel<NC, 1, 1024, PT, VR>, 1024); break;
+        case 2: launch(topk_kernel<NC, 2, 1024, PT, VR>, 1024); break;
+        case 3: launch(topk_kernel<NC, 3, 1024, PT, VR>, 1024); break;
+        case 4: launch(topk_kernel<NC, 4, 1024, PT, VR>, 1024); break;
+        case 5: launch(topk_kernel<NC, 5, 1024, PT, VR>, 1024); break;
+        case 6: launch(topk_kernel<NC, 6, 1024, PT, VR>, 1024); break;
+        case 7: launch(topk_kernel<NC, 7, 1024, PT, VR>, 1024); break;
+        case 8: launch(topk_kernel<NC, 8, 1024, PT, VR>, 1024); break;
+        case 9: case 10: launch(topk_kernel<NC, 10, 1024, PT, VR>, 1024); break;
+        case 11: case 12: launch(topk_kernel<NC, 12, 1024, PT, VR>, 1024); break;
+        default: launch(topk_kernel<NC, 16, 1024, PT, VR>, 1024); break;
       }
     };
     using One = std::integral_constant<int, 1>;
     using Two = std::integral_constant<int, 2>;
-    if (k1 > 0)
-      do_patch ? by_chunks(Two{}, std::true_type{}) : by_chunks(Two{}, std::false_type{});
-    else
-      do_patch ? by_chunks(One{}, std::true_type{}) : by_chunks(One{}, std::false_type{});
+    auto by_patch = [&](auto nc) {
+      if (!do_patch) by_chunks(nc, std::false_type{}, std::false_type{});
+      else if (vref) by_chunks(nc, std::true_type{}, std::true_type{});
+      else by_chunks(nc, std::true_type{}, std::false_type{});
+    };
+    if (k1 > 0) by_patch(Two{});
+    else by_patch(One{});
     if (int st = check_launch(what)) return st;
   }
   return RC_OK;
@@ -644,4 +676,15 @@ extern "C" int rc_select_tokens_eq3(const rc_shape* shape, const rc_segment* seg
   return rc::select_impl(shape, segs, S, n_fresh, true, item_pool_mask, lambda, k_hist, k_item,
                          mass, k_fresh, v_fresh, k_asm, v_asm, scores_in, scores_out, rows, patch,
                          stream, "rc_select_tokens_eq3");
+}
+
+extern "C" int rc_select_tokens_vref(const rc_shape* shape, const rc_segment* segs, int32_t S,
+                                     int32_t n_fresh, int32_t k, const void* k_fresh,
+                                     const void* v_fresh, void* k_asm, uint64_t* v_ref,
+                                     const float* scores_in, float* scores_out, int32_t* rows,
+                                     hipStream_t stream) {
+  rc::clear_error();
+  return rc::select_impl(shape, segs, S, n_fresh, false, 0u, 1.f, k, 0, nullptr, k_fresh, v_fresh,
+                         k_asm, v_ref, scores_in, scores_out, rows, 1, stream,
+                         "rc_select_tokens_vref", true);
 }

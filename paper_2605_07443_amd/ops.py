@@ -181,6 +181,31 @@ def kv_assemble(pools, segs: Segments, k_fresh, v_fresh, cos=None, sin=None, k_o
     return (None, None) if score_only else (k_out, v_out)
 
 
+def kv_assemble_vref(pools, segs: Segments, k_fresh, v_fresh, cos=None, sin=None, k_out=None,
+                     v_ref=None, scores_out=None, stream=None):
+    """rc_kv_assemble_vref: gather + fused re-alignment of K (+ deviation
+    scores), and a table v_ref [B, N] int64 of value-row byte addresses (pool
+    or fresh row) instead of a copy of V. The table refers to the pool tensors
+    and to v_fresh: they must outlive its use. Returns (k_asm, v_ref)."""
+    B, N, Hkv, D = k_fresh.shape
+    if v_fresh.shape != k_fresh.shape or v_fresh.dtype != k_fresh.dtype:
+        raise ValueError("k_fresh and v_fresh must match")
+    k_out = torch.empty_like(k_fresh) if k_out is None else k_out
+    if v_ref is None:
+        v_ref = torch.empty((B, N), dtype=torch.int64, device=k_fresh.device)
+    elif v_ref.dtype != torch.int64 or tuple(v_ref.shape) != (B, N):
+        raise ValueError("v_ref must be int64 [B, N]")
+    parr = _pool_array(pools, k_fresh.dtype, Hkv, D)
+    max_pos = 0 if cos is None else int(cos.shape[0])
+    check(_lib.load().rc_kv_assemble_vref(
+        ctypes.byref(_shape(B, N, 1, Hkv, D, _dtype_code(k_fresh))), parr, len(pools),
+        _dev(segs.dev, "segs"), segs.S, _dev(k_fresh, "k_fresh"), _dev(v_fresh, "v_fresh"),
+        None if cos is None else _dev(cos, "cos"), None if sin is None else _dev(sin, "sin"),
+        max_pos, _dev(k_out, "k_out"), _dev(v_ref, "v_ref"),
+        None if scores_out is None else _dev(scores_out, "scores_out"), _stream(stream)))
+    return k_out, v_ref
+
+
 def kv_gather_tokens(pools, token_map, k_fresh, v_fresh, cos=None, sin=None, k_out=None,
                      v_out=None, scores_out=None, stream=None, max_workgroups=0):
     """rc_kv_gather_tokens: per-position map gather + alignment (+ deviation
@@ -239,6 +264,53 @@ def select_tokens(segs: Segments, k: int, k_fresh, v_fresh, k_asm, v_asm, scores
     if DEBUG:
         check_rows(rows, N, "rc_select_tokens")
     return rows, (scores_out if scores_out is not None else scores_in)
+
+
+def select_tokens_vref(segs: Segments, k: int, k_fresh, v_fresh, k_asm, v_ref, scores_in=None,
+                       scores_out=None, rows_out=None, stream=None):
+    """rc_select_tokens_vref: score, top-k, and the correction over a value
+    reference table (fresh K rows copied, value entries of the selected
+    positions pointed at their fresh rows). Returns (rows, scores)."""
+    B, N, Hkv, D = k_fresh.shape
+    R = segs.n_fresh + int(k)
+    if v_ref.dtype != torch.int64 or tuple(v_ref.shape) != (B, N):
+        raise ValueError("v_ref must be int64 [B, N]")
+    rows = torch.empty((B, R), dtype=torch.int32, device=k_fresh.device) if rows_out is None else rows_out
+    if scores_in is None and scores_out is None:
+        scores_out = torch.empty((B, N), dtype=torch.float32, device=k_fresh.device)
+    check(_lib.load().rc_select_tokens_vref(
+        ctypes.byref(_shape(B, N, 1, Hkv, D, _dtype_code(k_fresh))), _dev(segs.dev, "segs"),
+        segs.S, segs.n_fresh, int(k), _dev(k_fresh, "k_fresh"), _dev(v_fresh, "v_fresh"),
+        _dev(k_asm, "k_asm"), _dev(v_ref, "v_ref"),
+        None if scores_in is None else _dev(scores_in, "scores_in"),
+        None if scores_out is None else _dev(scores_out, "scores_out"),
+        _dev(rows, "rows"), _stream(stream)))
+    if DEBUG:
+        check_rows(rows, N, "rc_select_tokens_vref")
+    return rows, (scores_out if scores_out is not None else scores_in)
+
+
+def selective_attention_vref(q, k, v_ref, rows=None, scale=None, out=None, stream=None):
+    """rc_selective_attention_vref: rc_selective_attention with V read
+    through v_ref [B, N] int64 (value-row byte addresses); bf16, D = 128."""
+    B, N, Hq, D = q.shape
+    Hkv = k.shape[2]
+    if k.shape[:2] != q.shape[:2] or k.shape[3] != D:
+        raise ValueError("q [B,N,Hq,D] and k [B,N,Hkv,D] do not match")
+    if v_ref.dtype != torch.int64 or tuple(v_ref.shape) != (B, N):
+        raise ValueError("v_ref must be int64 [B, N]")
+    R = N if rows is None else int(rows.shape[1])
+    if rows is not None and (rows.dtype != torch.int32 or rows.shape[0] != B):
+        raise ValueError("rows must be int32 [B, R]")
+    scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
+    out = torch.empty((B, R, Hq, D), dtype=q.dtype, device=q.device) if out is None else out
+    if DEBUG and rows is not None:
+        check_rows(rows, N, "rc_selective_attention_vref")
+    check(_lib.load().rc_selective_attention_vref(
+        ctypes.byref(_shape(B, N, Hq, Hkv, D, _dtype_code(q))), _dev(q, "q"),
+        None if rows is None else _dev(rows, "rows"), R, _dev(k, "k"), _dev(v_ref, "v_ref"),
+        ctypes.c_float(scale), _dev(out, "out"), _stream(stream)))
+    return out
 
 
 def selective_attention(q, k, v, rows=None, scale=None, out=None, stream=None):
@@ -377,19 +449,21 @@ def segments_with_window(segs, N: int, W: int) -> np.ndarray:
 @dataclass
 class PrefillBuffers:
     k_asm: torch.Tensor
-    v_asm: torch.Tensor
+    v_asm: torch.Tensor | None      # assembled V (None: value rows by reference)
     scores: torch.Tensor
     rows: torch.Tensor
     out: torch.Tensor
+    v_ref: torch.Tensor | None = None   # [B, N] int64 value-row addresses
 
     @staticmethod
-    def alloc(B, N, Hq, Hkv, D, R, dtype, device):
+    def alloc(B, N, Hq, Hkv, D, R, dtype, device, v_copy=True, v_ref=False):
         return PrefillBuffers(
             k_asm=torch.empty((B, N, Hkv, D), dtype=dtype, device=device),
-            v_asm=torch.empty((B, N, Hkv, D), dtype=dtype, device=device),
+            v_asm=torch.empty((B, N, Hkv, D), dtype=dtype, device=device) if v_copy else None,
             scores=torch.empty((B, N), dtype=torch.float32, device=device),
             rows=torch.empty((B, R), dtype=torch.int32, device=device),
-            out=torch.empty((B, R, Hq, D), dtype=dtype, device=device))
+            out=torch.empty((B, R, Hq, D), dtype=dtype, device=device),
+            v_ref=torch.empty((B, N), dtype=torch.int64, device=device) if v_ref else None)
 
 
 def selective_prefill(q, k_fresh, v_fresh, pools, segs: Segments, k: int, cos, sin,
@@ -409,6 +483,29 @@ def selective_prefill(q, k_fresh, v_fresh, pools, segs: Segments, k: int, cos, s
                   rows_out=bufs.rows, patch=True, stream=stream)
     if R > 0:
         selective_attention(q, bufs.k_asm, bufs.v_asm, bufs.rows, scale, bufs.out, stream)
+    return bufs
+
+
+def selective_prefill_vref(q, k_fresh, v_fresh, pools, segs: Segments, k: int, cos, sin,
+                           scale=None, bufs: PrefillBuffers | None = None, stream=None):
+    """selective_prefill with the value rows taken by reference: the gather
+    copies and aligns K and writes a table of value-row addresses, the patch
+    copies fresh K rows and redirects their value entries, and the attention
+    reads V through the table (bf16, D = 128). The pools and v_fresh must
+    outlive the use of bufs.v_ref. Returns the buffers (k_asm patched,
+    v_ref, scores, rows, out)."""
+    B, N, Hq, D = q.shape
+    Hkv = k_fresh.shape[2]
+    R = segs.n_fresh + int(k)
+    if bufs is None:
+        bufs = PrefillBuffers.alloc(B, N, Hq, Hkv, D, R, q.dtype, q.device, v_copy=False,
+                                    v_ref=True)
+    kv_assemble_vref(pools, segs, k_fresh, v_fresh, cos, sin, bufs.k_asm, bufs.v_ref,
+                     scores_out=bufs.scores, stream=stream)
+    select_tokens_vref(segs, k, k_fresh, v_fresh, bufs.k_asm, bufs.v_ref, scores_in=bufs.scores,
+                       rows_out=bufs.rows, stream=stream)
+    if R > 0:
+        selective_attention_vref(q, bufs.k_asm, bufs.v_ref, bufs.rows, scale, bufs.out, stream)
     return bufs
 
 

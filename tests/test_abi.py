@@ -114,6 +114,54 @@ def test_assemble_validation(lib):
 
 
 @no_gpu
+def test_value_reference_validation(lib):
+    """The value-reference chain checks what rc_kv_assemble, rc_select_tokens
+    and rc_selective_attention check, plus its own limits: the wave-level
+    gather's shapes (S <= 64, a key row of 32 bytes times a power of two up to
+    64) and bf16 with D = 128 for the attention."""
+    ok = dict(pools=_pools(), n=1, segs=FAKE, S=3, kf=FAKE, vf=FAKE + 8, cos=FAKE, sin=FAKE,
+              max_pos=64, ka=FAKE + 16, vr=FAKE + 24, sc=None)
+
+    def asm(shape=None, **kw):
+        a = dict(ok, **kw)
+        return lib.rc_kv_assemble_vref(_shape() if shape is None else shape, a["pools"], a["n"],
+                                       a["segs"], a["S"], a["kf"], a["vf"], a["cos"], a["sin"],
+                                       a["max_pos"], a["ka"], a["vr"], a["sc"], None)
+
+    assert asm(segs=None) == -1
+    assert asm(vr=None) == -1
+    assert asm(ka=None, vr=None, sc=FAKE + 32) == -1      # no score-only form
+    assert asm(vr=FAKE + 8) == -1                          # table aliases v_fresh
+    assert asm(max_pos=63) == -1
+    st, msg = _err(asm(S=65), lib)
+    assert st == -2 and "S=65" in msg
+    assert asm(shape=_shape(Hkv=3)) == -2                  # 24 pairs: not a power of two
+    assert asm(shape=_shape(Hkv=16)) == -2                 # 128 pairs
+    assert asm(shape=_shape(D=96)) == -2
+
+    def sel(shape=None, k=10, rows=FAKE, vr=FAKE + 24, ka=FAKE + 16, scores_in=FAKE + 32):
+        return lib.rc_select_tokens_vref(_shape() if shape is None else shape, FAKE, 3, 8, k, FAKE,
+                                         FAKE + 8, ka, vr, scores_in, None, rows, None)
+
+    assert sel(vr=None) == -1
+    assert sel(ka=None) == -1
+    assert sel(k=57) == -1
+    assert sel(rows=None) == -1
+    assert sel(shape=_shape(N=16385)) == -2
+
+    def att(shape=None, q=FAKE, vr=FAKE + 8, R=10):
+        return lib.rc_selective_attention_vref(_shape() if shape is None else shape, q, FAKE, R,
+                                               FAKE + 16, vr, ctypes.c_float(0.088), FAKE + 24,
+                                               None)
+
+    assert att(q=None) == -1
+    assert att(vr=None) == -1
+    assert att(shape=_shape(dtype=0)) == -2                # fp32
+    assert att(shape=_shape(D=64)) == -2
+    assert att(R=0) == 0
+
+
+@no_gpu
 def test_rerope_validation(lib):
     assert lib.rc_rerope(_shape(), None, FAKE, FAKE, FAKE, 8, None) == -1
     assert lib.rc_rerope(_shape(), FAKE, FAKE, FAKE, FAKE, 0, None) == -1

@@ -1,0 +1,161 @@
+"""GPU parity of the value-reference chain (rc_kv_assemble_vref ->
+rc_select_tokens_vref -> rc_selective_attention_vref), called through the C
+ABI, against the CPU oracle and against the assembled chain on the same
+seeded inputs.
+
+Bar: assembled and patched K bit-exact against the oracle; deviation scores
+and selected rows bit-identical to the assembled chain's; every value-row
+address equal to the one computed on the host from the segment table, the
+pool tensors and the selected rows; attention outputs bit-identical to
+rc_selective_attention over the assembled copy, and within max-abs 2e-2 /
+mean-abs 2e-3 of the oracle on the rows checked."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2605_07443_amd import _lib, inputs, ops
+
+from parity import H, assert_attn_close, oracle_attention_rows, sample_rows, say
+
+pytestmark = pytest.mark.gpu
+
+DEV = torch.device("cuda:0")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib_loaded():
+    _lib.load()
+    yield
+    torch.cuda.synchronize()
+
+
+def expected_vref(w, rows: np.ndarray) -> np.ndarray:
+    """Byte address of the value row each position reads: the pool row of a
+    cached position, the fresh row of a fresh or selected one."""
+    B, N, Hkv, D = w.v_fresh.shape
+    row_bytes = Hkv * D * w.v_fresh.element_size()
+    fresh = w.v_fresh.data_ptr() + row_bytes * np.arange(B * N, dtype=np.int64).reshape(B, N)
+    exp = fresh.copy()
+    for b, req in enumerate(w.segs.numpy()):
+        for dst, ln, p, blk in req.tolist():
+            if p < 0:
+                continue
+            pv = w.pools[p][1]
+            base = pv.data_ptr() + (blk * pv.shape[1]) * row_bytes
+            exp[b, dst:dst + ln] = base + row_bytes * np.arange(ln, dtype=np.int64)
+        r = rows[b][rows[b] >= 0]
+        exp[b, r] = fresh[b, r]
+    return exp
+
+
+def run_both(cfg, w, k):
+    """The assembled chain and the value-reference chain on the same inputs."""
+    segs = ops.prepare_segments(w.segs, cfg.N, w.pools, DEV)
+    cos, sin = ops.rope_table(cfg.N, cfg.D, cfg.rope_base, DEV)
+    sc_a = torch.empty((cfg.B, cfg.N), dtype=torch.float32, device=DEV)
+    k_asm, v_asm = ops.kv_assemble(w.pools, segs, w.k_fresh, w.v_fresh, cos, sin, scores_out=sc_a)
+    rows_a, _ = ops.select_tokens(segs, k, w.k_fresh, w.v_fresh, k_asm, v_asm, scores_in=sc_a,
+                                  patch=True)
+    R = rows_a.shape[1]
+    out_a = ops.selective_attention(w.q, k_asm, v_asm, rows_a) if R > 0 else None
+
+    sc_r = torch.empty((cfg.B, cfg.N), dtype=torch.float32, device=DEV)
+    k_ref, v_ref = ops.kv_assemble_vref(w.pools, segs, w.k_fresh, w.v_fresh, cos, sin,
+                                        scores_out=sc_r)
+    table_pre = v_ref.clone()
+    k_pre = k_ref.clone()
+    rows_r, _ = ops.select_tokens_vref(segs, k, w.k_fresh, w.v_fresh, k_ref, v_ref, scores_in=sc_r)
+    out_r = ops.selective_attention_vref(w.q, k_ref, v_ref, rows_r) if R > 0 else None
+    torch.cuda.synchronize()
+    return dict(segs=segs, sc_a=sc_a, rows_a=rows_a, k_asm=k_asm, v_asm=v_asm, out_a=out_a,
+                sc_r=sc_r, rows_r=rows_r, k_ref=k_ref, v_ref=v_ref, out_r=out_r,
+                table_pre=table_pre, k_pre=k_pre)
+
+
+def check_against_assembled(w, r):
+    np.testing.assert_array_equal(r["sc_r"].cpu().numpy(), r["sc_a"].cpu().numpy(),
+                                  err_msg="scores of the value-reference gather differ")
+    rows = r["rows_r"].cpu().numpy()
+    np.testing.assert_array_equal(rows, r["rows_a"].cpu().numpy(), err_msg="rows differ")
+    np.testing.assert_array_equal(H(r["k_ref"]), H(r["k_asm"]), err_msg="patched K differs")
+    # the table before the patch: every position's gather source
+    no_sel = np.full((rows.shape[0], 0), -1, np.int32)
+    np.testing.assert_array_equal(r["table_pre"].cpu().numpy(), expected_vref(w, no_sel),
+                                  err_msg="value-row addresses of the gather differ")
+    np.testing.assert_array_equal(r["v_ref"].cpu().numpy(), expected_vref(w, rows),
+                                  err_msg="value-row addresses after the patch differ")
+    if r["out_a"] is not None:
+        np.testing.assert_array_equal(H(r["out_r"]), H(r["out_a"]),
+                                      err_msg="attention through references differs")
+    return rows
+
+
+SMALL = ["tiny-bf16", "ragged-bf16", "miss-bf16", "allfresh-bf16"]
+
+
+@pytest.mark.parametrize("name", SMALL)
+@pytest.mark.parametrize("pct", [0, 15, 100])
+def test_vref_chain_small(name, pct):
+    cfg = inputs.TEST_WORKLOADS[name]
+    say(f"[vref] {name} pct={pct} N={cfg.N} B={cfg.B}")
+    w = inputs.make(cfg, 300 + pct, device=DEV)
+    k = cfg.k_for(pct)
+    r = run_both(cfg, w, k)
+    rows = check_against_assembled(w, r)
+
+    # against the oracle: assembled K before the patch, patched K, attention
+    ocos, osin = O.rope_table(cfg.N, cfg.D, cfg.rope_base)
+    subpools, segs_sub = inputs.referenced_subpools(w)
+    kf, vf = H(w.k_fresh), H(w.v_fresh)
+    ka_o, va_o = O.assemble(kf, vf, subpools, segs_sub, ocos, osin)
+    np.testing.assert_array_equal(H(r["k_pre"]), ka_o, err_msg="assembled K differs from the oracle")
+    sc_o = O.deviation(kf, ka_o)
+    np.testing.assert_allclose(r["sc_r"].cpu().numpy(), sc_o, rtol=1e-5, atol=1e-5)
+    kp_o, vp_o = O.patch(w.segs.numpy(), rows, kf, vf, ka_o, va_o)
+    np.testing.assert_array_equal(H(r["k_ref"]), kp_o, err_msg="patched K differs from the oracle")
+    if r["out_r"] is not None:
+        sel = sample_rows(cfg.B, rows.shape[1], 1)
+        ref = oracle_attention_rows(H(w.q), kp_o, vp_o, rows, sel)
+        g = np.concatenate([H(r["out_r"])[b, idx] for b, idx in enumerate(sel)])
+        say(f"  {assert_attn_close(g, np.concatenate(ref), cfg.dtype, 'vref attention')}")
+
+
+@pytest.mark.parametrize("cid,stride", [(2, 16), (4, 16), (5, 64)])
+def test_vref_chain_full_workloads(cid, stride):
+    """Full sizes at 15% recompute, in the launch configuration the benchmark
+    times: the chain is bit-identical to the assembled one, K against the
+    oracle, and sampled rows of the attention against the oracle."""
+    cfg = inputs.WORKLOADS[cid]
+    k = cfg.k_for(15)
+    say(f"[vref] workload {cid} B={cfg.B} N={cfg.N} k={k}")
+    w = inputs.make(cfg, 4200 + cid, device=DEV)
+    r = run_both(cfg, w, k)
+    rows = check_against_assembled(w, r)
+    ocos, osin = O.rope_table(cfg.N, cfg.D, cfg.rope_base)
+    subpools, segs_sub = inputs.referenced_subpools(w)
+    kf, vf = H(w.k_fresh), H(w.v_fresh)
+    ka_o, va_o = O.assemble(kf, vf, subpools, segs_sub, ocos, osin)
+    np.testing.assert_array_equal(H(r["k_pre"]), ka_o, err_msg="assembled K differs from the oracle")
+    kp_o, vp_o = O.patch(w.segs.numpy(), rows, kf, vf, ka_o, va_o)
+    np.testing.assert_array_equal(H(r["k_ref"]), kp_o, err_msg="patched K differs from the oracle")
+    sel = sample_rows(cfg.B, rows.shape[1], stride)
+    ref = oracle_attention_rows(H(w.q), kp_o, vp_o, rows, sel)
+    outh = H(r["out_r"])
+    g = np.concatenate([outh[b, idx] for b, idx in enumerate(sel)])
+    say(f"  {assert_attn_close(g, np.concatenate(ref), cfg.dtype, 'vref attention')}")
+    del w, r
+    torch.cuda.empty_cache()
+
+
+def test_vref_rejects_unsupported_shapes():
+    cfg = inputs.TEST_WORKLOADS["mha-d64-bf16"]
+    w = inputs.make(cfg, 7, device=DEV)
+    segs = ops.prepare_segments(w.segs, cfg.N, w.pools, DEV)
+    cos, sin = ops.rope_table(cfg.N, cfg.D, cfg.rope_base, DEV)
+    k_ref, v_ref = ops.kv_assemble_vref(w.pools, segs, w.k_fresh, w.v_fresh, cos, sin)
+    rows, _ = ops.select_tokens_vref(segs, cfg.k, w.k_fresh, w.v_fresh, k_ref, v_ref)
+    with pytest.raises(_lib.RcError) as e:
+        ops.selective_attention_vref(w.q, k_ref, v_ref, rows)
+    assert e.value.status == _lib.RC_ERR_UNSUPPORTED
+    torch.cuda.synchronize()

@@ -148,6 +148,49 @@ def test_vref_chain_full_workloads(cid, stride):
     torch.cuda.empty_cache()
 
 
+def test_vref_full_prefill_mode_equals_plain():
+    """rows = NULL (every row, the Full-Recompute baseline) through a table
+    that points at the rows of V itself: bit-identical to the plain call."""
+    cfg = inputs.TEST_WORKLOADS["ragged-bf16"]
+    w = inputs.make(cfg, 11, device=DEV)
+    B, N, Hkv, D = w.v_fresh.shape
+    row_bytes = Hkv * D * w.v_fresh.element_size()
+    table = (w.v_fresh.data_ptr() + row_bytes * torch.arange(B * N, device=DEV, dtype=torch.int64)).view(B, N)
+    ref = ops.selective_attention(w.q, w.k_fresh, w.v_fresh)
+    got = ops.selective_attention_vref(w.q, w.k_fresh, table)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(H(got), H(ref))
+
+
+def test_vref_unresolved_positions_point_at_fresh_rows():
+    """A segment naming a block outside its pool leaves its positions
+    unresolved: the gather writes no key row there (as rc_kv_assemble) and
+    their table entries address the fresh V rows, so that the table never
+    holds an unreadable address."""
+    cfg = inputs.TEST_WORKLOADS["tiny-bf16"]
+    w = inputs.make(cfg, 21, device=DEV)
+    segs_h = w.segs.clone()
+    bad = [s for s in range(segs_h.shape[1]) if int(segs_h[0, s, 2]) >= 0][0]
+    pool = int(segs_h[0, bad, 2])
+    segs_h[0, bad, 3] = w.pools[pool][0].shape[0] + 5          # block past the pool's end
+    segs = ops.prepare_segments(segs_h, cfg.N, w.pools, DEV, check_blocks=False)
+    cos, sin = ops.rope_table(cfg.N, cfg.D, cfg.rope_base, DEV)
+    k_ref = torch.zeros_like(w.k_fresh)
+    k_ref, v_ref = ops.kv_assemble_vref(w.pools, segs, w.k_fresh, w.v_fresh, cos, sin, k_out=k_ref)
+    torch.cuda.synchronize()
+    dst, ln = int(segs_h[0, bad, 0]), int(segs_h[0, bad, 1])
+    row_bytes = cfg.Hkv * cfg.D * w.v_fresh.element_size()
+    want = w.v_fresh.data_ptr() + row_bytes * (np.arange(dst, dst + ln, dtype=np.int64))
+    np.testing.assert_array_equal(v_ref.cpu().numpy()[0, dst:dst + ln], want)
+    assert not k_ref[0, dst:dst + ln].any(), "unresolved key rows must not be written"
+    # the other entries are those of the well-formed table
+    good = expected_vref(w, np.full((cfg.B, 0), -1, np.int32))
+    got = v_ref.cpu().numpy()
+    mask = np.ones_like(got, dtype=bool)
+    mask[0, dst:dst + ln] = False
+    np.testing.assert_array_equal(got[mask], good[mask])
+
+
 def test_vref_rejects_unsupported_shapes():
     cfg = inputs.TEST_WORKLOADS["mha-d64-bf16"]
     w = inputs.make(cfg, 7, device=DEV)

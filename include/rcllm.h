@@ -211,8 +211,8 @@ int rc_kv_assemble(const rc_shape* shape, const rc_pool* pools, int32_t n_pools,
  * the pools and to v_fresh, which must stay allocated and unchanged while it
  * is used. k_asm and v_ref are required (no score-only form).
  * Errors: those of rc_kv_assemble; UNSUPPORTED for S > 64 or a key row
- * (Hkv * D * element size) that is not 32 bytes times a power of two up to
- * 64 (64 bytes .. 2 KiB). */
+ * (Hkv * D * element size) that is not 32 bytes times a power of two, or is
+ * larger than 2 KiB. */
 int rc_kv_assemble_vref(const rc_shape* shape, const rc_pool* pools, int32_t n_pools,
                         const rc_segment* segs, int32_t S, const void* k_fresh,
                         const void* v_fresh, const float* rope_cos, const float* rope_sin,

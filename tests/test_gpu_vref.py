@@ -121,7 +121,7 @@ def test_vref_chain_small(name, pct):
         say(f"  {assert_attn_close(g, np.concatenate(ref), cfg.dtype, 'vref attention')}")
 
 
-@pytest.mark.parametrize("cid,stride", [(2, 16), (4, 16), (5, 64)])
+@pytest.mark.parametrize("cid,stride", [(2, 16), (3, 32), (4, 16), (5, 64)])
 def test_vref_chain_full_workloads(cid, stride):
     """Full sizes at 15% recompute, in the launch configuration the benchmark
     times: the chain is bit-identical to the assembled one, K against the
@@ -189,6 +189,31 @@ def test_vref_unresolved_positions_point_at_fresh_rows():
     mask = np.ones_like(got, dtype=bool)
     mask[0, dst:dst + ln] = False
     np.testing.assert_array_equal(got[mask], good[mask])
+
+
+def test_vref_fp32_gather_and_patch_exact_attention_rejected():
+    """The tiny fp32 workload (workload 1): the gather and the patch through
+    references work for any dtype and match the assembled chain; the
+    attention through references is bf16-only and says so."""
+    cfg = inputs.WORKLOADS[1]
+    w = inputs.make(cfg, 1001, device=DEV)
+    segs = ops.prepare_segments(w.segs, cfg.N, w.pools, DEV)
+    cos, sin = ops.rope_table(cfg.N, cfg.D, cfg.rope_base, DEV)
+    sc_a = torch.empty((cfg.B, cfg.N), dtype=torch.float32, device=DEV)
+    k_asm, v_asm = ops.kv_assemble(w.pools, segs, w.k_fresh, w.v_fresh, cos, sin, scores_out=sc_a)
+    rows_a, _ = ops.select_tokens(segs, cfg.k, w.k_fresh, w.v_fresh, k_asm, v_asm, scores_in=sc_a)
+    sc_r = torch.empty_like(sc_a)
+    k_ref, v_ref = ops.kv_assemble_vref(w.pools, segs, w.k_fresh, w.v_fresh, cos, sin, scores_out=sc_r)
+    rows_r, _ = ops.select_tokens_vref(segs, cfg.k, w.k_fresh, w.v_fresh, k_ref, v_ref, scores_in=sc_r)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(sc_r.cpu().numpy(), sc_a.cpu().numpy())
+    rows = rows_r.cpu().numpy()
+    np.testing.assert_array_equal(rows, rows_a.cpu().numpy())
+    np.testing.assert_array_equal(H(k_ref), H(k_asm))
+    np.testing.assert_array_equal(v_ref.cpu().numpy(), expected_vref(w, rows))
+    with pytest.raises(_lib.RcError) as e:
+        ops.selective_attention_vref(w.q, k_ref, v_ref, rows_r)
+    assert e.value.status == _lib.RC_ERR_UNSUPPORTED
 
 
 def test_vref_rejects_unsupported_shapes():

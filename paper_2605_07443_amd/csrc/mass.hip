@@ -14,6 +14,10 @@
 //     position on) stream through LDS in double-buffered tiles of 128 with
 //     their lse. Every wave multiplies its keys with every tile, turns the
 //     scores into weights and adds them to per-lane key sums.
+//   * A tile's 8 blocks of 16 query vectors are software-pipelined: the
+//     scores of block nb + 1 are issued on the matrix cores while the vector
+//     ALU turns block nb into weights (interleaved one product to three
+//     vector instructions), with two score sets in registers.
 //   * Each key's sum is finished inside one wave (16-lane shuffles), so no
 //     atomics are needed and the result is deterministic.
 //   * Workgroups of one group run on one XCD (ids are dealt round-robin over
@@ -33,6 +37,14 @@ constexpr int kQV = 128;        // query vectors per staged tile
 constexpr int kMassXcds = 8;
 
 using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
+
+template <int I, int M, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < M) {
+    f(std::integral_constant<int, I>{});
+    static_for<I + 1, M>(f);
+  }
+}
 
 // Q tile rows padded to 16 mod 256 bytes: the B-operand reads (16 bytes from
 // 16 consecutive rows per quarter-wave) are then conflict-free. Declared
@@ -144,30 +156,54 @@ void mass_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict
     const int cur = t & 1;
     const int p0 = p_begin + t * QP;
     __builtin_amdgcn_s_setprio(1);
-#pragma unroll 2
-    for (int nb = 0; nb < NB; ++nb) {
-      f32x4 s[4];
+    // scores of block nb + 1 on the matrix cores while the vector ALU turns
+    // block nb into weights (two score sets in flight)
+    f32x4 sa[4], sb[4];
+    auto scores = [&](f32x4 (&sc)[4], int nb) __attribute__((always_inline)) {
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) s[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int kb = 0; kb < 4; ++kb) sc[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int dc = 0; dc < DC; ++dc) {
         const bf16x8 bq = __builtin_bit_cast(
             bf16x8, *reinterpret_cast<const u32x4*>(&sm.q[cur][nb * 16 + c16][dc * 32 + q4 * 8]));
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb)
-          s[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kb][dc], bq, s[kb], 0, 0, 0);
+          sc[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kb][dc], bq, sc[kb], 0, 0, 0);
       }
+    };
+    auto weights = [&](f32x4 (&sc)[4], int nb) __attribute__((always_inline)) {
       const float l2 = sm.lse2[cur][nb * 16 + c16];
       const int pq = p0 + ((nb * 16 + c16) >> g_shift);  // position of this column's vector
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          float w = __builtin_amdgcn_exp2f(fmaf(s[kb][i], scale_log2e, -l2));
+          float w = __builtin_amdgcn_exp2f(fmaf(sc[kb][i], scale_log2e, -l2));
           if constexpr (MASK) w = (j0 + kb * 16 + q4 * 4 + i <= pq) ? w : 0.f;
           acc[kb][i] += w;
         }
+    };
+    auto interleave = [&]() __attribute__((always_inline)) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 2 * DC, 0);
+      static_for<0, 4 * DC>([&](auto) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+      });
+    };
+    scores(sa, 0);
+#pragma unroll 1
+    for (int nb = 0; nb < NB - 2; nb += 2) {
+      scores(sb, nb + 1);
+      weights(sa, nb);
+      interleave();
+      scores(sa, nb + 2);
+      weights(sb, nb + 1);
+      interleave();
     }
+    scores(sb, NB - 1);
+    weights(sa, NB - 2);
+    interleave();
+    weights(sb, NB - 1);
     __builtin_amdgcn_s_setprio(0);
     if (t + 1 < n_qt) {
       store_tile(cur ^ 1);

@@ -71,6 +71,9 @@ def parse_args():
                     help="value rows: copied into the assembled V (copy) or read through a table "
                          "of row addresses (vref); auto: vref where the library supports it "
                          "(bf16, D = 128, at most 64 segments per request), else copy")
+    ap.add_argument("--no-two-streams", action="store_true",
+                    help="skip the two-stream pipelined context leg (its kernels overlap, so a "
+                         "kernel-trace profile would mix their durations into the headline's)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (HBM counter calibration)")
     return ap.parse_args()
@@ -689,7 +692,8 @@ def main():
                       "value": round(B * R / (c["ms_per_step"] * 1e-3), 1),
                       "kernels": c["kernels"],
                       "vref_speedup": round(c["ms_per_step"] / ms_per_step, 3)}
-    two = time_two_streams(cfg, k, batches, cos, sin, args.steps, args.warmup, vref)
+    two = None if args.no_two_streams else time_two_streams(cfg, k, batches, cos, sin, args.steps,
+                                                             args.warmup, vref)
     if two is not None:
         two["vs_one_stream"] = round(ms_per_step / two["ms_per_step"], 3)
     traffic = None

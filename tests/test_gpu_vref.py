@@ -121,6 +121,27 @@ def test_vref_chain_small(name, pct):
         say(f"  {assert_attn_close(g, np.concatenate(ref), cfg.dtype, 'vref attention')}")
 
 
+def test_vref_chain_single_partial_tile():
+    """A prompt shorter than one key tile (N = 40): the attention's only tile
+    is partial and takes its V rows through the table too."""
+    cfg = inputs.Config("short-bf16", "bf16", B=3, Hq=8, Hkv=2, D=128, rope_base=500000.0, F=8,
+                        hist_len=16, hist_pool=3, n_items=1, item_len=16, item_pool=4, pct=40)
+    assert cfg.N < 64
+    w = inputs.make(cfg, 77, device=DEV)
+    r = run_both(cfg, w, cfg.k)
+    rows = check_against_assembled(w, r)
+    ocos, osin = O.rope_table(cfg.N, cfg.D, cfg.rope_base)
+    subpools, segs_sub = inputs.referenced_subpools(w)
+    kf, vf = H(w.k_fresh), H(w.v_fresh)
+    ka_o, va_o = O.assemble(kf, vf, subpools, segs_sub, ocos, osin)
+    kp_o, vp_o = O.patch(w.segs.numpy(), rows, kf, vf, ka_o, va_o)
+    np.testing.assert_array_equal(H(r["k_ref"]), kp_o)
+    sel = sample_rows(cfg.B, rows.shape[1], 1)
+    ref = oracle_attention_rows(H(w.q), kp_o, vp_o, rows, sel)
+    g = np.concatenate([H(r["out_r"])[b, idx] for b, idx in enumerate(sel)])
+    assert_attn_close(g, np.concatenate(ref), cfg.dtype, "vref attention, one partial tile")
+
+
 @pytest.mark.parametrize("cid,stride", [(2, 16), (3, 32), (4, 16), (5, 64)])
 def test_vref_chain_full_workloads(cid, stride):
     """Full sizes at 15% recompute, in the launch configuration the benchmark

@@ -121,6 +121,27 @@ def test_vref_chain_small(name, pct):
         say(f"  {assert_attn_close(g, np.concatenate(ref), cfg.dtype, 'vref attention')}")
 
 
+@pytest.mark.parametrize("Hq,Hkv", [(8, 1), (16, 1)])
+def test_vref_chain_one_kv_head(Hq, Hkv):
+    """One KV head (a key row of 256 bytes): the wave gather then owns 8
+    positions per wave and writes 8 table entries per wave."""
+    cfg = inputs.Config(f"mqa{Hq}-bf16", "bf16", B=2, Hq=Hq, Hkv=Hkv, D=128, rope_base=500000.0,
+                        F=9, hist_len=70, hist_pool=3, n_items=4, item_len=33, item_pool=6, pct=25)
+    w = inputs.make(cfg, 55 + Hq, device=DEV)
+    r = run_both(cfg, w, cfg.k)
+    rows = check_against_assembled(w, r)
+    ocos, osin = O.rope_table(cfg.N, cfg.D, cfg.rope_base)
+    subpools, segs_sub = inputs.referenced_subpools(w)
+    kf, vf = H(w.k_fresh), H(w.v_fresh)
+    ka_o, va_o = O.assemble(kf, vf, subpools, segs_sub, ocos, osin)
+    kp_o, vp_o = O.patch(w.segs.numpy(), rows, kf, vf, ka_o, va_o)
+    np.testing.assert_array_equal(H(r["k_ref"]), kp_o)
+    sel = sample_rows(cfg.B, rows.shape[1], 1)
+    ref = oracle_attention_rows(H(w.q), kp_o, vp_o, rows, sel)
+    g = np.concatenate([H(r["out_r"])[b, idx] for b, idx in enumerate(sel)])
+    assert_attn_close(g, np.concatenate(ref), cfg.dtype, f"vref attention, Hq={Hq}, one KV head")
+
+
 def test_vref_chain_single_partial_tile():
     """A prompt shorter than one key tile (N = 40): the attention's only tile
     is partial and takes its V rows through the table too."""

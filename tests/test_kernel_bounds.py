@@ -351,3 +351,38 @@ def test_gemm_split_tail_bounds(M, n, k):
     _check("reduce output", M_main * n, M_main * n + count, M * n)
     # partial bytes end before the tail rows of y begin
     assert S * count * 4 <= M_main * n * 2
+
+
+@pytest.mark.parametrize("Hkv,D,es", [(1, 128, 2), (2, 128, 2), (4, 128, 2), (8, 128, 2),
+                                      (2, 64, 2), (8, 64, 4)])
+@pytest.mark.parametrize("n", [1, 40, 64, 65, 1000, 3008])
+def test_value_reference_table_coverage(Hkv, D, es, n):
+    """The gather with V by reference: lane t < T of wave (4x + w) writes the
+    entry of position (4x + w) T + t. Every entry of [B, N] is written
+    exactly once (so that the attention never reads an unwritten address),
+    and the attention's table loads (lane l of wave w reads, for the pair of
+    tiles starting at t, the entry of key (t + (l / 16) % 2) * 64 + 16 w +
+    l % 16, clamped to N - 1) stay inside the request's N entries."""
+    row_units = Hkv * D * es // 16
+    ppr = row_units // 2
+    assert ppr & (ppr - 1) == 0 and 1 <= ppr <= 64 * WAVE_KP
+    T = (64 * WAVE_KP) // ppr
+    assert T <= 64
+    waves = ASM_THREADS // 64
+    grid_x = (n + waves * T - 1) // (waves * T)
+    hits = np.zeros(n, np.int64)
+    lane = np.arange(64)
+    for x in range(grid_x):
+        for w in range(waves):
+            i0 = (x * waves + w) * T
+            if i0 >= n:
+                continue
+            live = (lane < T) & (i0 + lane < n)
+            np.add.at(hits, (i0 + lane)[live], 1)
+    assert (hits == 1).all(), "table entries written other than once"
+    kkt = 64
+    n_kv = (n - 1) // kkt + 1
+    for t in range(0, n_kv + 1, 2):          # the prologue's pair and every even tile's
+        for w in range(4):
+            key = np.minimum((t + ((lane >> 4) & 1)) * kkt + w * 16 + (lane & 15), n - 1)
+            assert key.min() >= 0 and key.max() < n

@@ -31,6 +31,18 @@ def test_header_declarations_are_exported(lib):
         assert hasattr(lib, name), name
 
 
+def test_binding_argument_counts_match_header(lib):
+    """Every ctypes binding passes as many arguments as its header
+    declaration has parameters."""
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    decls = re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?(rc_\w+)\s*\(([^)]*)\)\s*;", text, re.M)
+    assert {name for name, _ in decls} == set(_lib.EXPORTS)
+    for name, params in decls:
+        p = params.strip()
+        n = 0 if p in ("", "void") else p.count(",") + 1
+        assert len(getattr(lib, name).argtypes) == n, name
+
+
 def test_status_strings(lib):
     assert _lib.status_string(0) == "RC_OK"
     assert _lib.status_string(-1) == "RC_ERR_INVALID_ARG"

@@ -437,6 +437,25 @@ def test_eight_pools_in_one_request(dtype, D, Hq):
         assert torch.equal(a.scores, p.scores)
         assert torch.equal(a.rows, p.rows)
         assert torch.equal(a.out, p.out), "paged attention differs from the assembled path"
+    if dtype == "bf16" and D == 128:
+        # V by reference over the same eight pools: identical outputs, and
+        # every table entry the address of the row the copy would have taken
+        r = ops.selective_prefill_vref(q, kf, vf, pools, segs, k, cos, sin)
+        torch.cuda.synchronize()
+        assert torch.equal(r.scores, a.scores) and torch.equal(r.rows, a.rows)
+        assert torch.equal(r.k_asm, a.k_asm)
+        assert torch.equal(r.out, a.out), "attention through V references differs"
+        row_bytes = Hkv * D * 2
+        fresh = vf.data_ptr() + row_bytes * np.arange(B * N, dtype=np.int64).reshape(B, N)
+        want = fresh.copy()
+        for b in range(B):
+            for dst, ln, pool, blk in segs_h[b].tolist():
+                if pool >= 0:
+                    pv = pools[pool][1]
+                    want[b, dst:dst + ln] = (pv.data_ptr() + (blk * pv.shape[1]) * row_bytes
+                                             + row_bytes * np.arange(ln, dtype=np.int64))
+            want[b, rows[b]] = fresh[b, rows[b]]
+        np.testing.assert_array_equal(r.v_ref.cpu().numpy(), want)
 
 
 # ------------------------------------------------- cache misses, bad row lists
